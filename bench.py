@@ -1,0 +1,305 @@
+#!/usr/bin/env python3
+"""CompAct layer benchmark: fwd + bwd + Adam step over every linear layer of a
+synthetic model-shaped workload, on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload llama-350m]
+
+One step = compact_fwd over all layers, compact_bwd over all layers (reverse
+order), compact_step over all layers, on synthetic inputs resident in HBM.
+Prints ONE JSON line: tokens/s, the MFMA roofline fraction of the dominant
+kernel (the fused forward GEMM), per-phase timings, activation bytes saved and
+the CPU oracle's throughput on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_traffic.json")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama-350m")
+    ap.add_argument("--fwd-mode", choices=["panel", "lds"], default="panel",
+                    help="panel: P^T panel in workspace; lds: P tiles regenerated in LDS")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=4096,
+                    help="token slice for the oracle timing (GEMM cost is linear in tokens)")
+    ap.add_argument("--reseed-period", type=int, default=50)
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2410_15352_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+class Model:
+    """Device buffers of every CompAct linear layer of a workload."""
+
+    def __init__(self, wl, fwd_mode):
+        import torch
+        import paper_2410_15352_amd as cp
+        from synthetic import bf16_bits, bf16_round
+        self.wl, self.cp, self.torch = wl, cp, torch
+        dev = torch.device("cuda:0")
+        T = wl.tokens
+        assert wl.dtype == "bf16", "the benchmark workloads are bf16"
+
+        def ld8(c):
+            return (c + 7) // 8 * 8
+
+        def dev_bf16(a, ld):
+            rows, cols = a.shape
+            buf = np.zeros((rows, ld), np.uint16)
+            buf[:, :cols] = bf16_bits(a)
+            return torch.from_numpy(buf.view(np.int16)).view(torch.bfloat16).to(dev)[:, :cols]
+
+        def rng(seed):
+            return np.random.Generator(np.random.PCG64(seed))
+
+        # one activation / gradient / output buffer per distinct width (values
+        # do not affect timing); everything per layer is separate
+        self.x, self.dy, self.y, self.dx = {}, {}, {}, {}
+        for L in wl.layers:
+            if L.n not in self.x:
+                self.x[L.n] = dev_bf16(bf16_round(rng(1234 + L.n).standard_normal((T, L.n), np.float32)), ld8(L.n))
+                self.dx[L.n] = torch.empty(T, ld8(L.n), dtype=torch.bfloat16, device=dev)[:, :L.n]
+            if L.m not in self.dy:
+                self.dy[L.m] = dev_bf16(bf16_round(0.01 * rng(4321 + L.m).standard_normal((T, L.m), np.float32)), ld8(L.m))
+                self.y[L.m] = torch.empty(T, ld8(L.m), dtype=torch.bfloat16, device=dev)[:, :L.m]
+        self.W, self.z, self.G, self.M, self.V = [], [], [], [], []
+        for L in wl.layers:
+            g = rng(1234 + L.layer_id)
+            self.W.append(dev_bf16(bf16_round(0.02 * g.standard_normal((L.n, L.m), np.float32)), ld8(L.m)))
+            self.z.append(torch.empty(T, ld8(L.r), dtype=torch.bfloat16, device=dev)[:, :L.r])
+            self.G.append(torch.empty(L.r, L.m, dtype=torch.float32, device=dev))
+            self.M.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
+            self.V.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
+        wf = max(cp.fwd_workspace_bytes(L.n, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
+        wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
+        wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
+        self.ws_f = torch.zeros(wf, dtype=torch.uint8, device=dev) if wf else None
+        self.ws_b = torch.zeros(wb, dtype=torch.uint8, device=dev)
+        self.ws_s = torch.zeros(wsz, dtype=torch.uint8, device=dev)
+        self.seeds = [L.seed for L in wl.layers]
+        self.t = 0
+
+    def fwd(self, i):
+        L = self.wl.layers[i]
+        self.cp.compact_fwd(self.x[L.n], self.W[i], self.y[L.m], self.z[i], self.seeds[i], ws=self.ws_f)
+
+    def bwd(self, i):
+        L = self.wl.layers[i]
+        self.cp.compact_bwd(self.dy[L.m], self.W[i], self.z[i], self.dx[L.n], self.G[i], ws=self.ws_b)
+
+    def upd(self, i, t):
+        wl = self.wl
+        self.cp.compact_step(self.W[i], self.G[i], self.M[i], self.V[i], self.seeds[i], t, wl.lr,
+                             wl.beta1, wl.beta2, wl.eps, wl.alpha, ws=self.ws_s)
+
+    def step(self, reseed_period):
+        self.t += 1
+        n = len(self.wl.layers)
+        for i in range(n):
+            self.fwd(i)
+        for i in reversed(range(n)):
+            self.bwd(i)
+        for i in range(n):
+            self.upd(i, self.t)
+        for i in range(n):
+            self.seeds[i] = self.cp.compact_next_seed(self.seeds[i], self.t, reseed_period)
+
+
+def algorithmic(wl):
+    """Per-step algorithmic work (sums over layers), per the kernel inventory."""
+    T = wl.tokens
+    f = dict(fwd=0.0, dx=0.0, ghat=0.0, dec=0.0)
+    b = dict(fwd=0.0, dx=0.0, ghat=0.0, adam=0.0, dec=0.0)
+    for L in wl.layers:
+        n, m, r = L.n, L.m, L.r
+        f["fwd"] += 2.0 * T * n * (m + r)
+        f["dx"] += 2.0 * T * n * m
+        f["ghat"] += 2.0 * T * r * m
+        f["dec"] += 2.0 * n * r * m
+        b["fwd"] += 2.0 * (T * n + n * m + T * m + T * r)
+        b["dx"] += 2.0 * (T * m + n * m + T * n)
+        b["ghat"] += 2.0 * (T * r + T * m) + 4.0 * r * m
+        b["adam"] += 22.0 * r * m
+        b["dec"] += 4.0 * n * m + 2.0 * r * m
+    return f, b
+
+
+def time_phases(model, torch, reps=2):
+    """Per-phase GPU time (ms per step) with HIP events on the launch stream."""
+    n = len(model.wl.layers)
+    stream = torch.cuda.current_stream()
+    out = {}
+    phases = {
+        "fwd": lambda: [model.fwd(i) for i in range(n)],
+        "bwd_dx": lambda: [model.cp.compact_bwd(model.dy[L.m], model.W[i], None, model.dx[L.n], None)
+                           for i, L in enumerate(model.wl.layers)],
+        "bwd_ghat": lambda: [model.cp.compact_bwd(model.dy[L.m], None, model.z[i], None, model.G[i],
+                                                  ws=model.ws_b) for i, L in enumerate(model.wl.layers)],
+        "step": lambda: [model.upd(i, max(model.t, 1)) for i in range(n)],
+    }
+    for name, fn in phases.items():
+        fn()  # warm
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        out[name] = e0.elapsed_time(e1) / reps
+    return out
+
+
+def cpu_baseline(wl, t_slice):
+    """The oracle (numpy fp64) timed on this host's cores on a bounded sample:
+    fwd + bwd + step of each distinct layer shape on a slice of t_slice tokens,
+    extrapolated linearly in tokens to the full step (the step is token-free)."""
+    from oracle import compact as oc
+    from synthetic import bwd_inputs, fwd_inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    counts = {}
+    for L in wl.layers:
+        counts[(L.n, L.m, L.r)] = counts.get((L.n, L.m, L.r), 0) + 1
+    total = 0.0
+    sample_secs = 0.0
+    Ts = min(t_slice, wl.tokens)
+    for (n, m, r), cnt in counts.items():
+        x, W = fwd_inputs(Ts, n, m, wl.dtype, data_seed=1)
+        dy, _, _ = bwd_inputs(Ts, n, m, r, wl.dtype, data_seed=1)
+        t0 = time.perf_counter()
+        _, z = oc.ref_fwd(x, W, 1 << 32, r)
+        _, G = oc.ref_bwd(dy, z, W)
+        t1 = time.perf_counter()
+        oc.ref_step(W, G, np.zeros_like(G), np.zeros_like(G), 1 << 32, r, 1, wl.lr, wl.beta1,
+                    wl.beta2, wl.eps, wl.alpha)
+        t2 = time.perf_counter()
+        sample_secs += t2 - t0
+        total += cnt * ((t1 - t0) * wl.tokens / Ts + (t2 - t1))
+    return {
+        "value": wl.tokens / total,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"numpy fp64 oracle, fwd+bwd+step of each of {len(counts)} distinct layer shapes "
+                   f"on {Ts} tokens ({sample_secs:.1f} s), extrapolated linearly in tokens to "
+                   f"{wl.tokens} tokens x {len(wl.layers)} layers"),
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "single-GPU build: this benchmark runs on exactly one GPU "
+                                   "(no collectives); rerun with --gpus 1"}), flush=True)
+        sys.exit(2)
+    import torch
+    import paper_2410_15352_amd as cp
+    from oracle import compact as oc  # noqa: F401  (cpu_baseline leg only)
+    from synthetic import workload
+
+    cp.library()  # fails loudly when the HIP library is missing
+    wl = workload(args.workload)
+    T = wl.tokens
+    print(f"[bench] workload {wl.name}: {len(wl.layers)} layers, {T} tokens; allocating", file=sys.stderr, flush=True)
+    model = Model(wl, args.fwd_mode)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        model.step(args.reseed_period)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        model.step(args.reseed_period)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    phases = time_phases(model, torch)
+    flops, bytes_ = algorithmic(wl)
+    fwd_tflops = flops["fwd"] / (phases["fwd"] * 1e-3) / 1e12
+    gemm_ms = phases["fwd"] + phases["bwd_dx"] + phases["bwd_ghat"]
+    gemm_frac = (flops["fwd"] + flops["dx"] + flops["ghat"]) / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+    upd_gbs = (bytes_["adam"] + bytes_["dec"]) / (phases["step"] * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        rec = json.load(open(TRAFFIC_FILE))
+        if rec.get("src_hash") == kernel_source_hash() and rec.get("workload") == wl.name:
+            traffic = rec.get("bytes_per_launch")
+    nl = len(wl.layers)
+    roofline = {
+        "bound": "mfma", "kernel": "k_fwd_bf16 (fused [y|z] = x[W|P], incl. its P^T panel launch)",
+        "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+        "flops_per_launch": flops["fwd"] / nl,
+        "avg_launch_ms": phases["fwd"] / nl,
+    }
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, args.cpu_tokens)
+    act = [{"layer": L.name, "n": L.n, "r": L.r, "saved_bytes": 2 * T * L.r, "uncompressed_bytes": 2 * T * L.n}
+           for L in wl.distinct_shapes()]
+    line = {
+        "metric": "CompAct linear fwd+bwd+step tokens/s, % bf16 MFMA peak, LLaMA-350M shapes",
+        "value": round(T / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.description, "tokens_per_step": T, "layers": nl,
+                   "fwd_mode": args.fwd_mode, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "phases_ms": {k: round(v, 4) for k, v in phases.items()},
+        "gemm_phases_mfma_frac": round(gemm_frac, 4),
+        "update_phase_hbm_GBs": round(upd_gbs, 1),
+        "update_phase_hbm_frac": round(upd_gbs / PEAK_HBM_GBS, 4),
+        "activation_bytes_per_layer": act,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

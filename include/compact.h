@@ -1,0 +1,191 @@
+/*
+ * compact.h — C ABI of the CompAct compressed linear layer on AMD MI355X (gfx950).
+ *
+ * CompAct (Shamshoum et al., "CompAct: Compressed Activations for
+ * Memory-Efficient LLM Training") replaces the activation a linear layer saves
+ * for its backward pass, x in R^{T x n} (T = b*l tokens), by the projection
+ * z = x P in R^{T x r}, where P in R^{n x r} is a Gaussian random matrix with
+ * entries N(0, 1/r) drawn from a per-layer seed and never stored (§3.2, §3.3).
+ * The weight gradient is then computed compressed, G^ = z^T dL/do (r x m),
+ * Adam runs on r x m moments, and the update is decompressed as P N (§3.2,
+ * Alg. 1-3).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - All matrices are row-major with an explicit leading dimension (ld, in
+ *    elements).  W is n x m as in the paper (input features by output
+ *    features), NOT the out x in layout of torch.nn.Linear.
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    allocates nothing and frees nothing.  Scratch memory comes from a
+ *    caller-provided workspace whose size is given by the matching
+ *    *_workspace_bytes function.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Every call is asynchronous and ordered on that stream; the call returns
+ *    after the launches are enqueued.
+ *  - dtype COMPACT_BF16: x, W, y, z, dL/do, dx are bfloat16, stored as 16-bit
+ *    patterns; accumulation is fp32 (MFMA); results are rounded to nearest-even.
+ *    The compressed gradient G^ and the Adam moments M, V are always fp32.
+ *    dtype COMPACT_F32: every tensor is fp32.
+ *  - Alignment: tensor base pointers must be 16-byte aligned; bf16 leading
+ *    dimensions must be multiples of 8 and fp32 leading dimensions multiples
+ *    of 4 (rows start on 16-byte boundaries).  A row of n = 5461 bf16 values,
+ *    for instance, needs ld >= 5464.
+ *  - Errors: every entry point validates its arguments on the host before any
+ *    launch and returns a compact_status; nothing is launched when the result
+ *    is not COMPACT_OK.  A failed launch returns COMPACT_EHIP.  A fault while a
+ *    kernel runs surfaces at the caller's next synchronisation.  The library
+ *    never aborts, throws or prints; compact_last_error() gives a description
+ *    of the last failure on the calling thread.
+ *  - Projection: the caller passes the same seed to compact_fwd and to
+ *    compact_step of the same iteration (Alg. 1 and Alg. 3 re-sample P from
+ *    the layer seed); compact_bwd needs no seed (Alg. 2 uses only z and W).
+ */
+#ifndef COMPACT_H_
+#define COMPACT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COMPACT_OK = 0,
+  COMPACT_EINVAL = -1,        /* bad size, pointer, rank or hyper-parameter */
+  COMPACT_EALIGN = -2,        /* pointer or leading dimension misaligned    */
+  COMPACT_EUNSUPPORTED = -3,  /* valid request this build does not support  */
+  COMPACT_EWORKSPACE = -4,    /* workspace missing or too small             */
+  COMPACT_EHIP = -5           /* a HIP runtime call or launch failed        */
+} compact_status;
+
+typedef enum { COMPACT_F32 = 0, COMPACT_BF16 = 1 } compact_dtype;
+
+typedef enum {
+  COMPACT_PROJ_GAUSSIAN = 0, /* P = G / sqrt(r), G the seeded N(0,1) stream  */
+  COMPACT_PROJ_IDENTITY = 1  /* P = I (requires r == n): uncompressed layer  */
+} compact_proj;
+
+/*
+ * Forward pass, Alg. 1:  y = x W  and  z = x P.
+ *
+ *   x  [tokens x n]  (ld ldx)  input activations
+ *   W  [n x m]       (ld ldw)  weight
+ *   y  [tokens x m]  (ld ldy)  output o = x W
+ *   z  [tokens x r]  (ld ldz)  compressed activation saved for the backward pass
+ *   seed  layer seed; P[i][j] = G(seed, i, j) / sqrt(r) (the P stream, below)
+ *   proj  COMPACT_PROJ_GAUSSIAN, or COMPACT_PROJ_IDENTITY with r == n
+ *   ws, ws_bytes  optional workspace.  With at least
+ *         compact_fwd_workspace_bytes(n, r, dtype) bytes the bf16 path first
+ *         writes this call's P^T panel (r x n bf16) into it and the fused GEMM
+ *         reads it from cache; with ws == NULL the fused GEMM regenerates every
+ *         P tile in LDS.  Both give bitwise identical y and z.  The panel is
+ *         scratch: it is dead when the call's kernels have finished.
+ * Requirements: tokens >= 0, n >= 1, m >= 1, 1 <= r <= n.
+ */
+int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy,
+                void* z, int64_t ldz, int64_t tokens, int64_t n, int64_t m, int64_t r,
+                uint64_t seed, int proj, int dtype, void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_fwd_workspace_bytes(int64_t n, int64_t r, int dtype);
+
+/*
+ * Backward pass, Alg. 2:  G^ = z^T dL/do  and  dx = dL/do W^T.
+ *
+ *   dy [tokens x m]  (ld lddy)  gradient of the loss with respect to y
+ *   W  [n x m]       (ld ldw)
+ *   z  [tokens x r]  (ld ldz)   the activation saved by compact_fwd
+ *   dx [tokens x n]  (ld lddx)  input gradient (exact: it does not involve P);
+ *                               may be NULL to skip it (e.g. the first layer)
+ *   G  [r x m] fp32, dense (ld = m): compressed weight gradient; may be NULL
+ *                               to skip it (not both NULL)
+ *   ws, ws_bytes  workspace of at least
+ *         compact_bwd_workspace_bytes(tokens, n, m, r, dtype) bytes for the
+ *         split-K partial sums of G^ (bf16 path; the sum over tokens is split
+ *         and reduced in a fixed order, so G^ is deterministic).
+ */
+int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
+                int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
+                int64_t m, int64_t r, int dtype, void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype);
+
+/*
+ * Optimizer step, Alg. 3 (Adam on the compressed gradient, then decompression):
+ *
+ *   M <- b1 M + (1 - b1) G^,   V <- b2 V + (1 - b2) G^2     (stored uncorrected)
+ *   N  = (M / (1 - b1^t)) / (sqrt(V / (1 - b2^t)) + eps)
+ *   W <- W - lr * alpha * P N,  P re-sampled from `seed` (same as the forward)
+ *
+ *   W  [n x m] (ld ldw)  updated in place; w_dtype COMPACT_BF16 or COMPACT_F32
+ *                        (fp32 master weights; allowed with either dtype)
+ *   G  [r x m] fp32 dense   compressed gradient from compact_bwd
+ *   M, V [r x m] fp32 dense Adam moments, updated in place (zero before t = 1)
+ *   t     1-based step index used in the bias correction (t >= 1)
+ *   lr, beta1, beta2, eps, alpha   Adam hyper-parameters and the scale alpha
+ *         (0 <= beta < 1, eps > 0, lr >= 0), as doubles: 1 - beta, the bias
+ *         corrections 1 - beta^t and lr alpha / sqrt(r) are formed in fp64 on
+ *         the host and rounded once to fp32 (rounding beta2 = 0.999 to fp32
+ *         first would move 1 - beta2 by 1.3e-5 relative)
+ *   dtype compute type of the decompression P N: COMPACT_BF16 (bf16 P and N,
+ *         MFMA, fp32 accumulate) or COMPACT_F32
+ *   ws, ws_bytes  workspace of at least compact_step_workspace_bytes(n, m, r,
+ *         dtype) bytes (holds N between the two kernels)
+ * The seed schedule of Alg. 3 (t <- t+1, new seed every T steps) is host logic:
+ * compact_next_seed.
+ */
+int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n,
+                 int64_t m, int64_t r, uint64_t seed, int64_t t, double lr, double beta1,
+                 double beta2, double eps, double alpha, int proj, int dtype, int w_dtype,
+                 void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_step_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype);
+
+/*
+ * The P stream (§3.3: P sampled from the layer seed, re-sampled with the same
+ * seed, never stored), exported for tests: writes the UNSCALED normals
+ * G(seed, i, j), 0 <= i < n, 0 <= j < r, as fp32 into out [n x r] (ld >= r,
+ * device pointer).  P = G / sqrt(r).
+ *
+ * Definition: key = (seed mod 2^32, seed >> 32); counter = (i >> 2, j, 0, 0);
+ * (w0, w1, w2, w3) = Philox4x32-10(counter, key) [Salmon et al., SC'11];
+ * (a, b) = (w0, w1) for rows 4p, 4p+1 and (w2, w3) for rows 4p+2, 4p+3;
+ * Box-Muller with radius sqrt(-2 ln u), u = (2 (a >> 9) + 1) 2^-24, and angle
+ * 2 pi ((b >> 8) + 1/2) 2^-24; even rows take the cosine, odd rows the sine.
+ * ln, sin and cos are fixed fp32 series (atanh series, Taylor series), so the
+ * stream is reproducible bit for bit on any IEEE fp32 machine.
+ */
+int compact_pstream(uint64_t seed, int64_t n, int64_t r, float* out, int64_t ld, void* stream);
+
+/*
+ * Test export: the Box-Muller step of the P stream applied to arbitrary word
+ * pairs, g_even[e] = rho(a[e]) cos(theta(b[e])), g_odd[e] = rho(a[e]) sin(theta(b[e])),
+ * for 0 <= e < count (all device pointers, count >= 0).  Lets a test sweep every
+ * radius and angle code exhaustively.
+ */
+int compact_pstream_boxmuller(const uint32_t* a, const uint32_t* b, float* g_even, float* g_odd,
+                              int64_t count, void* stream);
+
+/*
+ * Seed schedule, end of Alg. 3: after step t (1-based) taken with `seed`,
+ * returns the seed of step t+1: seed + 1 when T > 0 and t mod T == 0, else
+ * seed (T <= 0: never re-sample).  Host-only, no GPU work.
+ */
+uint64_t compact_next_seed(uint64_t seed, int64_t t, int64_t T);
+
+/* Activation elements saved per layer (Table 1): tokens * r, against tokens * n. */
+int64_t compact_saved_activation_elems(int64_t tokens, int64_t n, int64_t r);
+
+const char* compact_status_string(int status);
+
+/* Description of the last failure on the calling thread ("" if none). */
+const char* compact_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int compact_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COMPACT_H_ */

@@ -1,0 +1,160 @@
+"""CompAct compressed linear layer on AMD MI355X (gfx950).
+
+A thin Python binding over the C ABI of ``libcompact.so`` (include/compact.h):
+the functions below only translate torch tensors into device pointers, leading
+dimensions and the current HIP stream, call the library, and raise on a
+non-zero status.  All arithmetic runs in the library's HIP kernels; there is
+no fallback path.
+
+    compact_fwd   Alg. 1: y = x W, z = x P          (CompAct, §3.2)
+    compact_bwd   Alg. 2: G^ = z^T dy, dx = dy W^T
+    compact_step  Alg. 3: Adam on r x m moments, W -= lr alpha P N
+    compact_pstream      the seeded projection stream (unscaled normals)
+    compact_next_seed    the Alg. 3 seed schedule
+"""
+from __future__ import annotations
+
+from . import _lib
+
+F32, BF16 = 0, 1
+PROJ = {"gaussian": 0, "identity": 1}
+
+__all__ = ["compact_fwd", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
+           "compact_pstream_boxmuller",
+           "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
+           "saved_activation_elems", "CompactError", "library", "F32", "BF16"]
+
+
+class CompactError(RuntimeError):
+    def __init__(self, fn, status):
+        lib = _lib.load()
+        msg = lib.compact_status_string(status).decode()
+        detail = lib.compact_last_error().decode()
+        super().__init__(f"{fn}: {msg} ({status}): {detail}")
+        self.status = status
+
+
+def library():
+    return _lib.load()
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _ld(t):
+    if t is None:
+        return 0
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a 2-D tensor with unit column stride")
+    return t.stride(0)
+
+
+def _stream(stream, ref):
+    import torch
+    if stream is not None:
+        return stream
+    return torch.cuda.current_stream(ref.device).cuda_stream
+
+
+def _ws(ws):
+    if ws is None:
+        return None, 0
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def _check(fn, status):
+    if status != 0:
+        raise CompactError(fn, status)
+
+
+def fwd_workspace_bytes(n, r, dtype=BF16):
+    return int(_lib.load().compact_fwd_workspace_bytes(n, r, dtype))
+
+
+def bwd_workspace_bytes(tokens, n, m, r, dtype=BF16):
+    return int(_lib.load().compact_bwd_workspace_bytes(tokens, n, m, r, dtype))
+
+
+def step_workspace_bytes(n, m, r, dtype=BF16):
+    return int(_lib.load().compact_step_workspace_bytes(n, m, r, dtype))
+
+
+def saved_activation_elems(tokens, n, r):
+    return int(_lib.load().compact_saved_activation_elems(tokens, n, r))
+
+
+def compact_fwd(x, W, y, z, seed, proj="gaussian", ws=None, stream=None):
+    """y = x W and z = x P (Alg. 1).  x (T, n), W (n, m), y (T, m), z (T, r)."""
+    lib = _lib.load()
+    T, n = x.shape
+    m = W.shape[1]
+    r = z.shape[1]
+    wp, wb = _ws(ws)
+    st = lib.compact_fwd(_ptr(x), _ld(x), _ptr(W), _ld(W), _ptr(y), _ld(y), _ptr(z), _ld(z),
+                         T, n, m, r, int(seed) & (2**64 - 1), PROJ[proj], _dtype_code(x),
+                         wp, wb, _stream(stream, x))
+    _check("compact_fwd", st)
+
+
+def compact_bwd(dy, W, z, dx, G, ws=None, stream=None):
+    """G^ = z^T dy (fp32, r x m) and dx = dy W^T (Alg. 2).  dx or G may be None."""
+    lib = _lib.load()
+    T, m = dy.shape
+    r = z.shape[1] if z is not None else (G.shape[0] if G is not None else 1)
+    n = W.shape[0] if W is not None else (dx.shape[1] if dx is not None else r)
+    if G is not None and (not G.is_contiguous() or tuple(G.shape) != (r, m)):
+        raise ValueError("G must be a contiguous (r, m) fp32 tensor")
+    wp, wb = _ws(ws)
+    st = lib.compact_bwd(_ptr(dy), _ld(dy), _ptr(W), _ld(W), _ptr(z), _ld(z), _ptr(dx), _ld(dx),
+                         _ptr(G), T, n, m, r, _dtype_code(dy), wp, wb, _stream(stream, dy))
+    _check("compact_bwd", st)
+
+
+def compact_step(W, G, M, V, seed, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, alpha=1.0,
+                 proj="gaussian", dtype=None, ws=None, stream=None):
+    """Adam on the compressed gradient and W -= lr alpha P N (Alg. 3), in place."""
+    lib = _lib.load()
+    n, m = W.shape
+    r = G.shape[0]
+    for name, t_ in (("G", G), ("M", M), ("V", V)):
+        if not t_.is_contiguous() or tuple(t_.shape) != (r, m):
+            raise ValueError(f"{name} must be a contiguous (r, m) fp32 tensor")
+    w_code = _dtype_code(W)
+    d_code = w_code if dtype is None else {"bf16": BF16, "f32": F32}[dtype]
+    wp, wb = _ws(ws)
+    st = lib.compact_step(_ptr(W), _ld(W), _ptr(G), _ptr(M), _ptr(V), n, m, r,
+                          int(seed) & (2**64 - 1), int(t), float(lr), float(beta1), float(beta2),
+                          float(eps), float(alpha), PROJ[proj], d_code, w_code, wp, wb,
+                          _stream(stream, W))
+    _check("compact_step", st)
+
+
+def compact_pstream(seed, out, stream=None):
+    """Fill out (n, r) fp32 with the unscaled stream G(seed, i, j)."""
+    lib = _lib.load()
+    n, r = out.shape
+    st = lib.compact_pstream(int(seed) & (2**64 - 1), n, r, _ptr(out), _ld(out),
+                             _stream(stream, out))
+    _check("compact_pstream", st)
+
+
+def compact_pstream_boxmuller(a, b, g_even, g_odd, stream=None):
+    """Box-Muller step of the stream on word pairs (int32 tensors viewed as uint32)."""
+    lib = _lib.load()
+    st = lib.compact_pstream_boxmuller(_ptr(a), _ptr(b), _ptr(g_even), _ptr(g_odd), a.numel(),
+                                       _stream(stream, a))
+    _check("compact_pstream_boxmuller", st)
+
+
+def compact_next_seed(seed, t, T):
+    return int(_lib.load().compact_next_seed(int(seed) & (2**64 - 1), int(t), int(T)))

@@ -1,0 +1,463 @@
+// Host side of the C ABI declared in include/compact.h: argument validation,
+// workspace sizing and kernel launches.  See the header for the contract.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/compact.h"
+#include "kernels_bf16.hpp"
+#include "kernels_common.hpp"
+
+using namespace compact;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return COMPACT_OK;
+}
+
+int check_launch(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(COMPACT_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return COMPACT_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t elem_size(int dtype) { return dtype == COMPACT_BF16 ? 2 : 4; }
+
+bool valid_dtype(int d) { return d == COMPACT_F32 || d == COMPACT_BF16; }
+
+// Leading-dimension rule: ld >= cols and rows start on 16-byte boundaries.
+int check_matrix(const char* name, const void* p, int64_t ld, int64_t cols, int dtype) {
+  if (p == nullptr) return fail(COMPACT_EINVAL, "%s is NULL", name);
+  if (ld < cols) return fail(COMPACT_EINVAL, "%s: ld %lld < columns %lld", name, (long long)ld, (long long)cols);
+  if (!aligned16(p)) return fail(COMPACT_EALIGN, "%s: pointer not 16-byte aligned", name);
+  const int64_t q = dtype == COMPACT_BF16 ? 8 : 4;
+  if (ld % q != 0) return fail(COMPACT_EALIGN, "%s: ld %lld not a multiple of %lld", name, (long long)ld, (long long)q);
+  return COMPACT_OK;
+}
+
+int check_dense(const char* name, const void* p) {
+  if (p == nullptr) return fail(COMPACT_EINVAL, "%s is NULL", name);
+  if (!aligned16(p)) return fail(COMPACT_EALIGN, "%s: pointer not 16-byte aligned", name);
+  return COMPACT_OK;
+}
+
+int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
+  if (tokens < 0 || n < 1 || m < 1) return fail(COMPACT_EINVAL, "bad shape tokens=%lld n=%lld m=%lld", (long long)tokens, (long long)n, (long long)m);
+  if (r < 1 || r > n) return fail(COMPACT_EINVAL, "rank r=%lld must satisfy 1 <= r <= n=%lld", (long long)r, (long long)n);
+  if (proj != COMPACT_PROJ_GAUSSIAN && proj != COMPACT_PROJ_IDENTITY) return fail(COMPACT_EINVAL, "unknown projection %d", proj);
+  if (proj == COMPACT_PROJ_IDENTITY && r != n) return fail(COMPACT_EINVAL, "identity projection needs r == n (r=%lld, n=%lld)", (long long)r, (long long)n);
+  if (n > (int64_t(1) << 31) || r > (int64_t(1) << 31)) return fail(COMPACT_EUNSUPPORTED, "n and r must be below 2^31");
+  return COMPACT_OK;
+}
+
+constexpr size_t kWsAlign = 256;
+
+// Tile shapes of the bf16 kernels.
+constexpr int kBM = 128, kBN = 128, kWGM = 2, kWGN = 2;
+constexpr int kThreads = kWGM * kWGN * kWave;
+constexpr size_t kGemmLds = 2u * (kBM + kBN) * kBK * sizeof(uint16_t);
+
+// Split-K plan for G^ = z^T dL/do (K = tokens).
+struct SplitPlan {
+  int tiles_r, tiles_m, splits;
+  int64_t split_len;
+};
+
+SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
+  SplitPlan s;
+  s.tiles_r = static_cast<int>(ceil_div(r, kBM));
+  s.tiles_m = static_cast<int>(ceil_div(m, kBN));
+  const int64_t tiles = int64_t(s.tiles_r) * s.tiles_m;
+  const int64_t ktiles = ceil_div(tokens > 0 ? tokens : 1, kBK);
+  int64_t splits = ceil_div(512, tiles);
+  if (splits < 1) splits = 1;
+  if (splits > ktiles) splits = ktiles;
+  s.split_len = ceil_div(ktiles, splits) * kBK;
+  s.splits = static_cast<int>(ceil_div(tokens > 0 ? tokens : 1, s.split_len));
+  return s;
+}
+
+size_t ghat_ws_bytes(int64_t tokens, int64_t r, int64_t m) {
+  const SplitPlan s = ghat_plan(tokens, r, m);
+  return size_t(s.splits) * size_t(s.tiles_r) * kBM * size_t(s.tiles_m) * kBN * sizeof(float);
+}
+
+int64_t pt_ld(int64_t n) { return round_up(n, kBK); }
+int64_t n_ld(int64_t m) { return round_up(m, 8); }
+
+float inv_sqrt_rank(int64_t r, int proj) {
+  return proj == COMPACT_PROJ_IDENTITY ? 1.0f : static_cast<float>(1.0 / std::sqrt(static_cast<double>(r)));
+}
+
+int set_lds(const void* fn, size_t bytes) {
+  if (bytes <= 65536) return COMPACT_OK;
+  const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
+  if (e != hipSuccess) return fail(COMPACT_EHIP, "hipFuncSetAttribute(%zu B LDS): %s", bytes, hipGetErrorString(e));
+  return COMPACT_OK;
+}
+
+__global__ void k_fill_f32(float* p, int64_t count, float v) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e < count) p[e] = v;
+}
+
+int launch_gemm_f32(const GemmF32Params& gp, hipStream_t s, const char* what) {
+  GemmF32Params p = gp;
+  const int64_t tm = ceil_div(p.M, 64), tn = ceil_div(p.N, 64);
+  if (tm == 0 || tn == 0) return COMPACT_OK;
+  p.tiles_n = static_cast<int>(tn);
+  hipLaunchKernelGGL(k_gemm_f32, dim3(static_cast<uint32_t>(tm * tn)), dim3(256), 0, s, p);
+  return check_launch(what);
+}
+
+OperandF32 mem_operand(const float* p, int64_t su, int64_t sv, int64_t U, int64_t V) {
+  OperandF32 o{};
+  o.p = p;
+  o.su = su;
+  o.sv = sv;
+  o.U = U;
+  o.V = V;
+  return o;
+}
+
+OperandF32 pgen_operand(uint64_t seed, int64_t n, int64_t r, int proj) {
+  OperandF32 o{};
+  o.pgen = 1;
+  o.identity = proj == COMPACT_PROJ_IDENTITY;
+  o.key = philox_key(seed);
+  o.U = n;
+  o.V = r;
+  return o;
+}
+
+}  // namespace
+
+extern "C" {
+
+int compact_version(void) { return 100; }
+
+const char* compact_last_error(void) { return g_last_error.c_str(); }
+
+const char* compact_status_string(int status) {
+  switch (status) {
+    case COMPACT_OK: return "ok";
+    case COMPACT_EINVAL: return "invalid argument";
+    case COMPACT_EALIGN: return "misaligned pointer or leading dimension";
+    case COMPACT_EUNSUPPORTED: return "unsupported configuration";
+    case COMPACT_EWORKSPACE: return "workspace missing or too small";
+    case COMPACT_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+uint64_t compact_next_seed(uint64_t seed, int64_t t, int64_t T) {
+  if (T > 0 && t >= 1 && t % T == 0) return seed + 1u;
+  return seed;
+}
+
+int64_t compact_saved_activation_elems(int64_t tokens, int64_t n, int64_t r) {
+  (void)n;
+  return tokens * r;
+}
+
+size_t compact_fwd_workspace_bytes(int64_t n, int64_t r, int dtype) {
+  if (dtype != COMPACT_BF16 || n < 1 || r < 1) return 0;
+  return size_t(r) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
+}
+
+size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype) {
+  (void)n;
+  if (dtype != COMPACT_BF16 || tokens < 0 || m < 1 || r < 1) return 0;
+  return ghat_ws_bytes(tokens, r, m) + kWsAlign;
+}
+
+size_t compact_step_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
+  (void)n;
+  if (m < 1 || r < 1) return 0;
+  return size_t(r) * size_t(n_ld(m)) * elem_size(dtype) + kWsAlign;
+}
+
+static void* align_ws(void* ws) {
+  const uintptr_t a = (reinterpret_cast<uintptr_t>(ws) + kWsAlign - 1) & ~uintptr_t(kWsAlign - 1);
+  return reinterpret_cast<void*>(a);
+}
+
+int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy,
+                void* z, int64_t ldz, int64_t tokens, int64_t n, int64_t m, int64_t r,
+                uint64_t seed, int proj, int dtype, void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
+  if ((st = check_shape(tokens, n, m, r, proj))) return st;
+  if ((st = check_matrix("x", x, ldx, n, dtype))) return st;
+  if ((st = check_matrix("W", W, ldw, m, dtype))) return st;
+  if ((st = check_matrix("y", y, ldy, m, dtype))) return st;
+  if ((st = check_matrix("z", z, ldz, r, dtype))) return st;
+  if (ws != nullptr && ws_bytes < compact_fwd_workspace_bytes(n, r, dtype))
+    return fail(COMPACT_EWORKSPACE, "forward workspace %zu B < %zu B", ws_bytes, compact_fwd_workspace_bytes(n, r, dtype));
+  if (tokens == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float zscale = inv_sqrt_rank(r, proj);
+  const int identity = proj == COMPACT_PROJ_IDENTITY;
+
+  if (dtype == COMPACT_F32) {
+    GemmF32Params gp{};
+    gp.A = mem_operand(static_cast<const float*>(x), ldx, 1, tokens, n);
+    gp.B = mem_operand(static_cast<const float*>(W), ldw, 1, n, m);
+    gp.M = tokens; gp.N = m; gp.K = n; gp.mode = 0;
+    gp.out = static_cast<float*>(y); gp.ldo = ldy; gp.scale = 1.0f;
+    if ((st = launch_gemm_f32(gp, s, "forward y (fp32)"))) return st;
+    gp.B = pgen_operand(seed, n, r, proj);
+    gp.N = r; gp.out = static_cast<float*>(z); gp.ldo = ldz; gp.scale = zscale;
+    if ((st = launch_gemm_f32(gp, s, "forward z (fp32)"))) return st;
+    return ok();
+  }
+
+  FwdParams p{};
+  p.x = static_cast<const uint16_t*>(x); p.ldx = ldx;
+  p.W = static_cast<const uint16_t*>(W); p.ldw = ldw;
+  p.y = static_cast<uint16_t*>(y); p.ldy = ldy;
+  p.z = static_cast<uint16_t*>(z); p.ldz = ldz;
+  p.T = tokens; p.n = n; p.m = m; p.r = r;
+  p.key = philox_key(seed);
+  p.identity = identity;
+  p.zscale = zscale;
+  p.tiles_y = static_cast<int>(ceil_div(m, kBN));
+  p.tiles_z = static_cast<int>(ceil_div(r, kBN));
+  if (ws != nullptr) {
+    uint16_t* pt = static_cast<uint16_t*>(align_ws(ws));
+    const int64_t ld = pt_ld(n);
+    const int64_t quads = (ld / 4) * r;
+    hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0, s,
+                       p.key, n, r, identity, pt, ld);
+    if ((st = check_launch("P panel (bf16)"))) return st;
+    p.pt = pt;
+    p.ldpt = ld;
+  }
+  const int64_t blocks = ceil_div(tokens, kBM) * (p.tiles_y + p.tiles_z);
+  if (blocks > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
+  hipLaunchKernelGGL((k_fwd_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
+                     kGemmLds, s, p);
+  if ((st = check_launch("fused forward (bf16)"))) return st;
+  return ok();
+}
+
+int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
+                int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
+                int64_t m, int64_t r, int dtype, void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
+  if ((st = check_shape(tokens, n, m, r, COMPACT_PROJ_GAUSSIAN))) return st;
+  if (dx == nullptr && G == nullptr) return fail(COMPACT_EINVAL, "dx and G are both NULL");
+  if ((st = check_matrix("dy", dy, lddy, m, dtype))) return st;
+  if (dx != nullptr) {
+    if ((st = check_matrix("W", W, ldw, m, dtype))) return st;
+    if ((st = check_matrix("dx", dx, lddx, n, dtype))) return st;
+  }
+  if (G != nullptr) {
+    if ((st = check_matrix("z", z, ldz, r, dtype))) return st;
+    if ((st = check_dense("G", G))) return st;
+    const size_t need = compact_bwd_workspace_bytes(tokens, n, m, r, dtype);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+      return fail(COMPACT_EWORKSPACE, "backward workspace %zu B < %zu B", ws_bytes, need);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (tokens == 0) {
+    if (G != nullptr) {
+      hipLaunchKernelGGL(k_fill_f32, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s, G, r * m, 0.0f);
+      if ((st = check_launch("zero G"))) return st;
+    }
+    return ok();
+  }
+
+  if (dtype == COMPACT_F32) {
+    if (dx != nullptr) {
+      GemmF32Params gp{};
+      gp.A = mem_operand(static_cast<const float*>(dy), lddy, 1, tokens, m);
+      gp.B = mem_operand(static_cast<const float*>(W), 1, ldw, m, n);
+      gp.M = tokens; gp.N = n; gp.K = m; gp.mode = 0;
+      gp.out = static_cast<float*>(dx); gp.ldo = lddx; gp.scale = 1.0f;
+      if ((st = launch_gemm_f32(gp, s, "dx (fp32)"))) return st;
+    }
+    if (G != nullptr) {
+      GemmF32Params gp{};
+      gp.A = mem_operand(static_cast<const float*>(z), 1, ldz, r, tokens);
+      gp.B = mem_operand(static_cast<const float*>(dy), lddy, 1, tokens, m);
+      gp.M = r; gp.N = m; gp.K = tokens; gp.mode = 0;
+      gp.out = G; gp.ldo = m; gp.scale = 1.0f;
+      if ((st = launch_gemm_f32(gp, s, "G^ (fp32)"))) return st;
+    }
+    return ok();
+  }
+
+  if (dx != nullptr) {
+    DxParams p{};
+    p.dy = static_cast<const uint16_t*>(dy); p.lddy = lddy;
+    p.W = static_cast<const uint16_t*>(W); p.ldw = ldw;
+    p.dx = static_cast<uint16_t*>(dx); p.lddx = lddx;
+    p.T = tokens; p.n = n; p.m = m;
+    p.tiles_n = static_cast<int>(ceil_div(n, kBN));
+    const int64_t blocks = ceil_div(tokens, kBM) * p.tiles_n;
+    hipLaunchKernelGGL((k_dx_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
+                       kGemmLds, s, p);
+    if ((st = check_launch("dx (bf16)"))) return st;
+  }
+  if (G != nullptr) {
+    const SplitPlan sp = ghat_plan(tokens, r, m);
+    GhatParams p{};
+    p.z = static_cast<const uint16_t*>(z); p.ldz = ldz;
+    p.dy = static_cast<const uint16_t*>(dy); p.lddy = lddy;
+    p.part = static_cast<float*>(align_ws(ws));
+    p.T = tokens; p.r = r; p.m = m;
+    p.tiles_r = sp.tiles_r; p.tiles_m = sp.tiles_m; p.splits = sp.splits; p.split_len = sp.split_len;
+    const int64_t blocks = int64_t(sp.tiles_r) * sp.tiles_m * sp.splits;
+    hipLaunchKernelGGL((k_ghat_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
+                       kGemmLds, s, p);
+    if ((st = check_launch("G^ split-K (bf16)"))) return st;
+    const int64_t ldp = int64_t(sp.tiles_m) * kBN, plane = int64_t(sp.tiles_r) * kBM * ldp;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s,
+                       static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
+    if ((st = check_launch("G^ reduce"))) return st;
+  }
+  return ok();
+}
+
+int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n,
+                 int64_t m, int64_t r, uint64_t seed, int64_t t, double lr, double beta1,
+                 double beta2, double eps, double alpha, int proj, int dtype, int w_dtype,
+                 void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (!valid_dtype(dtype) || !valid_dtype(w_dtype)) return fail(COMPACT_EINVAL, "unknown dtype");
+  if ((st = check_shape(0, n, m, r, proj))) return st;
+  if ((st = check_matrix("W", W, ldw, m, w_dtype))) return st;
+  if ((st = check_dense("G", G)) || (st = check_dense("M", M)) || (st = check_dense("V", V))) return st;
+  if (t < 1) return fail(COMPACT_EINVAL, "step index t=%lld must be >= 1", (long long)t);
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+    return fail(COMPACT_EINVAL, "betas must lie in [0, 1)");
+  if (!(eps > 0.0) || !std::isfinite(eps)) return fail(COMPACT_EINVAL, "eps must be > 0");
+  if (!(lr >= 0.0) || !std::isfinite(lr) || !std::isfinite(alpha)) return fail(COMPACT_EINVAL, "bad lr or alpha");
+  if (dtype == COMPACT_F32 && w_dtype != COMPACT_F32)
+    return fail(COMPACT_EUNSUPPORTED, "fp32 decompression needs fp32 W");
+  const size_t need = compact_step_workspace_bytes(n, m, r, dtype);
+  if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "step workspace %zu B < %zu B", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  void* Nbuf = align_ws(ws);
+  const int64_t ldn = n_ld(m);
+
+  AdamParams ap{};
+  ap.G = G; ap.M = M; ap.V = V; ap.N = Nbuf; ap.ldn = ldn;
+  ap.n_f32 = dtype == COMPACT_F32;
+  ap.r = r; ap.m = m;
+  ap.b1 = static_cast<float>(beta1);
+  ap.b2 = static_cast<float>(beta2);
+  ap.omb1 = static_cast<float>(1.0 - beta1);
+  ap.omb2 = static_cast<float>(1.0 - beta2);
+  ap.bc1 = static_cast<float>(1.0 - std::pow(beta1, static_cast<double>(t)));
+  ap.bc2 = static_cast<float>(1.0 - std::pow(beta2, static_cast<double>(t)));
+  ap.eps = static_cast<float>(eps);
+  {
+    int64_t blocks = ceil_div(r * m, 256);
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(k_adam, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, ap);
+    if ((st = check_launch("Adam"))) return st;
+  }
+  const double coef64 = lr * alpha *
+                        (proj == COMPACT_PROJ_IDENTITY ? 1.0 : 1.0 / std::sqrt(static_cast<double>(r)));
+  const float coef = static_cast<float>(coef64);
+
+  if (dtype == COMPACT_F32) {
+    GemmF32Params gp{};
+    gp.A = pgen_operand(seed, n, r, proj);
+    gp.B = mem_operand(static_cast<const float*>(Nbuf), ldn, 1, r, m);
+    gp.M = n; gp.N = m; gp.K = r; gp.mode = 1;
+    gp.out = static_cast<float*>(W); gp.ldo = ldw; gp.coef = coef;
+    if ((st = launch_gemm_f32(gp, s, "decompress (fp32)"))) return st;
+    return ok();
+  }
+
+  DecParams p{};
+  p.W = W; p.ldw = ldw; p.w_f32 = w_dtype == COMPACT_F32;
+  p.N = static_cast<const uint16_t*>(Nbuf); p.ldn = ldn;
+  p.n = n; p.m = m; p.r = r;
+  p.r_pad = round_up(r, kBK);
+  p.key = philox_key(seed);
+  p.identity = proj == COMPACT_PROJ_IDENTITY;
+  p.coef = coef;
+  p.tiles_m = static_cast<int>(ceil_div(m, 128));
+  const size_t tiles_lds = 2u * 128 * kBK * sizeof(uint16_t);
+  const size_t panel64 = size_t(64) * (p.r_pad + 8) * sizeof(uint16_t);
+  const size_t panel32 = size_t(32) * (p.r_pad + 8) * sizeof(uint16_t);
+  const size_t lds_limit = 160 * 1024;
+  if (panel64 + tiles_lds <= 100 * 1024) {
+    p.panels = static_cast<int>(ceil_div(n, 64));
+    int64_t groups = ceil_div(1024, p.panels);
+    if (groups > p.tiles_m) groups = p.tiles_m;
+    if (groups < 1) groups = 1;
+    p.col_groups = static_cast<int>(groups);
+    const size_t lds = panel64 + tiles_lds;
+    auto fn = k_decompress_bf16<64, 128, 2, 2>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
+    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(int64_t(p.panels) * p.col_groups)), dim3(256), lds, s, p);
+    if ((st = check_launch("decompress (bf16, 64-row panels)"))) return st;
+  } else if (panel32 + tiles_lds <= lds_limit) {
+    p.panels = static_cast<int>(ceil_div(n, 32));
+    int64_t groups = ceil_div(1024, p.panels);
+    if (groups > p.tiles_m) groups = p.tiles_m;
+    if (groups < 1) groups = 1;
+    p.col_groups = static_cast<int>(groups);
+    const size_t lds = panel32 + tiles_lds;
+    auto fn = k_decompress_bf16<32, 128, 1, 4>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
+    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(int64_t(p.panels) * p.col_groups)), dim3(256), lds, s, p);
+    if ((st = check_launch("decompress (bf16, 32-row panels)"))) return st;
+  } else {
+    return fail(COMPACT_EUNSUPPORTED, "rank r=%lld too large for the resident projection panel", (long long)r);
+  }
+  return ok();
+}
+
+int compact_pstream(uint64_t seed, int64_t n, int64_t r, float* out, int64_t ld, void* stream) {
+  if (n < 1 || r < 1) return fail(COMPACT_EINVAL, "bad shape n=%lld r=%lld", (long long)n, (long long)r);
+  if (out == nullptr) return fail(COMPACT_EINVAL, "out is NULL");
+  if (ld < r) return fail(COMPACT_EINVAL, "ld < r");
+  if (n > (int64_t(1) << 31) || r > (int64_t(1) << 31)) return fail(COMPACT_EUNSUPPORTED, "n and r must be below 2^31");
+  const int64_t quads = ceil_div(n, 4) * r;
+  hipLaunchKernelGGL(k_pstream_f32, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), philox_key(seed), n, r, out, ld);
+  int st;
+  if ((st = check_launch("P stream"))) return st;
+  return ok();
+}
+
+int compact_pstream_boxmuller(const uint32_t* a, const uint32_t* b, float* g_even, float* g_odd,
+                              int64_t count, void* stream) {
+  if (count < 0) return fail(COMPACT_EINVAL, "count < 0");
+  if (count == 0) return ok();
+  if (!a || !b || !g_even || !g_odd) return fail(COMPACT_EINVAL, "NULL pointer");
+  if (count > (int64_t(1) << 40)) return fail(COMPACT_EUNSUPPORTED, "count too large");
+  hipLaunchKernelGGL(k_boxmuller, dim3(static_cast<uint32_t>(ceil_div(count, 256))), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), a, b, g_even, g_odd, count);
+  int st;
+  if ((st = check_launch("Box-Muller"))) return st;
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,338 @@
+// bf16 kernels of the CompAct layer (gfx950, MFMA 32x32x16, fp32 accumulate).
+//
+//   k_fwd_bf16          [y | z] = x [W | P]     (CompAct Alg. 1)
+//   k_pstream_t_bf16    P^T panel (r x n, bf16, unscaled) for the forward
+//   k_dx_bf16           dx = dL/do W^T          (Alg. 2, second line)
+//   k_ghat_bf16         split-K partials of G^ = z^T dL/do (Alg. 2, first line)
+//   k_splitk_reduce     fixed-order sum of the split-K partials
+//   k_decompress_bf16   W <- W - lr alpha P N, P regenerated per row panel in
+//                       LDS (Alg. 3, decompression and update)
+#pragma once
+#include "gemm_bf16.hpp"
+
+namespace compact {
+
+// ------------------------------- forward -----------------------------------
+struct FwdParams {
+  const uint16_t* x;
+  int64_t ldx;
+  const uint16_t* W;
+  int64_t ldw;
+  uint16_t* y;
+  int64_t ldy;
+  uint16_t* z;
+  int64_t ldz;
+  const uint16_t* pt;  // materialised P^T (r rows, K = n contiguous), or null
+  int64_t ldpt;
+  int64_t T, n, m, r;
+  PhiloxKey key;
+  int identity;
+  float zscale;      // fp32(1/sqrt(r)), 1 for the identity projection
+  int tiles_y;       // column tiles covering y (m columns)
+  int tiles_z;       // column tiles covering z (r columns)
+};
+
+template <int BM, int BN, int WGM, int WGN>
+__device__ __forceinline__ void store_tile_bf16(const f32x16 (&acc)[BM / WGM / 32][BN / WGN / 32],
+                                                uint16_t* out, int64_t ld, int64_t rows,
+                                                int64_t cols, int64_t row0, int64_t col0,
+                                                float scale) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
+  for_each_acc(acc, lane, [&](int row, int col, float v) {
+    const int64_t gr = r0 + row, gc = c0 + col;
+    if (gr < rows && gc < cols) out[gr * ld + gc] = f32_to_bf16(v * scale);
+  });
+}
+
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_fwd_bf16(FwdParams p) {
+  constexpr int NT = WGM * WGN * kWave;
+  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int ncols = p.tiles_y + p.tiles_z;
+  const int rt = static_cast<int>(logical / ncols), ct = static_cast<int>(logical % ncols);
+  const int64_t row0 = static_cast<int64_t>(rt) * BM;
+  KMajorLoader<BM, NT> la{p.x, p.ldx, p.T, p.n, row0};
+  f32x16 acc[FM][FN];
+  if (ct < p.tiles_y) {
+    const int64_t col0 = static_cast<int64_t>(ct) * BN;
+    MNMajorLoader<BN, NT> lb{p.W, p.ldw, p.m, p.n, col0};
+    gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
+    store_tile_bf16<BM, BN, WGM, WGN>(acc, p.y, p.ldy, p.T, p.m, row0, col0, 1.0f);
+  } else {
+    const int64_t col0 = static_cast<int64_t>(ct - p.tiles_y) * BN;
+    if (p.pt != nullptr) {
+      KMajorLoader<BN, NT> lb{p.pt, p.ldpt, p.r, p.n, col0};
+      gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
+    } else {
+      PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.identity};
+      gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
+    }
+    store_tile_bf16<BM, BN, WGM, WGN>(acc, p.z, p.ldz, p.T, p.r, row0, col0, p.zscale);
+  }
+}
+
+// P^T panel for the forward: out[j * ld + i] = bf16(G[i][j]) (unscaled), or the
+// identity.  One thread per quad (4 rows of one column); columns i >= n of the
+// padded rows are written as zero.
+__global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identity,
+                                 uint16_t* out, int64_t ld) {
+  const int64_t quads_per_row = ld / 4;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (q >= quads_per_row * r) return;
+  const int64_t j = q / quads_per_row, i0 = (q % quads_per_row) * 4;
+  float g[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i0 < n) {
+    if (identity) {
+      for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
+    } else {
+      pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
+    }
+    for (int e = 0; e < 4; ++e)
+      if (i0 + e >= n) g[e] = 0.0f;
+  }
+  u32x2 v;
+  v.x = pack_bf16x2(g[0], g[1]);
+  v.y = pack_bf16x2(g[2], g[3]);
+  *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
+}
+
+// Unscaled fp32 stream G (n x r, leading dimension ld): the standalone P tile
+// generator, exported for bitwise tests.
+__global__ void k_pstream_f32(PhiloxKey key, int64_t n, int64_t r, float* out, int64_t ld) {
+  const int64_t nq = (n + 3) / 4;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (q >= nq * r) return;
+  const int64_t p = q % nq, j = q / nq;
+  float g[4];
+  pstream_quad(key, static_cast<uint32_t>(p), static_cast<uint32_t>(j), g);
+  for (int e = 0; e < 4; ++e) {
+    const int64_t i = 4 * p + e;
+    if (i < n) out[i * ld + j] = g[e];
+  }
+}
+
+__global__ void k_boxmuller(const uint32_t* a, const uint32_t* b, float* ge, float* go,
+                            int64_t count) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= count) return;
+  float g0, g1;
+  pstream_pair(a[e], b[e], g0, g1);
+  ge[e] = g0;
+  go[e] = g1;
+}
+
+// ------------------------------- backward ----------------------------------
+struct DxParams {
+  const uint16_t* dy;
+  int64_t lddy;
+  const uint16_t* W;
+  int64_t ldw;
+  uint16_t* dx;
+  int64_t lddx;
+  int64_t T, n, m;
+  int tiles_n;
+};
+
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_dx_bf16(DxParams p) {
+  constexpr int NT = WGM * WGN * kWave;
+  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int rt = static_cast<int>(logical / p.tiles_n), ct = static_cast<int>(logical % p.tiles_n);
+  const int64_t row0 = static_cast<int64_t>(rt) * BM, col0 = static_cast<int64_t>(ct) * BN;
+  KMajorLoader<BM, NT> la{p.dy, p.lddy, p.T, p.m, row0};
+  KMajorLoader<BN, NT> lb{p.W, p.ldw, p.n, p.m, col0};
+  f32x16 acc[FM][FN];
+  gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.m, lds, acc);
+  store_tile_bf16<BM, BN, WGM, WGN>(acc, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
+}
+
+struct GhatParams {
+  const uint16_t* z;
+  int64_t ldz;
+  const uint16_t* dy;
+  int64_t lddy;
+  float* part;        // [splits][tiles_r * BM][tiles_m * BN]
+  int64_t T, r, m;
+  int tiles_r, tiles_m, splits;
+  int64_t split_len;  // tokens per split, a multiple of 64
+};
+
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_ghat_bf16(GhatParams p) {
+  constexpr int NT = WGM * WGN * kWave;
+  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int tiles = p.tiles_r * p.tiles_m;
+  const int split = static_cast<int>(logical / tiles), tile = static_cast<int>(logical % tiles);
+  const int rt = tile / p.tiles_m, ct = tile % p.tiles_m;
+  const int64_t row0 = static_cast<int64_t>(rt) * BM, col0 = static_cast<int64_t>(ct) * BN;
+  const int64_t k_begin = split * p.split_len;
+  const int64_t k_end = k_begin + p.split_len < p.T ? k_begin + p.split_len : p.T;
+  MNMajorLoader<BM, NT> la{p.z, p.ldz, p.r, p.T, row0};
+  MNMajorLoader<BN, NT> lb{p.dy, p.lddy, p.m, p.T, col0};
+  f32x16 acc[FM][FN];
+  gemm_mainloop<BM, BN, WGM, WGN>(la, lb, k_begin, k_end, lds, acc);
+  const int64_t ldp = static_cast<int64_t>(p.tiles_m) * BN;
+  float* out = p.part + static_cast<int64_t>(split) * (p.tiles_r * BM) * ldp;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
+  for_each_acc(acc, lane, [&](int row, int col, float v) { out[(r0 + row) * ldp + c0 + col] = v; });
+}
+
+// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c].
+__global__ void k_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t plane,
+                                int64_t r, int64_t m, float* G) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= r * m) return;
+  const int64_t j = e / m, c = e % m;
+  const float* src = part + j * ldp + c;
+  float s = 0.0f;
+  for (int k = 0; k < splits; ++k) s += src[k * plane];
+  G[e] = s;
+}
+
+// ------------------------------- update ------------------------------------
+struct DecParams {
+  void* W;              // bf16 or fp32, n x m
+  int64_t ldw;
+  int w_f32;
+  const uint16_t* N;    // r x m, bf16, leading dimension ldn (multiple of 8)
+  int64_t ldn;
+  int64_t n, m, r;
+  int64_t r_pad;        // round_up(r, 64): panel columns
+  PhiloxKey key;
+  int identity;
+  float coef;           // fp32(lr * alpha / sqrt(r))
+  int panels;           // ceil(n / BM)
+  int col_groups;       // column groups per panel
+  int tiles_m;          // ceil(m / BN)
+};
+
+// Panel layout: [BM][r_pad + 8] bf16; the +8 pad puts the rows of one MFMA
+// fragment read on distinct LDS banks (r_pad / 8 is even).
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParams p) {
+  constexpr int NT = WGM * WGN * kWave;
+  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const int64_t ldp = p.r_pad + 8;
+  uint16_t* Ap = lds;
+  uint16_t* Bs[2] = {lds + BM * ldp, lds + BM * ldp + BN * kBK};
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int panel = static_cast<int>(logical % p.panels), group = static_cast<int>(logical / p.panels);
+  const int64_t row0 = static_cast<int64_t>(panel) * BM;
+
+  // 1. P panel rows row0 .. row0+BM-1, all r_pad columns, generated once.
+  {
+    const int jgroups = static_cast<int>(p.r_pad / 8);
+    const int items = (BM / 4) * jgroups;
+    for (int it = tid; it < items; it += NT) {
+      const int jg = it % jgroups, qr = it / jgroups;
+      const int64_t i0 = row0 + qr * 4, j0 = static_cast<int64_t>(jg) * 8;
+      float g[8][4];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const int64_t j = j0 + jj;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) g[jj][e] = 0.0f;
+        if (j < p.r && i0 < p.n) {
+          if (p.identity) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g[jj][e] = (i0 + e == j) ? 1.0f : 0.0f;
+          } else {
+            pstream_quad(p.key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g[jj]);
+          }
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        u32x4 v;
+        v.x = pack_bf16x2(g[0][e], g[1][e]);
+        v.y = pack_bf16x2(g[2][e], g[3][e]);
+        v.z = pack_bf16x2(g[4][e], g[5][e]);
+        v.w = pack_bf16x2(g[6][e], g[7][e]);
+        if (i0 + e >= p.n) v = u32x4{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4*>(Ap + (qr * 4 + e) * ldp + j0) = v;
+      }
+    }
+  }
+  __syncthreads();
+
+  // 2. Column tiles of this group: acc = P_panel N_tile, then W -= coef acc.
+  const int per = (p.tiles_m + p.col_groups - 1) / p.col_groups;
+  const int ct_begin = group * per;
+  const int ct_end = ct_begin + per < p.tiles_m ? ct_begin + per : p.tiles_m;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int kt_count = static_cast<int>(p.r_pad / kBK);
+  for (int ct = ct_begin; ct < ct_end; ++ct) {
+    const int64_t col0 = static_cast<int64_t>(ct) * BN;
+    MNMajorLoader<BN, NT> lb{p.N, p.ldn, p.m, p.r, col0};
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.0f;
+    lb.fetch(0, tid);
+    lb.commit(Bs[0], tid);
+    __syncthreads();
+    for (int kt = 0; kt < kt_count; ++kt) {
+      const int cur = kt & 1;
+      const bool more = kt + 1 < kt_count;
+      if (more) lb.fetch(static_cast<int64_t>(kt + 1) * kBK, tid);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        u32x4 a[FM], b[FN];
+        const int k = kk * 16 + lh * 8;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          a[fm] = *reinterpret_cast<const u32x4*>(Ap + (wm * FM * 32 + fm * 32 + lr) * ldp +
+                                                  kt * kBK + k);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+          b[fn] = *reinterpret_cast<const u32x4*>(Bs[cur] + tile_off(wn * FN * 32 + fn * 32 + lr, k));
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32x32x16(a[fm], b[fn], acc[fm][fn]);
+      }
+      if (more) lb.commit(Bs[cur ^ 1], tid);
+      __syncthreads();
+    }
+    const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
+    const float coef = p.coef;
+    if (p.w_f32) {
+      float* W = static_cast<float*>(p.W);
+      for_each_acc(acc, lane, [&](int row, int col, float v) {
+        const int64_t gr = r0 + row, gc = c0 + col;
+        if (gr < p.n && gc < p.m) {
+          const float d = coef * v;
+          W[gr * p.ldw + gc] = W[gr * p.ldw + gc] - d;
+        }
+      });
+    } else {
+      uint16_t* W = static_cast<uint16_t*>(p.W);
+      for_each_acc(acc, lane, [&](int row, int col, float v) {
+        const int64_t gr = r0 + row, gc = c0 + col;
+        if (gr < p.n && gc < p.m) {
+          const float d = coef * v;
+          const float w = bf16_to_f32(W[gr * p.ldw + gc]);
+          W[gr * p.ldw + gc] = f32_to_bf16(w - d);
+        }
+      });
+    }
+  }
+}
+
+}  // namespace compact

@@ -1,0 +1,146 @@
+"""CPU checks of the C ABI: the library loads, exports every function declared
+in include/compact.h, and its host-only logic (argument validation, workspace
+sizing, seed schedule, status strings) behaves as documented.  No call here
+reaches a kernel launch: every invalid call returns before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import compact as oc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "compact.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(compact_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2410_15352_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libcompact.so not built (run __graft_entry__.build())")
+    return _lib.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("compact_fwd", "compact_bwd", "compact_step", "compact_pstream",
+                     "compact_next_seed", "compact_fwd_workspace_bytes",
+                     "compact_bwd_workspace_bytes", "compact_step_workspace_bytes"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    from paper_2410_15352_amd import _lib
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+        assert name in _lib.SIGNATURES, f"binding lacks a signature for {name}"
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    from paper_2410_15352_amd import _lib
+    saved = _lib._lib
+    _lib._lib = None
+    try:
+        with pytest.raises(_lib.CompactLibraryMissing):
+            _lib.load(str(tmp_path / "absent.so"))
+    finally:
+        _lib._lib = saved
+
+
+def test_seed_schedule_matches_oracle(lib):
+    for seed in (0, 7 << 32, 2**64 - 1):
+        for T in (0, 1, 3, 50):
+            for t in range(1, 12):
+                assert lib.compact_next_seed(seed, t, T) == oc.next_seed(seed, t, T)
+
+
+def test_saved_activation_elems(lib):
+    me = oc.memory_elements(256, 256, 1024, 1024, 128)
+    assert lib.compact_saved_activation_elems(65536, 1024, 128) == me["compact"]["activations"]
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert lib.compact_status_string(code)
+    assert lib.compact_status_string(0) == b"ok"
+    assert lib.compact_version() >= 100
+
+
+def test_workspace_sizes(lib):
+    # P^T panel: r rows of round_up(n, 64) bf16 values (+ alignment slack)
+    assert lib.compact_fwd_workspace_bytes(1024, 128, 1) >= 128 * 1024 * 2
+    assert lib.compact_fwd_workspace_bytes(1024, 128, 0) == 0
+    assert lib.compact_bwd_workspace_bytes(65536, 1024, 1024, 128, 1) > 128 * 1024 * 4
+    assert lib.compact_step_workspace_bytes(1024, 1024, 128, 1) >= 128 * 1024 * 2
+    assert lib.compact_step_workspace_bytes(256, 512, 32, 0) >= 32 * 512 * 4
+
+
+FAKE = 0x100000  # an aligned non-NULL address; never dereferenced (validation fails first)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(r=0), -1), (dict(r=2000), -1), (dict(n=0), -1), (dict(tokens=-1), -1),
+    (dict(proj=1), -1),             # identity needs r == n
+    (dict(proj=7), -1), (dict(dtype=5), -1),
+    (dict(ldx=1000), -1),           # ld < n
+    (dict(ldx=1028), -2),           # bf16 ld not a multiple of 8
+    (dict(x=FAKE + 2), -2),         # misaligned pointer
+    (dict(x=None), -1),
+    (dict(ws=FAKE, ws_bytes=16), -4),
+])
+def test_fwd_validation(lib, kw, status):
+    a = dict(x=FAKE, ldx=1024, W=FAKE, ldw=1024, y=FAKE, ldy=1024, z=FAKE, ldz=128, tokens=64,
+             n=1024, m=1024, r=128, seed=1, proj=0, dtype=1, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    st = lib.compact_fwd(a["x"], a["ldx"], a["W"], a["ldw"], a["y"], a["ldy"], a["z"], a["ldz"],
+                         a["tokens"], a["n"], a["m"], a["r"], a["seed"], a["proj"], a["dtype"],
+                         a["ws"], a["ws_bytes"], a["stream"])
+    assert st == status
+    assert lib.compact_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dx=None, G=None), -1), (dict(ws=None), -4), (dict(ws_bytes=8), -4),
+    (dict(lddy=1020), -1), (dict(G=FAKE + 4), -2), (dict(r=1025), -1),
+])
+def test_bwd_validation(lib, kw, status):
+    a = dict(dy=FAKE, lddy=1024, W=FAKE, ldw=1024, z=FAKE, ldz=128, dx=FAKE, lddx=1024, G=FAKE,
+             tokens=4096, n=1024, m=1024, r=128, dtype=1, ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    st = lib.compact_bwd(a["dy"], a["lddy"], a["W"], a["ldw"], a["z"], a["ldz"], a["dx"], a["lddx"],
+                         a["G"], a["tokens"], a["n"], a["m"], a["r"], a["dtype"], a["ws"],
+                         a["ws_bytes"], a["stream"])
+    assert st == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(t=0), -1), (dict(beta1=1.0), -1), (dict(beta2=-0.1), -1), (dict(eps=0.0), -1),
+    (dict(lr=-1.0), -1), (dict(lr=float("nan")), -1), (dict(ws=None), -4),
+    (dict(dtype=0, w_dtype=1), -3),  # fp32 decompression into bf16 weights
+    (dict(M=None), -1), (dict(proj=1), -1),
+])
+def test_step_validation(lib, kw, status):
+    a = dict(W=FAKE, ldw=1024, G=FAKE, M=FAKE, V=FAKE, n=1024, m=1024, r=128, seed=1, t=1,
+             lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, alpha=1.0, proj=0, dtype=1, w_dtype=1,
+             ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    st = lib.compact_step(a["W"], a["ldw"], a["G"], a["M"], a["V"], a["n"], a["m"], a["r"],
+                          a["seed"], a["t"], a["lr"], a["beta1"], a["beta2"], a["eps"], a["alpha"],
+                          a["proj"], a["dtype"], a["w_dtype"], a["ws"], a["ws_bytes"], a["stream"])
+    assert st == status
+
+
+def test_pstream_validation(lib):
+    assert lib.compact_pstream(1, 0, 4, FAKE, 4, None) == -1
+    assert lib.compact_pstream(1, 4, 4, None, 4, None) == -1
+    assert lib.compact_pstream(1, 4, 4, FAKE, 2, None) == -1
+    assert lib.compact_pstream_boxmuller(None, None, None, None, 0, None) == 0
+    assert lib.compact_pstream_boxmuller(None, None, None, None, 5, None) == -1

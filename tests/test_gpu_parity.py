@@ -1,0 +1,220 @@
+"""GPU parity of the CompAct layer against the fp64 oracle.
+
+Each ABI call is checked on seeded inputs from ``synthetic`` (the oracle never
+sees a value produced on the GPU): relative Frobenius error <= 1e-5 on the fp32
+path and <= 2e-2 on the bf16 path, per output.  Shapes span several tiles and
+ragged tails in every dimension; a three-step chain checks the whole
+fwd -> bwd -> step loop (the first Adam step is sign-like, N = G^/(|G^|+eps),
+so the update of step 1 is compared only through the smooth moments).
+"""
+import numpy as np
+import pytest
+
+from oracle import compact as oc
+from synthetic import bf16_round, bwd_inputs, fwd_inputs, step_inputs, workload
+
+from gpu_util import dev, empty, ld_for, to_dev, to_np, to_np_f32, workspace
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+cp = pytest.importorskip("paper_2410_15352_amd")
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+CODE = {"f32": 0, "bf16": 1}
+
+# (tokens, n, m, r, dtype): tile multiples, ragged tails, r not a multiple of 8
+SHAPES = [
+    (256, 256, 512, 32, "f32"),          # the single fp32 layer workload
+    (100, 36, 20, 12, "f32"),
+    (300, 200, 136, 40, "bf16"),
+    (1000, 1376, 512, 344, "bf16"),
+    (513, 512, 1376, 128, "bf16"),
+    (2048, 768, 3072, 384, "bf16"),
+    (777, 1024, 2736, 128, "bf16"),
+    (128, 5461, 64, 682, "bf16"),
+]
+
+
+def _ids(s):
+    return "T{}-n{}-m{}-r{}-{}".format(*s)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("use_ws", [True, False])
+def test_forward_parity(shape, use_ws):
+    T, n, m, r, dt = shape
+    if dt == "f32" and use_ws:
+        pytest.skip("no workspace mode on the fp32 path")
+    seed = (11 << 32) | 3
+    x, W = fwd_inputs(T, n, m, dt, data_seed=T + n)
+    xd, Wd = to_dev(x, dt, ld_for(n, dt)), to_dev(W, dt, ld_for(m, dt))
+    y = empty(T, m, dt, ld_for(m, dt))
+    z = empty(T, r, dt, ld_for(r, dt))
+    ws = workspace(cp.fwd_workspace_bytes(n, r, CODE[dt])) if use_ws else None
+    cp.compact_fwd(xd, Wd, y, z, seed, ws=ws)
+    torch.cuda.synchronize()
+    y_ref, z_ref = oc.ref_fwd(x, W, seed, r)
+    assert oc.rel_fro(to_np(y), y_ref) <= TOL[dt]
+    assert oc.rel_fro(to_np(z), z_ref) <= TOL[dt]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+def test_backward_parity(shape):
+    T, n, m, r, dt = shape
+    dy, z, W = bwd_inputs(T, n, m, r, dt, data_seed=T + m)
+    dyd = to_dev(dy, dt, ld_for(m, dt))
+    zd = to_dev(z, dt, ld_for(r, dt))
+    Wd = to_dev(W, dt, ld_for(m, dt))
+    dx = empty(T, n, dt, ld_for(n, dt))
+    G = torch.empty(r, m, dtype=torch.float32, device=dev())
+    ws = workspace(cp.bwd_workspace_bytes(T, n, m, r, CODE[dt]))
+    cp.compact_bwd(dyd, Wd, zd, dx, G, ws=ws)
+    torch.cuda.synchronize()
+    dx_ref, G_ref = oc.ref_bwd(dy, z, W)
+    assert oc.rel_fro(to_np(dx), dx_ref) <= TOL[dt]
+    assert oc.rel_fro(G.cpu().numpy(), G_ref) <= TOL[dt]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("t", [1, 3])
+def test_step_parity(shape, t):
+    _, n, m, r, dt = shape
+    seed, lr, b1, b2, eps, alpha = (5 << 32) | 1, 1e-3, 0.9, 0.999, 1e-8, 0.25
+    W, G, M, V = step_inputs(n, m, r, dt, t=t, data_seed=n + r)
+    Wd = to_dev(W, "f32", ld_for(m, "f32"))     # fp32 master copy: dW is exact to fp32
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+    ws = workspace(cp.step_workspace_bytes(n, m, r, CODE[dt]))
+    cp.compact_step(Wd, Gd, Md, Vd, seed, t, lr, b1, b2, eps, alpha, dtype=dt, ws=ws)
+    torch.cuda.synchronize()
+    W_ref, M_ref, V_ref, dW_ref = oc.ref_step(W, G, M, V, seed, r, t, lr, b1, b2, eps, alpha)
+    dW = to_np_f32(Wd).astype(np.float64) - W.astype(np.float64)
+    assert oc.rel_fro(Md.cpu().numpy(), M_ref) <= TOL[dt]
+    assert oc.rel_fro(Vd.cpu().numpy(), V_ref) <= TOL[dt]
+    # fp32 W: dW is recovered from W' - W with about 1e-7 |W| / |dW| relative error
+    tol_dw = TOL[dt] if dt == "bf16" else 2e-4
+    assert oc.rel_fro(dW, dW_ref) <= tol_dw
+
+    if dt == "bf16":
+        # bf16 weights: same kernel, update rounded once to bf16 (RNE(fp32 result))
+        Wb = to_dev(W, "bf16", ld_for(m, "bf16"))
+        Gd2, Md2, Vd2 = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+        cp.compact_step(Wb, Gd2, Md2, Vd2, seed, t, lr, b1, b2, eps, alpha, dtype="bf16", ws=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_f32(Wb).view(np.uint32), bf16_round(to_np_f32(Wd)).view(np.uint32))
+        assert oc.rel_fro(to_np(Wb), W_ref) <= TOL[dt]
+
+
+def test_step_dw_fp32_exact_precision():
+    # W = 0 in fp32: W' = -fp32(coef * acc) exactly, so dW is compared without
+    # the cancellation of W' - W.
+    n, m, r = 256, 512, 32
+    _, G, M, V = step_inputs(n, m, r, "f32", t=1, data_seed=3)
+    Wd = torch.zeros(n, m, dtype=torch.float32, device=dev())
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+    ws = workspace(cp.step_workspace_bytes(n, m, r, 0))
+    cp.compact_step(Wd, Gd, Md, Vd, 1, 1, 1e-3, dtype="f32", ws=ws)
+    torch.cuda.synchronize()
+    _, _, _, dW_ref = oc.ref_step(np.zeros((n, m)), G, M, V, 1, r, 1, 1e-3, 0.9, 0.999, 1e-8, 1.0)
+    assert oc.rel_fro(Wd.cpu().numpy(), dW_ref) <= 1e-5
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_identity_projection(dt):
+    # P = I, r = n: z equals x bit for bit, and the step equals uncompressed Adam
+    T, n, m = 300, 64, 72
+    x, W = fwd_inputs(T, n, m, dt, data_seed=1)
+    xd, Wd = to_dev(x, dt), to_dev(W, dt)
+    y = empty(T, m, dt)
+    z = empty(T, n, dt)
+    cp.compact_fwd(xd, Wd, y, z, 0, proj="identity")
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(z), x.astype(np.float64))
+    Wm, G, M, V = step_inputs(n, m, n, dt, t=2, data_seed=2)
+    Wmd = to_dev(Wm, "f32")
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+    ws = workspace(cp.step_workspace_bytes(n, m, n, CODE[dt]))
+    cp.compact_step(Wmd, Gd, Md, Vd, 0, 2, 1e-2, alpha=0.5, proj="identity", dtype=dt, ws=ws)
+    torch.cuda.synchronize()
+    W_ref, M_ref, V_ref, dW_ref = oc.ref_step(Wm, G, M, V, 0, n, 2, 1e-2, 0.9, 0.999, 1e-8, 0.5,
+                                              identity=True)
+    dW = to_np_f32(Wmd).astype(np.float64) - Wm.astype(np.float64)
+    assert oc.rel_fro(dW, dW_ref) <= (TOL[dt] if dt == "bf16" else 1e-4)
+    assert oc.rel_fro(Md.cpu().numpy(), M_ref) <= TOL[dt]
+
+
+def test_outputs_independent_of_seed_and_deterministic():
+    T, n, m, r, dt = 700, 512, 1376, 128, "bf16"
+    x, W = fwd_inputs(T, n, m, dt, data_seed=9)
+    xd, Wd = to_dev(x, dt), to_dev(W, dt)
+    outs = []
+    for seed in (1, 2, 1):
+        y, z = empty(T, m, dt), empty(T, r, dt)
+        cp.compact_fwd(xd, Wd, y, z, seed)
+        outs.append((y.clone(), z.clone()))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0].view(torch.int16), outs[1][0].view(torch.int16))
+    assert not torch.equal(outs[0][1].view(torch.int16), outs[1][1].view(torch.int16))
+    assert torch.equal(outs[0][1].view(torch.int16), outs[2][1].view(torch.int16))
+    dy, _, _ = bwd_inputs(T, n, m, r, dt, data_seed=9)
+    dyd = to_dev(dy, dt)
+    ws = workspace(cp.bwd_workspace_bytes(T, n, m, r))
+    res = []
+    for z_ in (outs[0][1], outs[1][1], outs[0][1]):
+        dx = empty(T, n, dt)
+        G = torch.empty(r, m, dtype=torch.float32, device=dev())
+        cp.compact_bwd(dyd, Wd, z_, dx, G, ws=ws)
+        res.append((dx.clone(), G.clone()))
+    torch.cuda.synchronize()
+    assert torch.equal(res[0][0].view(torch.int16), res[1][0].view(torch.int16))  # dx ignores P
+    assert torch.equal(res[0][1], res[2][1])                                      # G^ deterministic
+
+
+@pytest.mark.parametrize("name", ["single-f32", "llama-60m"])
+def test_three_step_chain(name):
+    wl = workload(name)
+    L = wl.layers[0] if name == "single-f32" else wl.layers[6]  # the down projection
+    T = min(wl.tokens, 1024)
+    dt = wl.dtype
+    n, m, r, seed = L.n, L.m, L.r, L.seed
+    x0, W0 = fwd_inputs(T, n, m, dt, data_seed=100)
+    W_gpu = to_dev(W0, "f32", ld_for(m, "f32"))     # fp32 master weights
+    M = torch.zeros(r, m, dtype=torch.float32, device=dev())
+    V = torch.zeros_like(M)
+    W_ref = W0.astype(np.float64)
+    M_ref = np.zeros((r, m))
+    V_ref = np.zeros((r, m))
+    ws_b = workspace(cp.bwd_workspace_bytes(T, n, m, r, CODE[dt]))
+    ws_s = workspace(cp.step_workspace_bytes(n, m, r, CODE[dt]))
+    for t in (1, 2, 3):
+        x, _ = fwd_inputs(T, n, m, dt, data_seed=100 + t)
+        dy, _, _ = bwd_inputs(T, n, m, r, dt, data_seed=200 + t)
+        W_cmp = W_gpu if dt == "f32" else W_gpu.to(torch.bfloat16)
+        xd, dyd = to_dev(x, dt), to_dev(dy, dt)
+        y, z = empty(T, m, dt), empty(T, r, dt)
+        cp.compact_fwd(xd, W_cmp, y, z, seed)
+        dx = empty(T, n, dt)
+        G = torch.empty(r, m, dtype=torch.float32, device=dev())
+        cp.compact_bwd(dyd, W_cmp, z, dx, G, ws=ws_b)
+        W_before = W_gpu.clone()
+        cp.compact_step(W_gpu, G, M, V, seed, t, wl.lr, wl.beta1, wl.beta2, wl.eps, wl.alpha,
+                        dtype=dt, ws=ws_s)
+        torch.cuda.synchronize()
+        _, z_ref = oc.ref_fwd(x, W_ref, seed, r)
+        dx_ref, G_ref = oc.ref_bwd(dy, z_ref, W_ref)
+        W_new, M_ref, V_ref, dW_ref = oc.ref_step(W_ref, G_ref, M_ref, V_ref, seed, r, t, wl.lr,
+                                                  wl.beta1, wl.beta2, wl.eps, wl.alpha)
+        tol = TOL[dt]
+        if t == 1:  # later steps use weights that already differ by rounding
+            assert oc.rel_fro(to_np(dx), dx_ref) <= tol
+        assert oc.rel_fro(to_np(z), z_ref) <= tol
+        assert oc.rel_fro(G.cpu().numpy(), G_ref) <= tol
+        assert oc.rel_fro(M.cpu().numpy(), M_ref) <= tol
+        assert oc.rel_fro(V.cpu().numpy(), V_ref) <= tol
+        if t >= 2:
+            dW = (W_gpu - W_before).cpu().numpy().astype(np.float64)
+            assert oc.rel_fro(dW, dW_ref) <= max(tol, 2e-4)
+        W_ref = W_new
+        new_seed = oc.next_seed(seed, t, 2)  # Alg. 3: re-sample every T = 2 steps
+        assert cp.compact_next_seed(seed, t, 2) == new_seed
+        seed = new_seed
