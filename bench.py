@@ -39,9 +39,13 @@ def parse_args():
     ap.add_argument("--fwd-mode", choices=["panel", "lds"], default="panel",
                     help="panel: P^T panel in workspace; lds: P tiles regenerated in LDS")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=4096,
-                    help="token slice for the oracle timing (GEMM cost is linear in tokens)")
+    ap.add_argument("--cpu-tokens", type=int, default=1 << 30,
+                    help="token slice for the oracle timing (default: the full step)")
     ap.add_argument("--reseed-period", type=int, default=50)
+    ap.add_argument("--no-phases", action="store_true",
+                    help="skip the per-phase timing pass (for counter collection runs)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one plain copy kernel over 256 MiB first (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -177,10 +181,12 @@ def time_phases(model, torch, reps=2):
     return out
 
 
-def cpu_baseline(wl, t_slice):
+def cpu_baseline(wl, t_slice, min_secs=10.0):
     """The oracle (numpy fp64) timed on this host's cores on a bounded sample:
-    fwd + bwd + step of each distinct layer shape on a slice of t_slice tokens,
-    extrapolated linearly in tokens to the full step (the step is token-free)."""
+    fwd + bwd + step of each distinct layer shape on t_slice tokens (the full
+    step when t_slice >= tokens), repeated until min_secs of CPU work, then
+    weighted by how many layers have each shape (GEMM cost is linear in tokens,
+    the step is token-free)."""
     from oracle import compact as oc
     from synthetic import bwd_inputs, fwd_inputs
     try:
@@ -191,29 +197,38 @@ def cpu_baseline(wl, t_slice):
     counts = {}
     for L in wl.layers:
         counts[(L.n, L.m, L.r)] = counts.get((L.n, L.m, L.r), 0) + 1
-    total = 0.0
-    sample_secs = 0.0
     Ts = min(t_slice, wl.tokens)
-    for (n, m, r), cnt in counts.items():
+    inputs = {}
+    for (n, m, r) in counts:
         x, W = fwd_inputs(Ts, n, m, wl.dtype, data_seed=1)
         dy, _, _ = bwd_inputs(Ts, n, m, r, wl.dtype, data_seed=1)
-        t0 = time.perf_counter()
-        _, z = oc.ref_fwd(x, W, 1 << 32, r)
-        _, G = oc.ref_bwd(dy, z, W)
-        t1 = time.perf_counter()
-        oc.ref_step(W, G, np.zeros_like(G), np.zeros_like(G), 1 << 32, r, 1, wl.lr, wl.beta1,
-                    wl.beta2, wl.eps, wl.alpha)
-        t2 = time.perf_counter()
-        sample_secs += t2 - t0
-        total += cnt * ((t1 - t0) * wl.tokens / Ts + (t2 - t1))
+        inputs[(n, m, r)] = (x, W, dy)
+    t_tok = {k: 0.0 for k in counts}
+    t_step = {k: 0.0 for k in counts}
+    reps, spent = 0, 0.0
+    while reps == 0 or spent < min_secs:
+        for (n, m, r), (x, W, dy) in inputs.items():
+            t0 = time.perf_counter()
+            _, z = oc.ref_fwd(x, W, 1 << 32, r)
+            _, G = oc.ref_bwd(dy, z, W)
+            t1 = time.perf_counter()
+            oc.ref_step(W, G, np.zeros_like(G), np.zeros_like(G), 1 << 32, r, 1, wl.lr, wl.beta1,
+                        wl.beta2, wl.eps, wl.alpha)
+            t2 = time.perf_counter()
+            t_tok[(n, m, r)] += t1 - t0
+            t_step[(n, m, r)] += t2 - t1
+            spent += t2 - t0
+        reps += 1
+    total = sum(cnt * (t_tok[k] / reps * wl.tokens / Ts + t_step[k] / reps) for k, cnt in counts.items())
+    scaled = "" if Ts == wl.tokens else f", extrapolated linearly in tokens to {wl.tokens}"
     return {
         "value": wl.tokens / total,
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"numpy fp64 oracle, fwd+bwd+step of each of {len(counts)} distinct layer shapes "
-                   f"on {Ts} tokens ({sample_secs:.1f} s), extrapolated linearly in tokens to "
-                   f"{wl.tokens} tokens x {len(wl.layers)} layers"),
+        "sample": (f"numpy fp64 oracle: fwd+bwd+step of each of the {len(counts)} distinct layer "
+                   f"shapes at {Ts} tokens, {reps} repetition(s) ({spent:.1f} s){scaled}, "
+                   f"weighted by the layer count of each shape ({len(wl.layers)} layers)"),
     }
 
 
@@ -225,10 +240,15 @@ def main():
         sys.exit(2)
     import torch
     import paper_2410_15352_amd as cp
-    from oracle import compact as oc  # noqa: F401  (cpu_baseline leg only)
     from synthetic import workload
 
     cp.library()  # fails loudly when the HIP library is missing
+    if args.calibrate_copy:
+        a = torch.ones(64 << 20, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        torch.neg(a, out=b)  # reads 256 MiB, writes 256 MiB
+        torch.cuda.synchronize()
+        del a, b
     wl = workload(args.workload)
     T = wl.tokens
     print(f"[bench] workload {wl.name}: {len(wl.layers)} layers, {T} tokens; allocating", file=sys.stderr, flush=True)
@@ -249,6 +269,9 @@ def main():
     ms_per_step = e0.elapsed_time(e1) / args.steps
     print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
 
+    if args.no_phases:
+        print(json.dumps({"ms_per_step": ms_per_step, "tokens_per_s": T / (ms_per_step * 1e-3)}), flush=True)
+        return
     phases = time_phases(model, torch)
     flops, bytes_ = algorithmic(wl)
     fwd_tflops = flops["fwd"] / (phases["fwd"] * 1e-3) / 1e12

@@ -71,10 +71,15 @@ int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
 
 constexpr size_t kWsAlign = 256;
 
-// Tile shapes of the bf16 kernels.
-constexpr int kBM = 128, kBN = 128, kWGM = 2, kWGN = 2;
+// Tile shapes of the bf16 kernels.  Forward and dx: 256 x 256 tiles, 8 waves
+// in a 4 x 2 grid (64 x 128 per wave), two LDS stages of 64 KB.  G^: 128 x 128
+// tiles, 4 waves (r is often 128 or less).
+constexpr int kBM = 256, kBN = 256, kWGM = 4, kWGN = 2;
 constexpr int kThreads = kWGM * kWGN * kWave;
 constexpr size_t kGemmLds = 2u * (kBM + kBN) * kBK * sizeof(uint16_t);
+constexpr int kGBM = 128, kGBN = 128, kGWGM = 2, kGWGN = 2;
+constexpr int kGThreads = kGWGM * kGWGN * kWave;
+constexpr size_t kGhatLds = 2u * (kGBM + kGBN) * kBK * sizeof(uint16_t);
 
 // Split-K plan for G^ = z^T dL/do (K = tokens).
 struct SplitPlan {
@@ -84,8 +89,8 @@ struct SplitPlan {
 
 SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
   SplitPlan s;
-  s.tiles_r = static_cast<int>(ceil_div(r, kBM));
-  s.tiles_m = static_cast<int>(ceil_div(m, kBN));
+  s.tiles_r = static_cast<int>(ceil_div(r, kGBM));
+  s.tiles_m = static_cast<int>(ceil_div(m, kGBN));
   const int64_t tiles = int64_t(s.tiles_r) * s.tiles_m;
   const int64_t ktiles = ceil_div(tokens > 0 ? tokens : 1, kBK);
   int64_t splits = ceil_div(512, tiles);
@@ -98,7 +103,7 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
 
 size_t ghat_ws_bytes(int64_t tokens, int64_t r, int64_t m) {
   const SplitPlan s = ghat_plan(tokens, r, m);
-  return size_t(s.splits) * size_t(s.tiles_r) * kBM * size_t(s.tiles_m) * kBN * sizeof(float);
+  return size_t(s.splits) * size_t(s.tiles_r) * kGBM * size_t(s.tiles_m) * kGBN * sizeof(float);
 }
 
 int64_t pt_ld(int64_t n) { return round_up(n, kBK); }
@@ -254,8 +259,11 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
   }
   const int64_t blocks = ceil_div(tokens, kBM) * (p.tiles_y + p.tiles_z);
   if (blocks > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
-  hipLaunchKernelGGL((k_fwd_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
-                     kGemmLds, s, p);
+  {
+    auto fn = k_fwd_bf16<kBM, kBN, kWGM, kWGN>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), kGemmLds))) return st;
+    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), kGemmLds, s, p);
+  }
   if ((st = check_launch("fused forward (bf16)"))) return st;
   return ok();
 }
@@ -316,8 +324,9 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     p.T = tokens; p.n = n; p.m = m;
     p.tiles_n = static_cast<int>(ceil_div(n, kBN));
     const int64_t blocks = ceil_div(tokens, kBM) * p.tiles_n;
-    hipLaunchKernelGGL((k_dx_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
-                       kGemmLds, s, p);
+    auto fn = k_dx_bf16<kBM, kBN, kWGM, kWGN>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), kGemmLds))) return st;
+    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), kGemmLds, s, p);
     if ((st = check_launch("dx (bf16)"))) return st;
   }
   if (G != nullptr) {
@@ -329,10 +338,10 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     p.T = tokens; p.r = r; p.m = m;
     p.tiles_r = sp.tiles_r; p.tiles_m = sp.tiles_m; p.splits = sp.splits; p.split_len = sp.split_len;
     const int64_t blocks = int64_t(sp.tiles_r) * sp.tiles_m * sp.splits;
-    hipLaunchKernelGGL((k_ghat_bf16<kBM, kBN, kWGM, kWGN>), dim3(static_cast<uint32_t>(blocks)), dim3(kThreads),
-                       kGemmLds, s, p);
+    hipLaunchKernelGGL((k_ghat_bf16<kGBM, kGBN, kGWGM, kGWGN>), dim3(static_cast<uint32_t>(blocks)),
+                       dim3(kGThreads), kGhatLds, s, p);
     if ((st = check_launch("G^ split-K (bf16)"))) return st;
-    const int64_t ldp = int64_t(sp.tiles_m) * kBN, plane = int64_t(sp.tiles_r) * kBM * ldp;
+    const int64_t ldp = int64_t(sp.tiles_m) * kGBN, plane = int64_t(sp.tiles_r) * kGBM * ldp;
     hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s,
                        static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
     if ((st = check_launch("G^ reduce"))) return st;

@@ -26,18 +26,24 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
-// Loads `cnt` (< 8) elements of a row tail, zero-filling the rest of the chunk.
-__device__ __forceinline__ u32x4 load16_partial(const uint16_t* p, int cnt) {
-  uint16_t v[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) v[e] = e < cnt ? p[e] : uint16_t(0);
-  u32x4 r;
-  r.x = v[0] | (uint32_t(v[1]) << 16);
-  r.y = v[2] | (uint32_t(v[3]) << 16);
-  r.z = v[4] | (uint32_t(v[5]) << 16);
-  r.w = v[6] | (uint32_t(v[7]) << 16);
-  return r;
+// Keeps the first cnt (0..8) bf16 elements of a 16-byte chunk, zeroes the rest.
+__device__ __forceinline__ u32x4 keep_first(u32x4 v, int cnt) {
+  const uint32_t m0 = cnt >= 2 ? 0xFFFFFFFFu : (cnt == 1 ? 0x0000FFFFu : 0u);
+  const uint32_t m1 = cnt >= 4 ? 0xFFFFFFFFu : (cnt == 3 ? 0x0000FFFFu : 0u);
+  const uint32_t m2 = cnt >= 6 ? 0xFFFFFFFFu : (cnt == 5 ? 0x0000FFFFu : 0u);
+  const uint32_t m3 = cnt >= 8 ? 0xFFFFFFFFu : (cnt == 7 ? 0x0000FFFFu : 0u);
+  v.x &= m0;
+  v.y &= m1;
+  v.z &= m2;
+  v.w &= m3;
+  return v;
 }
+
+// Loads are branch-free: a tile that lies wholly inside the matrix (a
+// workgroup-uniform test) uses plain 16-byte loads; an edge tile clamps each
+// chunk address into the matrix and zeroes the elements outside it.  Chunks
+// are 8-element aligned, so a chunk that starts inside a row may read up to 7
+// elements past the row's last column (never past round_up(cols, 8) <= ld).
 
 // ---------------------------------------------------------------------------
 // Operand stored K-contiguous in global memory: element (row, k) at
@@ -54,17 +60,26 @@ struct KMajorLoader {
   u32x4 reg[kPer];
 
   __device__ __forceinline__ void fetch(int64_t k0, int tid) {
+    if (row0 + ROWS <= rows_total && k0 + kBK <= K) {
 #pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int c = tid + p * NT;
-      const int row = c / kCpr, kc = c % kCpr;
-      const int64_t gr = row0 + row, gk = k0 + kc * 8;
-      if (gr < rows_total && gk + 8 <= K) {
-        reg[p] = load16(base + gr * ld + gk);
-      } else if (gr < rows_total && gk < K) {
-        reg[p] = load16_partial(base + gr * ld + gk, static_cast<int>(K - gk));
-      } else {
-        reg[p] = u32x4{0u, 0u, 0u, 0u};
+      for (int p = 0; p < kPer; ++p) {
+        const int c = tid + p * NT;
+        const int row = c / kCpr, kc = c % kCpr;
+        reg[p] = load16(base + (row0 + row) * ld + k0 + kc * 8);
+      }
+    } else {
+      const int64_t k_last = (K - 1) & ~int64_t(7);
+#pragma unroll
+      for (int p = 0; p < kPer; ++p) {
+        const int c = tid + p * NT;
+        const int row = c / kCpr, kc = c % kCpr;
+        const int64_t gr = row0 + row, gk = k0 + kc * 8;
+        const bool row_ok = gr < rows_total;
+        const int64_t rc = row_ok ? gr : rows_total - 1;
+        const int64_t kcl = gk < K ? gk : k_last;
+        const int64_t left = K - gk;
+        const int cnt = !row_ok || left <= 0 ? 0 : (left >= 8 ? 8 : static_cast<int>(left));
+        reg[p] = keep_first(load16(base + rc * ld + kcl), cnt);
       }
     }
   }
@@ -95,20 +110,31 @@ struct MNMajorLoader {
   u32x4 reg[kPer][4];
 
   __device__ __forceinline__ void fetch(int64_t k0, int tid) {
+    if (row0 + ROWS <= rows_total && k0 + kBK <= K) {
 #pragma unroll
-    for (int p = 0; p < kPer; ++p) {
-      const int b = tid + p * NT;
-      const int rb = b % kRowBlocks, kb = b / kRowBlocks;
-      const int64_t gr = row0 + rb * 8;
+      for (int p = 0; p < kPer; ++p) {
+        const int b = tid + p * NT;
+        const int rb = b % kRowBlocks, kb = b / kRowBlocks;
+        const uint16_t* src = base + (k0 + kb * 4) * ld + row0 + rb * 8;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t gk = k0 + kb * 4 + q;
-        if (gk < K && gr + 8 <= rows_total) {
-          reg[p][q] = load16(base + gk * ld + gr);
-        } else if (gk < K && gr < rows_total) {
-          reg[p][q] = load16_partial(base + gk * ld + gr, static_cast<int>(rows_total - gr));
-        } else {
-          reg[p][q] = u32x4{0u, 0u, 0u, 0u};
+        for (int q = 0; q < 4; ++q) reg[p][q] = load16(src + q * ld);
+      }
+    } else {
+      const int64_t r_last = (rows_total - 1) & ~int64_t(7);
+#pragma unroll
+      for (int p = 0; p < kPer; ++p) {
+        const int b = tid + p * NT;
+        const int rb = b % kRowBlocks, kb = b / kRowBlocks;
+        const int64_t gr = row0 + rb * 8;
+        const int64_t rcl = gr < rows_total ? gr : r_last;
+        const int64_t left = rows_total - gr;
+        const int cnt_r = left <= 0 ? 0 : (left >= 8 ? 8 : static_cast<int>(left));
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t gk = k0 + kb * 4 + q;
+          const bool k_ok = gk < K;
+          const int64_t kcl = k_ok ? gk : K - 1;
+          reg[p][q] = keep_first(load16(base + kcl * ld + rcl), k_ok ? cnt_r : 0);
         }
       }
     }
@@ -232,8 +258,9 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB& lb, int64_t k_begin, i
   constexpr int kAElems = BM * kBK, kBElems = BN * kBK;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  uint16_t* As[2] = {lds, lds + kAElems + kBElems};
-  uint16_t* Bs[2] = {lds + kAElems, lds + 2 * kAElems + kBElems};
+  // Stage s holds A at lds + s * kStage and B right after it.  Offsets (not a
+  // pointer array) keep every access in the LDS address space.
+  constexpr int kStage = kAElems + kBElems;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
@@ -244,20 +271,21 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB& lb, int64_t k_begin, i
   if (kt_count <= 0) return;
   la.fetch(k_begin, tid);
   lb.fetch(k_begin, tid);
-  la.commit(As[0], tid);
-  lb.commit(Bs[0], tid);
+  la.commit(lds, tid);
+  lb.commit(lds + kAElems, tid);
   __syncthreads();
   for (int64_t kt = 0; kt < kt_count; ++kt) {
-    const int cur = static_cast<int>(kt & 1);
+    const int cur = static_cast<int>(kt & 1) * kStage;
+    const int nxt = kStage - cur;
     const bool more = kt + 1 < kt_count;
     if (more) {
       la.fetch(k_begin + (kt + 1) * kBK, tid);
       lb.fetch(k_begin + (kt + 1) * kBK, tid);
     }
-    mma_tile<FM, FN>(As[cur], Bs[cur], wm * FM * 32, wn * FN * 32, lane, acc);
+    mma_tile<FM, FN>(lds + cur, lds + cur + kAElems, wm * FM * 32, wn * FN * 32, lane, acc);
     if (more) {
-      la.commit(As[cur ^ 1], tid);
-      lb.commit(Bs[cur ^ 1], tid);
+      la.commit(lds + nxt, tid);
+      lb.commit(lds + nxt + kAElems, tid);
     }
     __syncthreads();
   }

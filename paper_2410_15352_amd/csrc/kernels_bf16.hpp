@@ -12,6 +12,12 @@
 
 namespace compact {
 
+// Workgroups per CU the register budget is tuned for: wave tiles of 128x128 or
+// more keep 256 accumulators per lane and need the whole 512-register file.
+__host__ __device__ constexpr int occupancy_for(int bm, int bn, int wgm, int wgn) {
+  return (bm / wgm) * (bn / wgn) >= 128 * 128 ? 1 : 2;
+}
+
 // ------------------------------- forward -----------------------------------
 struct FwdParams {
   const uint16_t* x;
@@ -47,7 +53,7 @@ __device__ __forceinline__ void store_tile_bf16(const f32x16 (&acc)[BM / WGM / 3
 }
 
 template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_fwd_bf16(FwdParams p) {
+__global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_fwd_bf16(FwdParams p) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -138,7 +144,7 @@ struct DxParams {
 };
 
 template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_dx_bf16(DxParams p) {
+__global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_dx_bf16(DxParams p) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -164,7 +170,7 @@ struct GhatParams {
 };
 
 template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 2) void k_ghat_bf16(GhatParams p) {
+__global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_ghat_bf16(GhatParams p) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -225,7 +231,7 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const int64_t ldp = p.r_pad + 8;
   uint16_t* Ap = lds;
-  uint16_t* Bs[2] = {lds + BM * ldp, lds + BM * ldp + BN * kBK};
+  const int64_t bs0 = BM * ldp;  // N tile stages at lds + bs0 and lds + bs0 + BN * 64
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
   const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
@@ -285,10 +291,11 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.0f;
     lb.fetch(0, tid);
-    lb.commit(Bs[0], tid);
+    lb.commit(lds + bs0, tid);
     __syncthreads();
     for (int kt = 0; kt < kt_count; ++kt) {
-      const int cur = kt & 1;
+      const int64_t cur = bs0 + (kt & 1) * (BN * kBK);
+      const int64_t nxt = bs0 + ((kt + 1) & 1) * (BN * kBK);
       const bool more = kt + 1 < kt_count;
       if (more) lb.fetch(static_cast<int64_t>(kt + 1) * kBK, tid);
 #pragma unroll
@@ -301,13 +308,13 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
                                                   kt * kBK + k);
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn)
-          b[fn] = *reinterpret_cast<const u32x4*>(Bs[cur] + tile_off(wn * FN * 32 + fn * 32 + lr, k));
+          b[fn] = *reinterpret_cast<const u32x4*>(lds + cur + tile_off(wn * FN * 32 + fn * 32 + lr, k));
 #pragma unroll
         for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
           for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32x32x16(a[fm], b[fn], acc[fm][fn]);
       }
-      if (more) lb.commit(Bs[cur ^ 1], tid);
+      if (more) lb.commit(lds + nxt, tid);
       __syncthreads();
     }
     const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
