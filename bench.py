@@ -104,6 +104,9 @@ class Model:
         wf = max(cp.fwd_workspace_bytes(L.n, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
         wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
         wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
+        self.batch = [dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed, alpha=wl.alpha)
+                      for i, L in enumerate(wl.layers)]
+        wsz = max(wsz, cp.step_batched_workspace_bytes(self.batch))
         self.ws_f = torch.zeros(wf, dtype=torch.uint8, device=dev) if wf else None
         self.ws_b = torch.zeros(wb, dtype=torch.uint8, device=dev)
         self.ws_s = torch.zeros(wsz, dtype=torch.uint8, device=dev)
@@ -123,6 +126,13 @@ class Model:
         self.cp.compact_step(self.W[i], self.G[i], self.M[i], self.V[i], self.seeds[i], t, wl.lr,
                              wl.beta1, wl.beta2, wl.eps, wl.alpha, ws=self.ws_s)
 
+    def upd_all(self, t):
+        """Alg. 3 for every layer: batched Adam and decompression launches."""
+        wl = self.wl
+        for i, d in enumerate(self.batch):
+            d["seed"] = self.seeds[i]
+        self.cp.compact_step_batched(self.batch, t, wl.lr, wl.beta1, wl.beta2, wl.eps, ws=self.ws_s)
+
     def step(self, reseed_period):
         self.t += 1
         n = len(self.wl.layers)
@@ -130,8 +140,7 @@ class Model:
             self.fwd(i)
         for i in reversed(range(n)):
             self.bwd(i)
-        for i in range(n):
-            self.upd(i, self.t)
+        self.upd_all(self.t)
         for i in range(n):
             self.seeds[i] = self.cp.compact_next_seed(self.seeds[i], self.t, reseed_period)
 
@@ -166,7 +175,7 @@ def time_phases(model, torch, reps=2):
                            for i, L in enumerate(model.wl.layers)],
         "bwd_ghat": lambda: [model.cp.compact_bwd(model.dy[L.m], None, model.z[i], None, model.G[i],
                                                   ws=model.ws_b) for i, L in enumerate(model.wl.layers)],
-        "step": lambda: [model.upd(i, max(model.t, 1)) for i in range(n)],
+        "step": lambda: model.upd_all(max(model.t, 1)),
     }
     for name, fn in phases.items():
         fn()  # warm

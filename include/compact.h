@@ -142,6 +142,35 @@ int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64
 size_t compact_step_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype);
 
 /*
+ * One layer of compact_step_batched.  Pointers as in compact_step.
+ */
+typedef struct {
+  void* W;          /* [n x m], ld ldw, w_dtype of the call          */
+  int64_t ldw;
+  const float* G;   /* [r x m] fp32 dense                           */
+  float* M;         /* [r x m] fp32 dense                           */
+  float* V;         /* [r x m] fp32 dense                           */
+  int64_t n, m, r;
+  uint64_t seed;    /* the seed this layer's forward used            */
+  double alpha;     /* per-layer scale alpha (Alg. 3)               */
+} compact_layer;
+
+/*
+ * Alg. 3 for `count` layers at once (same step t and hyper-parameters lr,
+ * beta1, beta2, eps; per-layer seed and alpha): one Adam launch and one
+ * decompression launch per 16 layers instead of two launches per layer.
+ * `layers` is a HOST array, read during the call.  Results are bitwise equal
+ * to calling compact_step on each layer.  bf16 compute only (dtype
+ * COMPACT_BF16); w_dtype bf16 or fp32.  Workspace: at least
+ * compact_step_batched_workspace_bytes(layers, count, dtype) bytes.
+ */
+int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, double lr,
+                         double beta1, double beta2, double eps, int proj, int dtype, int w_dtype,
+                         void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_step_batched_workspace_bytes(const compact_layer* layers, int32_t count, int dtype);
+
+/*
  * The P stream (§3.3: P sampled from the layer seed, re-sampled with the same
  * seed, never stored), exported for tests: writes the UNSCALED normals
  * G(seed, i, j), 0 <= i < n, 0 <= j < r, as fp32 into out [n x r] (ld >= r,

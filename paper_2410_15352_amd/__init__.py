@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 PROJ = {"gaussian": 0, "identity": 1}
 
 __all__ = ["compact_fwd", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
-           "compact_pstream_boxmuller",
+           "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
            "saved_activation_elems", "CompactError", "library", "F32", "BF16"]
 
@@ -137,6 +137,41 @@ def compact_step(W, G, M, V, seed, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, alph
                           float(eps), float(alpha), PROJ[proj], d_code, w_code, wp, wb,
                           _stream(stream, W))
     _check("compact_step", st)
+
+
+def _layer_array(layers):
+    arr = (_lib.CompactLayer * len(layers))()
+    for i, L in enumerate(layers):
+        W, G, M, V = L["W"], L["G"], L["M"], L["V"]
+        r, m = G.shape
+        for name, t_ in (("G", G), ("M", M), ("V", V)):
+            if not t_.is_contiguous() or tuple(t_.shape) != (r, m):
+                raise ValueError(f"layer {i}: {name} must be a contiguous (r, m) fp32 tensor")
+        arr[i] = _lib.CompactLayer(W.data_ptr(), _ld(W), G.data_ptr(), M.data_ptr(), V.data_ptr(),
+                                   W.shape[0], m, r, int(L["seed"]) & (2**64 - 1),
+                                   float(L.get("alpha", 1.0)))
+    return arr
+
+
+def step_batched_workspace_bytes(layers, dtype=BF16):
+    arr = _layer_array(layers)
+    return int(_lib.load().compact_step_batched_workspace_bytes(arr, len(layers), dtype))
+
+
+def compact_step_batched(layers, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, proj="gaussian",
+                         ws=None, stream=None):
+    """Alg. 3 for many layers in a few launches.  layers: list of dicts with
+    keys W, G, M, V, seed and optional alpha (bf16 compute; W bf16 or fp32)."""
+    lib = _lib.load()
+    if not layers:
+        return
+    arr = _layer_array(layers)
+    w_code = _dtype_code(layers[0]["W"])
+    wp, wb = _ws(ws)
+    st = lib.compact_step_batched(arr, len(layers), int(t), float(lr), float(beta1), float(beta2),
+                                  float(eps), PROJ[proj], BF16, w_code, wp, wb,
+                                  _stream(stream, layers[0]["W"]))
+    _check("compact_step_batched", st)
 
 
 def compact_pstream(seed, out, stream=None):

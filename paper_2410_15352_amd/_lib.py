@@ -30,6 +30,19 @@ SIGNATURES = {
     "compact_version": (c_int, []),
 }
 
+
+class CompactLayer(ctypes.Structure):
+    """compact_layer of include/compact.h."""
+    _fields_ = [("W", c_vp), ("ldw", c_i64), ("G", c_vp), ("M", c_vp), ("V", c_vp),
+                ("n", c_i64), ("m", c_i64), ("r", c_i64), ("seed", c_u64), ("alpha", c_f64)]
+
+
+SIGNATURES["compact_step_batched"] = (c_int, [ctypes.POINTER(CompactLayer), ctypes.c_int32, c_i64, c_f64,
+                                              c_f64, c_f64, c_f64, c_int, c_int, c_int, c_vp, c_size,
+                                              c_vp])
+SIGNATURES["compact_step_batched_workspace_bytes"] = (c_size, [ctypes.POINTER(CompactLayer),
+                                                              ctypes.c_int32, c_int])
+
 _lib = None
 
 

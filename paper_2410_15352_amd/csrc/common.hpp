@@ -45,6 +45,19 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblk) {
   return x * q + (x < rem ? x : rem) + k;
 }
 
+// Several layers per launch: block b belongs to the layer l with
+// begin[l] <= b < begin[l + 1] (begin[0] = 0, begin[count] = grid size).
+constexpr int kBatchLayers = 16;
+
+__device__ __forceinline__ int batch_layer_of(const int* begin, int count, int b) {
+  int lo = 0, hi = count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (begin[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
 __host__ __device__ constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 

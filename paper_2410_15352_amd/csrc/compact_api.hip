@@ -6,6 +6,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <string>
+#include <vector>
+#include <algorithm>
 
 #include "../../include/compact.h"
 #include "kernels_bf16.hpp"
@@ -342,17 +344,34 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
                        dim3(kGThreads), kGhatLds, s, p);
     if ((st = check_launch("G^ split-K (bf16)"))) return st;
     const int64_t ldp = int64_t(sp.tiles_m) * kGBN, plane = int64_t(sp.tiles_r) * kGBM * ldp;
-    hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s,
-                       static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
+    if (m % 4 == 0 && aligned16(G)) {
+      hipLaunchKernelGGL(k_splitk_reduce4, dim3(static_cast<uint32_t>(ceil_div(r * (m / 4), 256))), dim3(256), 0, s,
+                         static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
+    } else {
+      hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s,
+                         static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
+    }
     if ((st = check_launch("G^ reduce"))) return st;
   }
   return ok();
 }
 
-int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n,
-                 int64_t m, int64_t r, uint64_t seed, int64_t t, double lr, double beta1,
-                 double beta2, double eps, double alpha, int proj, int dtype, int w_dtype,
-                 void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Per-layer launch description of Alg. 3 (Adam + decompression).
+struct StepPlan {
+  AdamParams ap;
+  int adam_blocks;
+  DecParams dp;
+  int dec_bm;       // 64 or 32 rows per P panel; 0 = fp32 path
+  size_t dec_lds;
+};
+
+int validate_step(const void* W, int64_t ldw, const float* G, const float* M, const float* V, int64_t n,
+                  int64_t m, int64_t r, int64_t t, double lr, double beta1, double beta2, double eps,
+                  double alpha, int proj, int dtype, int w_dtype) {
   int st;
   if (!valid_dtype(dtype) || !valid_dtype(w_dtype)) return fail(COMPACT_EINVAL, "unknown dtype");
   if ((st = check_shape(0, n, m, r, proj))) return st;
@@ -365,13 +384,17 @@ int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64
   if (!(lr >= 0.0) || !std::isfinite(lr) || !std::isfinite(alpha)) return fail(COMPACT_EINVAL, "bad lr or alpha");
   if (dtype == COMPACT_F32 && w_dtype != COMPACT_F32)
     return fail(COMPACT_EUNSUPPORTED, "fp32 decompression needs fp32 W");
-  const size_t need = compact_step_workspace_bytes(n, m, r, dtype);
-  if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "step workspace %zu B < %zu B", ws_bytes, need);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  void* Nbuf = align_ws(ws);
-  const int64_t ldn = n_ld(m);
+  return COMPACT_OK;
+}
 
-  AdamParams ap{};
+constexpr size_t kTilesLds = 2u * 128 * kBK * sizeof(uint16_t);  // N tile stages of the decompression
+
+int plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n, int64_t m, int64_t r,
+              uint64_t seed, int64_t t, double lr, double beta1, double beta2, double eps, double alpha,
+              int proj, int dtype, int w_dtype, void* Nbuf, bool fill_gpu, StepPlan& P) {
+  const int64_t ldn = n_ld(m);
+  AdamParams& ap = P.ap;
+  ap = AdamParams{};
   ap.G = G; ap.M = M; ap.V = V; ap.N = Nbuf; ap.ldn = ldn;
   ap.n_f32 = dtype == COMPACT_F32;
   ap.r = r; ap.m = m;
@@ -382,63 +405,173 @@ int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64
   ap.bc1 = static_cast<float>(1.0 - std::pow(beta1, static_cast<double>(t)));
   ap.bc2 = static_cast<float>(1.0 - std::pow(beta2, static_cast<double>(t)));
   ap.eps = static_cast<float>(eps);
-  {
-    int64_t blocks = ceil_div(r * m, 256);
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(k_adam, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, ap);
-    if ((st = check_launch("Adam"))) return st;
-  }
-  const double coef64 = lr * alpha *
-                        (proj == COMPACT_PROJ_IDENTITY ? 1.0 : 1.0 / std::sqrt(static_cast<double>(r)));
-  const float coef = static_cast<float>(coef64);
+  const int64_t work = (m % 4 == 0) ? ceil_div(r * m, 4) : r * m;
+  int64_t ab = ceil_div(work, 256);
+  P.adam_blocks = static_cast<int>(ab > 2048 ? 2048 : (ab < 1 ? 1 : ab));
 
-  if (dtype == COMPACT_F32) {
-    GemmF32Params gp{};
-    gp.A = pgen_operand(seed, n, r, proj);
-    gp.B = mem_operand(static_cast<const float*>(Nbuf), ldn, 1, r, m);
-    gp.M = n; gp.N = m; gp.K = r; gp.mode = 1;
-    gp.out = static_cast<float*>(W); gp.ldo = ldw; gp.coef = coef;
-    if ((st = launch_gemm_f32(gp, s, "decompress (fp32)"))) return st;
-    return ok();
-  }
-
-  DecParams p{};
+  const double coef64 = lr * alpha * (proj == COMPACT_PROJ_IDENTITY ? 1.0 : 1.0 / std::sqrt(static_cast<double>(r)));
+  DecParams& p = P.dp;
+  p = DecParams{};
   p.W = W; p.ldw = ldw; p.w_f32 = w_dtype == COMPACT_F32;
   p.N = static_cast<const uint16_t*>(Nbuf); p.ldn = ldn;
   p.n = n; p.m = m; p.r = r;
   p.r_pad = round_up(r, kBK);
   p.key = philox_key(seed);
   p.identity = proj == COMPACT_PROJ_IDENTITY;
-  p.coef = coef;
+  p.coef = static_cast<float>(coef64);
   p.tiles_m = static_cast<int>(ceil_div(m, 128));
-  const size_t tiles_lds = 2u * 128 * kBK * sizeof(uint16_t);
+  P.dec_bm = 0;
+  P.dec_lds = 0;
+  if (dtype == COMPACT_F32) return COMPACT_OK;
   const size_t panel64 = size_t(64) * (p.r_pad + 8) * sizeof(uint16_t);
   const size_t panel32 = size_t(32) * (p.r_pad + 8) * sizeof(uint16_t);
-  const size_t lds_limit = 160 * 1024;
-  if (panel64 + tiles_lds <= 100 * 1024) {
-    p.panels = static_cast<int>(ceil_div(n, 64));
-    int64_t groups = ceil_div(1024, p.panels);
-    if (groups > p.tiles_m) groups = p.tiles_m;
-    if (groups < 1) groups = 1;
-    p.col_groups = static_cast<int>(groups);
-    const size_t lds = panel64 + tiles_lds;
-    auto fn = k_decompress_bf16<64, 128, 2, 2>;
-    if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
-    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(int64_t(p.panels) * p.col_groups)), dim3(256), lds, s, p);
-    if ((st = check_launch("decompress (bf16, 64-row panels)"))) return st;
-  } else if (panel32 + tiles_lds <= lds_limit) {
-    p.panels = static_cast<int>(ceil_div(n, 32));
-    int64_t groups = ceil_div(1024, p.panels);
-    if (groups > p.tiles_m) groups = p.tiles_m;
-    if (groups < 1) groups = 1;
-    p.col_groups = static_cast<int>(groups);
-    const size_t lds = panel32 + tiles_lds;
-    auto fn = k_decompress_bf16<32, 128, 1, 4>;
-    if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
-    hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(int64_t(p.panels) * p.col_groups)), dim3(256), lds, s, p);
-    if ((st = check_launch("decompress (bf16, 32-row panels)"))) return st;
+  if (panel64 + kTilesLds <= 100 * 1024) {
+    P.dec_bm = 64;
+    P.dec_lds = panel64 + kTilesLds;
+  } else if (panel32 + kTilesLds <= 160 * 1024) {
+    P.dec_bm = 32;
+    P.dec_lds = panel32 + kTilesLds;
   } else {
     return fail(COMPACT_EUNSUPPORTED, "rank r=%lld too large for the resident projection panel", (long long)r);
+  }
+  p.panels = static_cast<int>(ceil_div(n, P.dec_bm));
+  // Column groups per panel: more groups = more workgroups in flight but one
+  // more regeneration of the panel each.  Two suit a batch of layers; a lone
+  // layer splits further (up to 4) to fill the GPU.
+  int64_t groups = 2;
+  if (fill_gpu) {
+    groups = ceil_div(512, p.panels);
+    if (groups > 4) groups = 4;
+  }
+  if (groups > p.tiles_m) groups = p.tiles_m;
+  if (groups < 1) groups = 1;
+  p.col_groups = static_cast<int>(groups);
+  return COMPACT_OK;
+}
+
+int launch_decompress(const StepPlan& P, hipStream_t s) {
+  int st;
+  const uint32_t blocks = static_cast<uint32_t>(int64_t(P.dp.panels) * P.dp.col_groups);
+  if (P.dec_bm == 64) {
+    auto fn = k_decompress_bf16<64, 128, 2, 2>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), P.dec_lds))) return st;
+    hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), P.dec_lds, s, P.dp);
+  } else {
+    auto fn = k_decompress_bf16<32, 128, 1, 4>;
+    if ((st = set_lds(reinterpret_cast<const void*>(fn), P.dec_lds))) return st;
+    hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), P.dec_lds, s, P.dp);
+  }
+  return check_launch("decompress (bf16)");
+}
+
+}  // namespace
+
+extern "C" {
+
+int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n,
+                 int64_t m, int64_t r, uint64_t seed, int64_t t, double lr, double beta1,
+                 double beta2, double eps, double alpha, int proj, int dtype, int w_dtype,
+                 void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if ((st = validate_step(W, ldw, G, M, V, n, m, r, t, lr, beta1, beta2, eps, alpha, proj, dtype, w_dtype)))
+    return st;
+  const size_t need = compact_step_workspace_bytes(n, m, r, dtype);
+  if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "step workspace %zu B < %zu B", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  StepPlan P;
+  if ((st = plan_step(W, ldw, G, M, V, n, m, r, seed, t, lr, beta1, beta2, eps, alpha, proj, dtype, w_dtype,
+                      align_ws(ws), true, P)))
+    return st;
+  hipLaunchKernelGGL(k_adam, dim3(static_cast<uint32_t>(P.adam_blocks)), dim3(256), 0, s, P.ap);
+  if ((st = check_launch("Adam"))) return st;
+  if (dtype == COMPACT_F32) {
+    GemmF32Params gp{};
+    gp.A = pgen_operand(seed, n, r, proj);
+    gp.B = mem_operand(static_cast<const float*>(P.ap.N), P.ap.ldn, 1, r, m);
+    gp.M = n; gp.N = m; gp.K = r; gp.mode = 1;
+    gp.out = static_cast<float*>(W); gp.ldo = ldw; gp.coef = P.dp.coef;
+    if ((st = launch_gemm_f32(gp, s, "decompress (fp32)"))) return st;
+    return ok();
+  }
+  if ((st = launch_decompress(P, s))) return st;
+  return ok();
+}
+
+size_t compact_step_batched_workspace_bytes(const compact_layer* layers, int32_t count, int dtype) {
+  if (layers == nullptr || count <= 0) return 0;
+  size_t total = kWsAlign;
+  for (int32_t i = 0; i < count; ++i)
+    total += round_up(static_cast<int64_t>(size_t(layers[i].r) * size_t(n_ld(layers[i].m)) * elem_size(dtype)),
+                      kWsAlign);
+  return total;
+}
+
+int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, double lr,
+                         double beta1, double beta2, double eps, int proj, int dtype, int w_dtype,
+                         void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (count < 0 || (count > 0 && layers == nullptr)) return fail(COMPACT_EINVAL, "bad layer list");
+  if (count == 0) return ok();
+  if (dtype != COMPACT_BF16) return fail(COMPACT_EUNSUPPORTED, "batched step supports bf16 compute only");
+  for (int32_t i = 0; i < count; ++i) {
+    const compact_layer& L = layers[i];
+    if ((st = validate_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, t, lr, beta1, beta2, eps, L.alpha, proj,
+                            dtype, w_dtype))) {
+      const std::string msg = g_last_error;
+      return fail(st, "layer %d: %s", static_cast<int>(i), msg.c_str());
+    }
+  }
+  const size_t need = compact_step_batched_workspace_bytes(layers, count, dtype);
+  if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "batched step workspace %zu B < %zu B", ws_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  std::vector<StepPlan> plans(static_cast<size_t>(count));
+  char* cursor = static_cast<char*>(align_ws(ws));
+  for (int32_t i = 0; i < count; ++i) {
+    const compact_layer& L = layers[i];
+    if ((st = plan_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, L.seed, t, lr, beta1, beta2, eps, L.alpha,
+                        proj, dtype, w_dtype, cursor, false, plans[i])))
+      return st;
+    cursor += round_up(static_cast<int64_t>(size_t(L.r) * size_t(n_ld(L.m)) * elem_size(dtype)), kWsAlign);
+  }
+  // Adam: up to kBatchLayers layers per launch
+  for (int32_t i0 = 0; i0 < count; i0 += kBatchLayers) {
+    AdamBatch a{};
+    a.count = std::min<int32_t>(kBatchLayers, count - i0);
+    a.begin[0] = 0;
+    for (int j = 0; j < a.count; ++j) {
+      a.layer[j] = plans[i0 + j].ap;
+      a.begin[j + 1] = a.begin[j] + plans[i0 + j].adam_blocks;
+    }
+    hipLaunchKernelGGL(k_adam_batched, dim3(static_cast<uint32_t>(a.begin[a.count])), dim3(256), 0, s, a);
+    if ((st = check_launch("Adam (batched)"))) return st;
+  }
+  // decompression: consecutive layers with the same panel height, up to kBatchLayers per launch
+  for (int32_t i0 = 0; i0 < count;) {
+    const int bm = plans[i0].dec_bm;
+    DecBatch d{};
+    d.count = 0;
+    d.begin[0] = 0;
+    size_t lds = 0;
+    int32_t i = i0;
+    while (i < count && d.count < kBatchLayers && plans[i].dec_bm == bm) {
+      d.layer[d.count] = plans[i].dp;
+      d.begin[d.count + 1] = d.begin[d.count] + plans[i].dp.panels * plans[i].dp.col_groups;
+      lds = std::max(lds, plans[i].dec_lds);
+      ++d.count;
+      ++i;
+    }
+    const uint32_t blocks = static_cast<uint32_t>(d.begin[d.count]);
+    if (bm == 64) {
+      auto fn = k_decompress_batched<64, 128, 2, 2>;
+      if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
+      hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), lds, s, d);
+    } else {
+      auto fn = k_decompress_batched<32, 128, 1, 4>;
+      if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
+      hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), lds, s, d);
+    }
+    if ((st = check_launch("decompress (batched)"))) return st;
+    i0 = i;
   }
   return ok();
 }

@@ -9,6 +9,7 @@
 //                       LDS (Alg. 3, decompression and update)
 #pragma once
 #include "gemm_bf16.hpp"
+#include "gemm_dtl.hpp"
 
 namespace compact {
 
@@ -39,20 +40,6 @@ struct FwdParams {
 };
 
 template <int BM, int BN, int WGM, int WGN>
-__device__ __forceinline__ void store_tile_bf16(const f32x16 (&acc)[BM / WGM / 32][BN / WGN / 32],
-                                                uint16_t* out, int64_t ld, int64_t rows,
-                                                int64_t cols, int64_t row0, int64_t col0,
-                                                float scale) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
-  for_each_acc(acc, lane, [&](int row, int col, float v) {
-    const int64_t gr = r0 + row, gc = c0 + col;
-    if (gr < rows && gc < cols) out[gr * ld + gc] = f32_to_bf16(v * scale);
-  });
-}
-
-template <int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_fwd_bf16(FwdParams p) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
@@ -67,7 +54,7 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
     const int64_t col0 = static_cast<int64_t>(ct) * BN;
     MNMajorLoader<BN, NT> lb{p.W, p.ldw, p.m, p.n, col0};
     gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
-    store_tile_bf16<BM, BN, WGM, WGN>(acc, p.y, p.ldy, p.T, p.m, row0, col0, 1.0f);
+    store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.y, p.ldy, p.T, p.m, row0, col0, 1.0f);
   } else {
     const int64_t col0 = static_cast<int64_t>(ct - p.tiles_y) * BN;
     if (p.pt != nullptr) {
@@ -77,7 +64,7 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
       PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.identity};
       gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
     }
-    store_tile_bf16<BM, BN, WGM, WGN>(acc, p.z, p.ldz, p.T, p.r, row0, col0, p.zscale);
+    store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.z, p.ldz, p.T, p.r, row0, col0, p.zscale);
   }
 }
 
@@ -155,7 +142,23 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
   KMajorLoader<BN, NT> lb{p.W, p.ldw, p.n, p.m, col0};
   f32x16 acc[FM][FN];
   gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.m, lds, acc);
-  store_tile_bf16<BM, BN, WGM, WGN>(acc, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
+  store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
+}
+
+// dx through the direct-to-LDS core (needs m % 8 == 0).
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_dx_bf16_dtl(DxParams p) {
+  constexpr int NW = WGM * WGN;
+  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int rt = static_cast<int>(logical / p.tiles_n), ct = static_cast<int>(logical % p.tiles_n);
+  const int64_t row0 = static_cast<int64_t>(rt) * BM, col0 = static_cast<int64_t>(ct) * BN;
+  const KMajorDTL<BM, NW> la{p.dy, p.lddy, p.T, p.m, row0};
+  const KMajorDTL<BN, NW> lb{p.W, p.ldw, p.n, p.m, col0};
+  f32x16 acc[FM][FN];
+  gemm_mainloop_dtl<BM, BN, WGM, WGN, KMajorDTL<BM, NW>, KMajorDTL<BN, NW>, KFrag, KFrag>(la, lb, 0, p.m, lds, acc);
+  store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
 }
 
 struct GhatParams {
@@ -176,21 +179,43 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
   const int tiles = p.tiles_r * p.tiles_m;
+  // order (split, column tile, row tile): the row tiles that read the same
+  // dL/do columns are adjacent, hence on the same XCD at the same time
   const int split = static_cast<int>(logical / tiles), tile = static_cast<int>(logical % tiles);
-  const int rt = tile / p.tiles_m, ct = tile % p.tiles_m;
+  const int ct = tile / p.tiles_r, rt = tile % p.tiles_r;
   const int64_t row0 = static_cast<int64_t>(rt) * BM, col0 = static_cast<int64_t>(ct) * BN;
   const int64_t k_begin = split * p.split_len;
   const int64_t k_end = k_begin + p.split_len < p.T ? k_begin + p.split_len : p.T;
-  MNMajorLoader<BM, NT> la{p.z, p.ldz, p.r, p.T, row0};
-  MNMajorLoader<BN, NT> lb{p.dy, p.lddy, p.m, p.T, col0};
+  MNMajorLoader<BM, NT> la[2] = {{p.z, p.ldz, p.r, p.T, row0}, {p.z, p.ldz, p.r, p.T, row0}};
+  MNMajorLoader<BN, NT> lb[2] = {{p.dy, p.lddy, p.m, p.T, col0}, {p.dy, p.lddy, p.m, p.T, col0}};
   f32x16 acc[FM][FN];
-  gemm_mainloop<BM, BN, WGM, WGN>(la, lb, k_begin, k_end, lds, acc);
+  gemm_mainloop_deep<BM, BN, WGM, WGN>(la, lb, k_begin, k_end, lds, acc);
   const int64_t ldp = static_cast<int64_t>(p.tiles_m) * BN;
   float* out = p.part + static_cast<int64_t>(split) * (p.tiles_r * BM) * ldp;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
   const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
   for_each_acc(acc, lane, [&](int row, int col, float v) { out[(r0 + row) * ldp + c0 + col] = v; });
+}
+
+// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c];
+// four consecutive columns per thread (m % 4 == 0), else one.
+__global__ void k_splitk_reduce4(const float* part, int splits, int64_t ldp, int64_t plane,
+                                 int64_t r, int64_t m, float* G) {
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t mq = m / 4;
+  if (q >= r * mq) return;
+  const int64_t j = q / mq, c = (q % mq) * 4;
+  const float* src = part + j * ldp + c;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < splits; ++k) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(src + k * plane);
+    s.x = s.x + v.x;
+    s.y = s.y + v.y;
+    s.z = s.z + v.z;
+    s.w = s.w + v.w;
+  }
+  *reinterpret_cast<f32x4*>(G + j * m + c) = s;
 }
 
 // G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c].
@@ -225,7 +250,7 @@ struct DecParams {
 // Panel layout: [BM][r_pad + 8] bf16; the +8 pad puts the rows of one MFMA
 // fragment read on distinct LDS banks (r_pad / 8 is even).
 template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParams p) {
+__device__ __forceinline__ void decompress_block(const DecParams& p, uint32_t logical) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
@@ -234,7 +259,6 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
   const int64_t bs0 = BM * ldp;  // N tile stages at lds + bs0 and lds + bs0 + BN * 64
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
   const int panel = static_cast<int>(logical % p.panels), group = static_cast<int>(logical / p.panels);
   const int64_t row0 = static_cast<int64_t>(panel) * BM;
 
@@ -275,13 +299,44 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
   __syncthreads();
 
   // 2. Column tiles of this group: acc = P_panel N_tile, then W -= coef acc.
+  //    The W tile (BM x BN) is read with 16-byte loads issued before the N tile
+  //    and the MFMAs, so its latency overlaps them; coef * acc is staged in LDS
+  //    (the N stages are free after the K loop) and W is written back in 16-byte
+  //    chunks.
   const int per = (p.tiles_m + p.col_groups - 1) / p.col_groups;
   const int ct_begin = group * per;
   const int ct_end = ct_begin + per < p.tiles_m ? ct_begin + per : p.tiles_m;
   const int lr = lane & 31, lh = lane >> 5;
   const int kt_count = static_cast<int>(p.r_pad / kBK);
+  constexpr int kWElems = 8;                                   // elements per 16-byte bf16 chunk
+  constexpr int kWChunks = BM * BN / kWElems / NT;             // bf16 chunks per thread
+  static_assert(BM * BN % (kWElems * NT) == 0, "W tile split");
+  constexpr int kCpr = BN / kWElems;                           // chunks per W-tile row
+  float* stage = reinterpret_cast<float*>(lds + bs0);          // BM x (BN + 4) fp32 after the K loop
+  constexpr int kSld = BN;
+  static_assert(BM * kSld * 4 <= 2 * BN * kBK * 2, "staging fits in the N stages");
   for (int ct = ct_begin; ct < ct_end; ++ct) {
     const int64_t col0 = static_cast<int64_t>(ct) * BN;
+    // (a) W tile loads (bf16: one 16-byte chunk = 8 columns; fp32: two)
+    u32x4 wreg[kWChunks][2];
+#pragma unroll
+    for (int i = 0; i < kWChunks; ++i) {
+      const int c = tid + i * NT;
+      const int row = c / kCpr, cc = c % kCpr;
+      int64_t gr = row0 + row;
+      gr = gr < p.n ? gr : p.n - 1;
+      int64_t gc = col0 + cc * kWElems;
+      const int64_t c_last = (p.m - 1) & ~int64_t(kWElems - 1);
+      gc = gc < p.m ? gc : c_last;
+      if (p.w_f32) {
+        const float* src = static_cast<const float*>(p.W) + gr * p.ldw + gc;
+        wreg[i][0] = *reinterpret_cast<const u32x4*>(src);
+        wreg[i][1] = *reinterpret_cast<const u32x4*>(src + 4);
+      } else {
+        wreg[i][0] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.W) + gr * p.ldw + gc);
+      }
+    }
+    // (b) acc = P_panel[:, k] N[k, col0 ..] over the rank
     MNMajorLoader<BN, NT> lb{p.N, p.ldn, p.m, p.r, col0};
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -317,29 +372,78 @@ __global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParam
       if (more) lb.commit(lds + nxt, tid);
       __syncthreads();
     }
-    const int64_t r0 = row0 + wm * (BM / WGM), c0 = col0 + wn * (BN / WGN);
+    // (c) d = coef * acc into the LDS staging tile (row-major, fp32)
     const float coef = p.coef;
-    if (p.w_f32) {
-      float* W = static_cast<float*>(p.W);
+    {
+      const int r0 = wm * (BM / WGM), c0 = wn * (BN / WGN);
       for_each_acc(acc, lane, [&](int row, int col, float v) {
-        const int64_t gr = r0 + row, gc = c0 + col;
-        if (gr < p.n && gc < p.m) {
-          const float d = coef * v;
-          W[gr * p.ldw + gc] = W[gr * p.ldw + gc] - d;
-        }
-      });
-    } else {
-      uint16_t* W = static_cast<uint16_t*>(p.W);
-      for_each_acc(acc, lane, [&](int row, int col, float v) {
-        const int64_t gr = r0 + row, gc = c0 + col;
-        if (gr < p.n && gc < p.m) {
-          const float d = coef * v;
-          const float w = bf16_to_f32(W[gr * p.ldw + gc]);
-          W[gr * p.ldw + gc] = f32_to_bf16(w - d);
-        }
+        const float d = coef * v;
+        stage[(r0 + row) * kSld + c0 + col] = d;
       });
     }
+    __syncthreads();
+    // (d) W = W - d, 16-byte chunks
+#pragma unroll
+    for (int i = 0; i < kWChunks; ++i) {
+      const int c = tid + i * NT;
+      const int row = c / kCpr, cc = c % kCpr;
+      const int64_t gr = row0 + row, gc = col0 + cc * kWElems;
+      if (gr >= p.n || gc >= p.m) continue;
+      const float* dsrc = stage + row * kSld + cc * kWElems;
+      const f32x4 d0 = *reinterpret_cast<const f32x4*>(dsrc);
+      const f32x4 d1 = *reinterpret_cast<const f32x4*>(dsrc + 4);
+      const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+      const int cnt = gc + kWElems <= p.m ? kWElems : static_cast<int>(p.m - gc);
+      if (p.w_f32) {
+        float* dst = static_cast<float*>(p.W) + gr * p.ldw + gc;
+        const uint32_t wbits[8] = {wreg[i][0].x, wreg[i][0].y, wreg[i][0].z, wreg[i][0].w,
+                                   wreg[i][1].x, wreg[i][1].y, wreg[i][1].z, wreg[i][1].w};
+        float out[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) out[e] = __uint_as_float(wbits[e]) - dv[e];
+        if (cnt == kWElems) {
+          *reinterpret_cast<f32x4*>(dst) = f32x4{out[0], out[1], out[2], out[3]};
+          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{out[4], out[5], out[6], out[7]};
+        } else {
+          for (int e = 0; e < cnt; ++e) dst[e] = out[e];
+        }
+      } else {
+        uint16_t* dst = static_cast<uint16_t*>(p.W) + gr * p.ldw + gc;
+        const uint32_t wp[4] = {wreg[i][0].x, wreg[i][0].y, wreg[i][0].z, wreg[i][0].w};
+        uint32_t outp[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float lo = __uint_as_float(wp[e] << 16) - dv[2 * e];
+          const float hi = __uint_as_float(wp[e] & 0xFFFF0000u) - dv[2 * e + 1];
+          outp[e] = pack_bf16x2(lo, hi);
+        }
+        if (cnt == kWElems) {
+          *reinterpret_cast<u32x4*>(dst) = u32x4{outp[0], outp[1], outp[2], outp[3]};
+        } else {
+          for (int e = 0; e < cnt; ++e) dst[e] = static_cast<uint16_t>(outp[e >> 1] >> (16 * (e & 1)));
+        }
+      }
+    }
+    __syncthreads();  // the staging tile is the next column tile's N stage
   }
+}
+
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParams p) {
+  decompress_block<BM, BN, WGM, WGN>(p, xcd_remap(blockIdx.x, gridDim.x));
+}
+
+struct DecBatch {
+  int count;
+  int begin[kBatchLayers + 1];
+  DecParams layer[kBatchLayers];
+};
+
+template <int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_batched(DecBatch d) {
+  const int b = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
+  const int l = batch_layer_of(d.begin, d.count, b);
+  decompress_block<BM, BN, WGM, WGN>(d.layer[l], static_cast<uint32_t>(b - d.begin[l]));
 }
 
 }  // namespace compact

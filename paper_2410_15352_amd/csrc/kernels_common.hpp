@@ -23,25 +23,79 @@ struct AdamParams {
   float b1, b2, omb1, omb2, bc1, bc2, eps;
 };
 
-__global__ void k_adam(AdamParams p) {
+__device__ __forceinline__ void adam_one(const AdamParams& p, int64_t e, float g, float mo, float vo,
+                                         float& m1, float& v1, float& nv) {
+  m1 = p.b1 * mo + p.omb1 * g;
+  v1 = p.b2 * vo + p.omb2 * (g * g);
+  const float mhat = m1 / p.bc1;
+  const float vhat = v1 / p.bc2;
+  nv = mhat / (__builtin_sqrtf(vhat) + p.eps);
+  (void)e;
+}
+
+// Elements [4 q, 4 q + 4) for q = first, first + stride, ... (m % 4 == 0, so a
+// group of four never crosses a row), else one element per index.
+__device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, int64_t stride) {
   const int64_t total = p.r * p.m;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-  for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
-       e += stride) {
-    const float g = p.G[e];
-    const float m1 = p.b1 * p.M[e] + p.omb1 * g;
-    const float v1 = p.b2 * p.V[e] + p.omb2 * (g * g);
-    p.M[e] = m1;
-    p.V[e] = v1;
-    const float mhat = m1 / p.bc1;
-    const float vhat = v1 / p.bc2;
-    const float nv = mhat / (__builtin_sqrtf(vhat) + p.eps);
-    const int64_t j = e / p.m, c = e - j * p.m;
-    if (p.n_f32)
-      static_cast<float*>(p.N)[j * p.ldn + c] = nv;
-    else
-      static_cast<uint16_t*>(p.N)[j * p.ldn + c] = f32_to_bf16(nv);
+  if (p.m % 4 == 0) {
+    for (int64_t q = first; q * 4 < total; q += stride) {
+      const int64_t e = q * 4;
+      const f32x4 g = *reinterpret_cast<const f32x4*>(p.G + e);
+      const f32x4 mo = *reinterpret_cast<const f32x4*>(p.M + e);
+      const f32x4 vo = *reinterpret_cast<const f32x4*>(p.V + e);
+      f32x4 m1, v1, nv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float a, b, c;
+        adam_one(p, e + i, g[i], mo[i], vo[i], a, b, c);
+        m1[i] = a;
+        v1[i] = b;
+        nv[i] = c;
+      }
+      *reinterpret_cast<f32x4*>(p.M + e) = m1;
+      *reinterpret_cast<f32x4*>(p.V + e) = v1;
+      const int64_t j = e / p.m, c = e - j * p.m;
+      if (p.n_f32) {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(p.N) + j * p.ldn + c) = nv;
+      } else {
+        u32x2 w;
+        w.x = pack_bf16x2(nv[0], nv[1]);
+        w.y = pack_bf16x2(nv[2], nv[3]);
+        *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(p.N) + j * p.ldn + c) = w;
+      }
+    }
+  } else {
+    for (int64_t e = first; e < total; e += stride) {
+      float m1, v1, nv;
+      adam_one(p, e, p.G[e], p.M[e], p.V[e], m1, v1, nv);
+      p.M[e] = m1;
+      p.V[e] = v1;
+      const int64_t j = e / p.m, c = e - j * p.m;
+      if (p.n_f32)
+        static_cast<float*>(p.N)[j * p.ldn + c] = nv;
+      else
+        static_cast<uint16_t*>(p.N)[j * p.ldn + c] = f32_to_bf16(nv);
+    }
   }
+}
+
+__global__ void k_adam(AdamParams p) {
+  adam_range(p, static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x,
+             static_cast<int64_t>(gridDim.x) * blockDim.x);
+}
+
+struct AdamBatch {
+  int count;
+  int begin[kBatchLayers + 1];
+  AdamParams layer[kBatchLayers];
+};
+
+__global__ void k_adam_batched(AdamBatch a) {
+  const int b = static_cast<int>(blockIdx.x);
+  const int l = batch_layer_of(a.begin, a.count, b);
+  const int nb = a.begin[l + 1] - a.begin[l];
+  adam_range(a.layer[l], static_cast<int64_t>(b - a.begin[l]) * blockDim.x + threadIdx.x,
+             static_cast<int64_t>(nb) * blockDim.x);
 }
 
 // ------------------------------- fp32 GEMM ---------------------------------

@@ -218,3 +218,29 @@ def test_three_step_chain(name):
         new_seed = oc.next_seed(seed, t, 2)  # Alg. 3: re-sample every T = 2 steps
         assert cp.compact_next_seed(seed, t, 2) == new_seed
         seed = new_seed
+
+
+def test_step_batched_equals_per_layer():
+    # the batched launch computes exactly what compact_step computes per layer
+    shapes = [(512, 512, 128), (512, 1376, 128), (1376, 512, 344), (300, 200, 40), (5461, 64, 1365)] * 4
+    layers_a, layers_b, states = [], [], []
+    for i, (n, m, r) in enumerate(shapes):
+        W, G, M, V = step_inputs(n, m, r, "bf16", t=2, data_seed=50 + i)
+        wa = to_dev(W, "bf16", ld_for(m, "bf16"))
+        wb = to_dev(W, "bf16", ld_for(m, "bf16"))
+        ga, ma, va = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+        gb, mb, vb = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+        seed = ((i + 1) << 32) | 7
+        layers_a.append(dict(W=wa, G=ga, M=ma, V=va, seed=seed, alpha=0.25 + 0.01 * i))
+        layers_b.append(dict(W=wb, G=gb, M=mb, V=vb, seed=seed, alpha=0.25 + 0.01 * i))
+    ws = workspace(cp.step_batched_workspace_bytes(layers_a))
+    cp.compact_step_batched(layers_a, 2, 1e-3, ws=ws)
+    for L in layers_b:
+        n, m = L["W"].shape
+        r = L["G"].shape[0]
+        ws1 = workspace(cp.step_workspace_bytes(n, m, r))
+        cp.compact_step(L["W"], L["G"], L["M"], L["V"], L["seed"], 2, 1e-3, alpha=L["alpha"], ws=ws1)
+    torch.cuda.synchronize()
+    for La, Lb in zip(layers_a, layers_b):
+        assert torch.equal(La["M"], Lb["M"]) and torch.equal(La["V"], Lb["V"])
+        assert torch.equal(La["W"].view(torch.int16), Lb["W"].view(torch.int16))
