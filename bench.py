@@ -101,7 +101,7 @@ class Model:
             self.G.append(torch.empty(L.r, L.m, dtype=torch.float32, device=dev))
             self.M.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
             self.V.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
-        wf = max(cp.fwd_workspace_bytes(L.n, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
+        wf = max(cp.fwd_workspace_bytes(L.n, L.m, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
         wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
         wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
         self.batch = [dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed, alpha=wl.alpha)

@@ -75,19 +75,22 @@ typedef enum {
  *   z  [tokens x r]  (ld ldz)  compressed activation saved for the backward pass
  *   seed  layer seed; P[i][j] = G(seed, i, j) / sqrt(r) (the P stream, below)
  *   proj  COMPACT_PROJ_GAUSSIAN, or COMPACT_PROJ_IDENTITY with r == n
- *   ws, ws_bytes  optional workspace.  With at least
- *         compact_fwd_workspace_bytes(n, r, dtype) bytes the bf16 path first
- *         writes this call's P^T panel (r x n bf16) into it and the fused GEMM
- *         reads it from cache; with ws == NULL the fused GEMM regenerates every
- *         P tile in LDS.  Both give bitwise identical y and z.  The panel is
- *         scratch: it is dead when the call's kernels have finished.
+ *   ws, ws_bytes  optional workspace of at least
+ *         compact_fwd_workspace_bytes(n, m, r, dtype) bytes (bf16 path).  With
+ *         it the call stages W^T and this call's P^T (r x n, P rounded to
+ *         bf16 once) in the workspace and runs one persistent GEMM over both
+ *         (when n % 8 == 0, n >= 320 and m, r are even; otherwise the fused
+ *         GEMM reads the staged P^T and W directly); with ws == NULL the fused
+ *         GEMM regenerates every P tile in LDS.  All paths give bitwise
+ *         identical y and z.  The workspace is scratch: it is dead when the
+ *         call's kernels have finished.
  * Requirements: tokens >= 0, n >= 1, m >= 1, 1 <= r <= n.
  */
 int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy,
                 void* z, int64_t ldz, int64_t tokens, int64_t n, int64_t m, int64_t r,
                 uint64_t seed, int proj, int dtype, void* ws, size_t ws_bytes, void* stream);
 
-size_t compact_fwd_workspace_bytes(int64_t n, int64_t r, int dtype);
+size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype);
 
 /*
  * Backward pass, Alg. 2:  G^ = z^T dL/do  and  dx = dL/do W^T.

@@ -77,8 +77,8 @@ def _check(fn, status):
         raise CompactError(fn, status)
 
 
-def fwd_workspace_bytes(n, r, dtype=BF16):
-    return int(_lib.load().compact_fwd_workspace_bytes(n, r, dtype))
+def fwd_workspace_bytes(n, m, r, dtype=BF16):
+    return int(_lib.load().compact_fwd_workspace_bytes(n, m, r, dtype))
 
 
 def bwd_workspace_bytes(tokens, n, m, r, dtype=BF16):

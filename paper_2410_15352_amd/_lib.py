@@ -13,7 +13,7 @@ c_i64, c_u64, c_int, c_size, c_vp, c_f64 = (ctypes.c_int64, ctypes.c_uint64, cty
 SIGNATURES = {
     "compact_fwd": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_i64, c_i64,
                             c_i64, c_i64, c_u64, c_int, c_int, c_vp, c_size, c_vp]),
-    "compact_fwd_workspace_bytes": (c_size, [c_i64, c_i64, c_int]),
+    "compact_fwd_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_int]),
     "compact_bwd": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
                             c_i64, c_i64, c_i64, c_int, c_vp, c_size, c_vp]),
     "compact_bwd_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_i64, c_int]),

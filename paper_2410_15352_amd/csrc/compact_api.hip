@@ -10,6 +10,7 @@
 #include <algorithm>
 
 #include "../../include/compact.h"
+#include "gemm_w4_launch.hpp"
 #include "kernels_bf16.hpp"
 #include "kernels_common.hpp"
 
@@ -109,6 +110,13 @@ size_t ghat_ws_bytes(int64_t tokens, int64_t r, int64_t m) {
 }
 
 int64_t pt_ld(int64_t n) { return round_up(n, kBK); }
+
+// Forward operand of the persistent GEMM, K = n contiguous: rows 0 .. m-1 hold
+// W^T, rows round_up(m, 256) .. + r - 1 hold P^T (rows in between are never
+// read into a stored output).
+int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + r; }
+
+int w4_tiles(int64_t cols) { return static_cast<int>(ceil_div(cols, kW4Tile)); }
 int64_t n_ld(int64_t m) { return round_up(m, 8); }
 
 float inv_sqrt_rank(int64_t r, int proj) {
@@ -186,9 +194,9 @@ int64_t compact_saved_activation_elems(int64_t tokens, int64_t n, int64_t r) {
   return tokens * r;
 }
 
-size_t compact_fwd_workspace_bytes(int64_t n, int64_t r, int dtype) {
-  if (dtype != COMPACT_BF16 || n < 1 || r < 1) return 0;
-  return size_t(r) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
+size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
+  if (dtype != COMPACT_BF16 || n < 1 || m < 1 || r < 1) return 0;
+  return size_t(stacked_rows(m, r)) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
 }
 
 size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype) {
@@ -218,11 +226,10 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
   if ((st = check_matrix("W", W, ldw, m, dtype))) return st;
   if ((st = check_matrix("y", y, ldy, m, dtype))) return st;
   if ((st = check_matrix("z", z, ldz, r, dtype))) return st;
-  if (ws != nullptr && ws_bytes < compact_fwd_workspace_bytes(n, r, dtype))
-    return fail(COMPACT_EWORKSPACE, "forward workspace %zu B < %zu B", ws_bytes, compact_fwd_workspace_bytes(n, r, dtype));
+  if (ws != nullptr && ws_bytes < compact_fwd_workspace_bytes(n, m, r, dtype))
+    return fail(COMPACT_EWORKSPACE, "forward workspace %zu B < %zu B", ws_bytes, compact_fwd_workspace_bytes(n, m, r, dtype));
   if (tokens == 0) return ok();
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const float zscale = inv_sqrt_rank(r, proj);
   const int identity = proj == COMPACT_PROJ_IDENTITY;
 
   if (dtype == COMPACT_F32) {
@@ -233,8 +240,38 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     gp.out = static_cast<float*>(y); gp.ldo = ldy; gp.scale = 1.0f;
     if ((st = launch_gemm_f32(gp, s, "forward y (fp32)"))) return st;
     gp.B = pgen_operand(seed, n, r, proj);
-    gp.N = r; gp.out = static_cast<float*>(z); gp.ldo = ldz; gp.scale = zscale;
+    gp.N = r; gp.out = static_cast<float*>(z); gp.ldo = ldz; gp.scale = inv_sqrt_rank(r, proj);
     if ((st = launch_gemm_f32(gp, s, "forward z (fp32)"))) return st;
+    return ok();
+  }
+
+  const PhiloxKey key = philox_key(seed);
+  const float pscale = inv_sqrt_rank(r, proj);
+  const int64_t ldb = pt_ld(n);
+  if (ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, stacked_rows(m, r), ldy, m, ldz, r)) {
+    // persistent GEMM over [W^T; P^T]: y in the first column tiles, z after
+    uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
+    const int64_t mp = round_up(m, kW4Tile);
+    const int tr = static_cast<int>(ceil_div(n, 64)), tc = static_cast<int>(ceil_div(m, 64));
+    hipLaunchKernelGGL(k_transpose_bf16, dim3(static_cast<uint32_t>(int64_t(tr) * tc)), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(W), ldw, n, m, bs, ldb, tc);
+    if ((st = check_launch("W^T (bf16)"))) return st;
+    const int64_t quads = (ldb / 4) * r;
+    hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0, s,
+                       key, n, r, identity, pscale, bs + mp * ldb, ldb);
+    if ((st = check_launch("P panel (bf16)"))) return st;
+    W4Gemm g{};
+    g.A = static_cast<const uint16_t*>(x); g.lda = static_cast<int>(ldx);
+    g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
+    g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(stacked_rows(m, r));
+    g.seg[0] = W4Seg{static_cast<uint16_t*>(y), static_cast<int>(ldy), static_cast<int>(m), w4_tiles(m)};
+    g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(r), w4_tiles(r)};
+    g.tiles_n = g.seg[0].tiles + g.seg[1].tiles;
+    const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
+    if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
+    g.tiles = static_cast<int>(tiles);
+    const hipError_t e = gemm_w4_launch(g, s);
+    if (e != hipSuccess) return fail(COMPACT_EHIP, "forward GEMM (bf16): %s", hipGetErrorString(e));
     return ok();
   }
 
@@ -244,20 +281,19 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
   p.y = static_cast<uint16_t*>(y); p.ldy = ldy;
   p.z = static_cast<uint16_t*>(z); p.ldz = ldz;
   p.T = tokens; p.n = n; p.m = m; p.r = r;
-  p.key = philox_key(seed);
+  p.key = key;
   p.identity = identity;
-  p.zscale = zscale;
+  p.pscale = pscale;
   p.tiles_y = static_cast<int>(ceil_div(m, kBN));
   p.tiles_z = static_cast<int>(ceil_div(r, kBN));
   if (ws != nullptr) {
     uint16_t* pt = static_cast<uint16_t*>(align_ws(ws));
-    const int64_t ld = pt_ld(n);
-    const int64_t quads = (ld / 4) * r;
+    const int64_t quads = (ldb / 4) * r;
     hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0, s,
-                       p.key, n, r, identity, pt, ld);
+                       key, n, r, identity, pscale, pt, ldb);
     if ((st = check_launch("P panel (bf16)"))) return st;
     p.pt = pt;
-    p.ldpt = ld;
+    p.ldpt = ldb;
   }
   const int64_t blocks = ceil_div(tokens, kBM) * (p.tiles_y + p.tiles_z);
   if (blocks > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
@@ -318,7 +354,21 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     return ok();
   }
 
-  if (dx != nullptr) {
+  if (dx != nullptr && gemm_w4_eligible(tokens, m, lddy, ldw, n, lddx, n, 0, 0)) {
+    // persistent GEMM: dx = dL/do W^T with W [n][m] as the K-contiguous B
+    W4Gemm g{};
+    g.A = static_cast<const uint16_t*>(dy); g.lda = static_cast<int>(lddy);
+    g.M = static_cast<int>(tokens); g.K = static_cast<int>(m);
+    g.B = static_cast<const uint16_t*>(W); g.ldb = static_cast<int>(ldw); g.rows_b = static_cast<int>(n);
+    g.seg[0] = W4Seg{static_cast<uint16_t*>(dx), static_cast<int>(lddx), static_cast<int>(n), w4_tiles(n)};
+    g.seg[1] = W4Seg{static_cast<uint16_t*>(dx), static_cast<int>(lddx), 0, 0};
+    g.tiles_n = g.seg[0].tiles;
+    const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
+    if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
+    g.tiles = static_cast<int>(tiles);
+    const hipError_t e = gemm_w4_launch(g, s);
+    if (e != hipSuccess) return fail(COMPACT_EHIP, "dx GEMM (bf16): %s", hipGetErrorString(e));
+  } else if (dx != nullptr) {
     DxParams p{};
     p.dy = static_cast<const uint16_t*>(dy); p.lddy = lddy;
     p.W = static_cast<const uint16_t*>(W); p.ldw = ldw;

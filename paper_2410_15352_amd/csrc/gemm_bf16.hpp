@@ -157,7 +157,8 @@ struct MNMajorLoader {
 
 // ---------------------------------------------------------------------------
 // Projection tile generated on the fly (B operand of z = x P, K = i, N = j):
-// LDS row j holds G[k0 .. k0+63][j] as bf16.  One Philox call gives the four
+// LDS row j holds scale * G[k0 .. k0+63][j] as bf16 (scale = 1/sqrt(r), so
+// the tile is P itself, rounded once).  One Philox call gives the four
 // consecutive rows i = 4p .. 4p+3 of column j, i.e. one 8-byte LDS store.
 // identity != 0 gives P = I instead (r == n).
 // ---------------------------------------------------------------------------
@@ -169,6 +170,7 @@ struct PGenLoader {
   PhiloxKey key;
   int64_t n, r, col0;  // K extent n, N extent r, first column of the tile
   int identity;
+  float scale;
   int64_t k_next;
 
   // Generation happens in commit(), straight into the LDS buffer that is not
@@ -187,8 +189,7 @@ struct PGenLoader {
         } else {
           pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (i0 + e >= n) g[e] = 0.0f;
+          for (int e = 0; e < 4; ++e) g[e] = i0 + e >= n ? 0.0f : g[e] * scale;
         }
       }
       u32x2 v;

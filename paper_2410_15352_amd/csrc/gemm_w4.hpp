@@ -1,0 +1,473 @@
+// Persistent four-wave bf16 GEMM for gfx950: C = A B^T, A [M][K] and B [N][K]
+// both K-contiguous, C bf16.  One workgroup per CU walks a list of 256 x 256
+// output tiles; each of its four waves owns a 128 x 128 accumulator tile
+// (4 x 4 MFMA 32x32x16 fragments, 256 accumulator registers).
+//
+// Why four waves of 128 x 128.  On MI355X an LDS fragment read (ds_read_b128)
+// moves about 170 B/clk per CU.  Eight 64 x 128 wave tiles read 192 KB of
+// fragments per 64-deep K step, which keeps LDS busy as long as the MFMA pipes
+// take for the step; four 128 x 128 tiles read 128 KB.  One wave per SIMD
+// cannot hide LDS latency by switching waves, so the loop software-pipelines
+// it: the fragments of the next 16-deep step are read while the current
+// step's 16 MFMAs issue.
+//
+// Global -> LDS copies use buffer_load_dwordx4 ... lds: one wave instruction
+// moves 64 x 16 bytes straight into LDS (lane L's chunk lands at M0 + 16 L),
+// with no staging registers and no ds_write.  K tiles are 32 deep and LDS
+// holds four of them; the copy stream runs 3 K tiles ahead of the MFMAs over
+// the workgroup's whole list of (tile, K tile) steps, across tile boundaries,
+// so a new tile starts with its operands already in LDS.
+//
+// Why persistent.  With one workgroup per output tile, all 256 workgroups
+// finish their tiles together and write 32 MB at once while no MFMA work is
+// left to overlap it.  Here a finished tile is converted to bf16 pairs in
+// registers and written out 16 stores at a time during the first 8 K tiles of
+// the next tile.
+//
+// Step h of the flat sequence (K tile t of tile q, LDS stage h % 4):
+//   step 0: 16 MFMAs on fragments (h, 0) (t = 0: accumulators start from
+//           zero); between them, read fragments (h, 1) and issue half of the
+//           copies of step h + 3 into stage (h + 3) % 4 (last read during step
+//           h - 1, before its barrier)
+//   step 1: wait until this wave's copies of step h + 1 have landed; barrier
+//           (every wave's copies landed, every read of stage h % 4 done);
+//           16 MFMAs on fragments (h, 1); between them, read fragments
+//           (h + 1, 0) and issue the other half of the copies of step h + 3
+//   t < 8: 16 stores of the previous tile, spread over both steps
+// Copies and stores share the in-order vmcnt counter; the wait of step 1
+// allows exactly the operations issued after the copies of step h + 1
+// (see w4_vm_allow).
+// Copies past the end of the list still issue, against an empty buffer range,
+// so that the count is the same on every step; they land in stages no later
+// step reads.
+//
+// LDS layout (bytes from the dynamic LDS base): A stage s at 16384 s, B stage
+// s at 65536 + 16384 s, each [256 rows][32] bf16.  Row R is 64 bytes = four
+// 16-byte chunks; logical chunk c of row R sits at c ^ ((R >> 2) & 3).  A
+// ds_read_b128 is served 16 lanes at a time over 64 four-byte banks (256
+// bytes): the 16 consecutive rows those lanes read then fill 16 distinct
+// 16-byte bank groups (4 rows per 256 bytes, 4 chunk positions).
+//
+// Edges: operand rows past the matrix and chunks at k >= K read as zero (buffer
+// range check), so the K sum is exact; stores past the last row are dropped by
+// the same check, column pairs past the last column are steered out of range.
+// Requirements (checked by the host): K % 8 == 0, K >= 320, every output
+// column count even, 256 * ld * 2 + 2 K < 2^31 for every matrix, lda and
+// ldb multiples of 8 (16-byte chunks).
+#pragma once
+#include "common.hpp"
+
+namespace compact {
+
+constexpr int kW4Tile = 256;     // workgroup tile, M and N
+constexpr int kW4Threads = 256;  // four waves
+constexpr int kW4K = 32;         // K tile
+constexpr int kW4Stages = 4;
+constexpr int kW4StageBytes = kW4Tile * kW4K * 2;          // one operand, one stage
+constexpr int kW4BBase = kW4Stages * kW4StageBytes;        // B stages follow A stages
+constexpr size_t kW4Lds = 2u * kW4Stages * kW4StageBytes;  // 128 KB
+constexpr int kW4MinKTiles = 10;                           // the store schedule spans K tiles 0 .. 9
+
+// Output columns come in up to two segments (the forward pass writes y and z
+// in one launch): column tile ct < seg[0].tiles writes columns 256 ct .. of
+// seg[0].C, the others columns 256 (ct - seg[0].tiles) .. of seg[1].C.  B row
+// 256 ct + c feeds column c of column tile ct in either case, so B stacks the
+// two segments' rows with segment 1 starting at row 256 seg[0].tiles.
+// Sizes are 32-bit (the host checks that they fit).
+struct W4Seg {
+  uint16_t* C;  // [M][ldc]
+  int ldc, cols;
+  int tiles;    // ceil(cols / 256)
+};
+
+struct W4Gemm {
+  const uint16_t* A;  // [M][lda]
+  int lda, M, K;
+  const uint16_t* B;  // [rows_b][ldb]
+  int ldb, rows_b;
+  W4Seg seg[2];       // seg[1].tiles == 0 when unused
+  int tiles_n;        // seg[0].tiles + seg[1].tiles
+  int tiles;          // ceil(M / 256) * tiles_n
+};
+
+typedef __attribute__((address_space(3))) void w4_lds_void;
+typedef __attribute__((address_space(3))) u32x4 w4_lds_u32x4;
+
+constexpr uint32_t kW4Oob = 0x80000000u;  // a buffer offset past every range
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t w4_rsrc(const void* base, int64_t bytes) {
+  const int nrec = bytes <= 0 ? 0 : (bytes > 0x7FFFFFFF ? 0x7FFFFFFF : static_cast<int>(bytes));
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), nrec, 0x00020000);
+}
+
+// s_waitcnt lgkmcnt(0) + s_barrier with the fragments of the following MFMAs
+// passed through it: MFMAs have no memory side effects, so without this data
+// dependence the compiler may issue them ahead of the barrier.  Global
+// operations stay in flight (a workgroup fence would wait for them).
+struct W4Frags {
+  u32x4 a[4], b[4];
+};
+
+__device__ __forceinline__ void w4_lds_barrier(W4Frags& f) {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier"
+               : "+v"(f.a[0]), "+v"(f.a[1]), "+v"(f.a[2]), "+v"(f.a[3]), "+v"(f.b[0]), "+v"(f.b[1]), "+v"(f.b[2]),
+                 "+v"(f.b[3])
+               :
+               : "memory");
+}
+
+// Keeps the fragment reads of the next step in this basic block: without a
+// use here the compiler sinks them past the branch that follows, next to the
+// MFMAs that consume them.
+__device__ __forceinline__ void w4_pin(W4Frags& f) {
+  asm volatile(""
+               : "+v"(f.a[0]), "+v"(f.a[1]), "+v"(f.a[2]), "+v"(f.a[3]), "+v"(f.b[0]), "+v"(f.b[1]), "+v"(f.b[2]),
+                 "+v"(f.b[3]));
+}
+
+// Orders the MFMAs issued so far before whatever follows (a barrier): without
+// a use of their results the compiler may move them past it.
+__device__ __forceinline__ void w4_pin_acc(f32x16 (&acc)[4][4]) {
+  asm volatile(""
+               : "+a"(acc[0][0]), "+a"(acc[0][1]), "+a"(acc[0][2]), "+a"(acc[0][3]), "+a"(acc[1][0]), "+a"(acc[1][1]),
+                 "+a"(acc[1][2]), "+a"(acc[1][3]), "+a"(acc[2][0]), "+a"(acc[2][1]), "+a"(acc[2][2]), "+a"(acc[2][3]),
+                 "+a"(acc[3][0]), "+a"(acc[3][1]), "+a"(acc[3][2]), "+a"(acc[3][3]));
+}
+
+// s_waitcnt vmcnt(N), other counters untouched (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void w4_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// VMEM operations issued after the last copy of step h + 1 by the time step
+// (h, 1) waits, for K tile T of a tile (T = 10 stands for every T >= 10).
+// Copies of step h + 3 go out at MFMAs 0, 4, 8, 12 of step (h, 0) and 2, 6,
+// 10, 14 of step (h, 1); during K tiles 0 .. 7 stores go out at the odd MFMAs
+// of both steps.  After copy 7 of step h + 1 (issued in step (h - 2, 1)) come
+// the store at MFMA 15 of that step, all of K tile h - 1 and step (h, 0).
+constexpr bool w4_drip(int T) { return T >= 0 && T < 8; }
+template <int T>
+constexpr int w4_vm_allow() {
+  return (w4_drip(T - 2) ? 1 : 0) + 8 + (w4_drip(T - 1) ? 16 : 0) + 4 + (w4_drip(T) ? 8 : 0);
+}
+
+// ------------------------------ per-lane state ------------------------------
+struct W4Lane {
+  int lane, wave, wm, wn;
+  uint32_t a0, a1, b0, b1;  // fragment byte addresses, stage 0, steps 0 and 1
+  uint32_t lds;             // dynamic LDS base
+  int va[4], vb[4];         // A and B copy offsets (k = 0) of blocks 4 wave + q
+  int kchunk;               // 8 * logical chunk this lane copies
+};
+
+// Fragment chunk of lane `lane` for step kk (0, 1), fragment 0, stage 0, in a
+// wave tile starting at row `wrow`; fragment i adds 2048 i, stage s 16384 s.
+__device__ __forceinline__ uint32_t w4_frag_off(int wrow, int lane, int kk) {
+  const int lr = lane & 31, lh = lane >> 5;
+  const int phys = (2 * kk + lh) ^ ((lr >> 2) & 3);
+  return static_cast<uint32_t>(wrow * 64 + lr * 64 + phys * 16);
+}
+
+// Lane L of copy block j lands at row 16 j + L / 4, physical chunk L % 4, so
+// it fetches logical chunk (L % 4) ^ ((L / 16) % 4).
+__device__ __forceinline__ int w4_copy_off(int64_t ld, int lane, int j, int& kchunk) {
+  const int c = (lane & 3) ^ ((lane >> 4) & 3);
+  kchunk = 8 * c;
+  return static_cast<int>((16 * j + (lane >> 2)) * ld * 2) + 16 * c;
+}
+
+__device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
+  W4Lane L;
+  const int tid = threadIdx.x;
+  L.lane = tid & 63;
+  L.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  L.wm = L.wave >> 1;
+  L.wn = L.wave & 1;
+  L.lds = __builtin_amdgcn_groupstaticsize();
+  L.a0 = L.lds + w4_frag_off(L.wm * 128, L.lane, 0);
+  L.a1 = L.lds + w4_frag_off(L.wm * 128, L.lane, 1);
+  L.b0 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 0);
+  L.b1 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 1);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = L.wave * 4 + q;
+    L.va[q] = w4_copy_off(g.lda, L.lane, j, L.kchunk);
+    L.vb[q] = w4_copy_off(g.ldb, L.lane, j, L.kchunk);
+  }
+  return L;
+}
+
+// ------------------------------ tile cursor --------------------------------
+// This workgroup's tiles are p, p + G, p + 2 G, ... (G = grid size); tile
+// index x is row tile x / tiles_n, column tile x % tiles_n.
+struct W4Cursor {
+  int q, rt, ct;
+};
+
+__device__ __forceinline__ void w4_next_tile(W4Cursor& c, int dct, int drt, int tiles_n) {
+  c.q += 1;
+  c.ct += dct;
+  c.rt += drt;
+  const bool carry = c.ct >= tiles_n;
+  c.ct = carry ? c.ct - tiles_n : c.ct;
+  c.rt = carry ? c.rt + 1 : c.rt;
+}
+
+struct W4CopyDesc {
+  __amdgpu_buffer_rsrc_t ra, rb;
+};
+
+__device__ __forceinline__ W4CopyDesc w4_copy_desc(const W4Gemm& g, const W4Cursor& c, int n_my) {
+  W4CopyDesc d;
+  const bool live = c.q < n_my;
+  const int64_t row0 = static_cast<int64_t>(c.rt) * kW4Tile;
+  const int64_t brow0 = static_cast<int64_t>(c.ct) * kW4Tile;
+  d.ra = w4_rsrc(g.A + row0 * g.lda, live ? (g.M - row0) * int64_t(g.lda) * 2 : 0);
+  d.rb = w4_rsrc(g.B + brow0 * g.ldb, live ? (g.rows_b - brow0) * int64_t(g.ldb) * 2 : 0);
+  return d;
+}
+
+// Copy the K tile starting at k0 of the tile `d` into stage byte offsets
+// (sa, sb) of A and B.  Chunks at k >= K get an offset past every range (set
+// with a shift, not a select, so the compiler keeps the copies branch-free).
+__device__ __forceinline__ void w4_copy(const W4Gemm& g, const W4Lane& L, const W4CopyDesc& d, int k0,
+                                        uint32_t sa, uint32_t sb) {
+  // bit 31 set iff k0 + kchunk >= K
+  const uint32_t oob = ~static_cast<uint32_t>(k0 + L.kchunk - g.K) & kW4Oob;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t vo = static_cast<uint32_t>(L.va[q] + 2 * k0) | oob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        d.ra, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(sa + (L.wave * 4 + q) * 1024u)), 16,
+        static_cast<int>(vo), 0, 0, 0);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t vo = static_cast<uint32_t>(L.vb[q] + 2 * k0) | oob;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        d.rb, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(sb + (L.wave * 4 + q) * 1024u)), 16,
+        static_cast<int>(vo), 0, 0, 0);
+  }
+}
+
+// The copy stream: the next (tile, K tile) to copy.
+struct W4CopyCursor {
+  W4Cursor c;
+  int k;  // K tile
+  W4CopyDesc d;
+};
+
+__device__ __forceinline__ void w4_copy_advance(const W4Gemm& g, W4CopyCursor& cc, int kt, int n_my, int dct,
+                                                int drt) {
+  cc.k += 1;
+  if (cc.k == kt) {
+    cc.k = 0;
+    w4_next_tile(cc.c, dct, drt, g.tiles_n);
+    cc.d = w4_copy_desc(g, cc.c, n_my);
+  }
+}
+
+// ------------------------------ output side --------------------------------
+// The bf16 result of a wave tile, as packed column pairs: for accumulator
+// block (i, j) and row group gr, the even lane of a pair holds rows R, R + 1
+// of columns C, C + 1 and the odd lane rows R + 2, R + 3 (one DPP swap).
+struct W4Out {
+  __amdgpu_buffer_rsrc_t rc;  // base at the wave tile's first element
+  uint32_t vj[4];             // lane byte offset for column block j, or out of range
+  uint32_t rstride;           // ldc * 2
+};
+
+__device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, const W4Cursor& c, bool live) {
+  W4Out o;
+  const int seg = c.ct >= g.seg[0].tiles ? 1 : 0;
+  uint16_t* C = seg ? g.seg[1].C : g.seg[0].C;
+  const int64_t ldc = seg ? g.seg[1].ldc : g.seg[0].ldc;
+  const int64_t cols = seg ? g.seg[1].cols : g.seg[0].cols;
+  const int64_t wrow0 = static_cast<int64_t>(c.rt) * kW4Tile + L.wm * 128;
+  const int64_t wcol0 = static_cast<int64_t>(seg ? c.ct - g.seg[0].tiles : c.ct) * kW4Tile + L.wn * 128;
+  o.rc = w4_rsrc(C + wrow0 * ldc + wcol0, live ? ((g.M - wrow0) * ldc - wcol0) * 2 : 0);
+  o.rstride = static_cast<uint32_t>(ldc * 2);
+  const int lr = L.lane & 31, lh = L.lane >> 5, odd = L.lane & 1;
+  const uint32_t rl = static_cast<uint32_t>(4 * lh + 2 * odd) * o.rstride;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int cl = j * 32 + (lr & ~1);
+    o.vj[j] = wcol0 + cl + 1 < cols ? rl + 2u * static_cast<uint32_t>(cl) : kW4Oob;
+  }
+  return o;
+}
+
+__device__ __forceinline__ void w4_pack(const f32x16 (&acc)[4][4], int lane, uint32_t (&out)[128]) {
+  const bool odd = (lane & 1) != 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int gr = 0; gr < 4; ++gr) {
+        const uint32_t p01 = pack_bf16x2(acc[i][j][4 * gr + 0], acc[i][j][4 * gr + 1]);
+        const uint32_t p23 = pack_bf16x2(acc[i][j][4 * gr + 2], acc[i][j][4 * gr + 3]);
+        const uint32_t snd = odd ? p01 : p23;
+        const uint32_t rcv = static_cast<uint32_t>(
+            __builtin_amdgcn_mov_dpp(static_cast<int>(snd), 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
+        const int e = ((i * 4 + j) * 4 + gr) * 2;
+        // even lane: rows R, R+1 of columns C (own), C+1 (partner);
+        // odd lane: rows R+2, R+3 of columns C-1 (partner), C (own)
+        out[e] = odd ? __builtin_amdgcn_perm(p23, rcv, 0x05040100u) : __builtin_amdgcn_perm(rcv, p01, 0x05040100u);
+        out[e + 1] = odd ? __builtin_amdgcn_perm(p23, rcv, 0x07060302u) : __builtin_amdgcn_perm(rcv, p01, 0x07060302u);
+      }
+}
+
+// Stores of accumulator blocks (i, j) = (B / 4, B % 4) for B in [B0, B0 + NB).
+template <int B0, int NB>
+__device__ __forceinline__ void w4_store(const W4Out& o, const uint32_t (&out)[128]) {
+#pragma unroll
+  for (int b = B0; b < B0 + NB; ++b) {
+    const int i = b >> 2, j = b & 3;
+#pragma unroll
+    for (int gr = 0; gr < 4; ++gr)
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const uint32_t vo = o.vj[j] + static_cast<uint32_t>(i * 32 + gr * 8 + w) * o.rstride;
+        __builtin_amdgcn_raw_buffer_store_b32(out[(b * 4 + gr) * 2 + w], o.rc, static_cast<int>(vo), 0, 0);
+      }
+  }
+}
+
+// ------------------------------ MFMA steps ---------------------------------
+__device__ __forceinline__ void w4_read(uint32_t a, uint32_t b, W4Frags& f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(a + i * 2048));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) f.b[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(b + i * 2048));
+}
+
+// One K tile, T = its index in the tile (10: any T >= 10); h = flat step.
+// The source order below is the issue order: this header is compiled with
+// the machine scheduler off, so MFMAs, LDS reads, copies and stores stay
+// interleaved as written.  Copies and stores are spread out because the
+// vector memory unit takes about 16 clocks per 64-lane 16-byte copy: issued
+// in bursts they stall the in-order issue of the MFMAs behind them.
+template <int T>
+__device__ __forceinline__ void w4_copy_one(const W4Lane& L, const W4CopyCursor& cc, int c, uint32_t oob,
+                                            int k3, uint32_t s3) {
+  const int q = c & 3;
+  const bool is_a = c < 4;
+  const uint32_t vo = static_cast<uint32_t>((is_a ? L.va[q] : L.vb[q]) + 2 * k3) | oob;
+  const uint32_t dst = L.lds + (is_a ? 0u : static_cast<uint32_t>(kW4BBase)) + s3 + (L.wave * 4 + q) * 1024u;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(is_a ? cc.d.ra : cc.d.rb,
+                                           reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
+                                           static_cast<int>(vo), 0, 0, 0);
+}
+
+// Store n (0 .. 15) of K tile T: block 2 T + n / 8, row group (n / 2) % 4, row n % 2.
+template <int T>
+__device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&out)[128], int n) {
+  const int b = 2 * T + (n >> 3), gr = (n >> 1) & 3, w = n & 1;
+  const int bi = b >> 2, bj = b & 3;
+  const uint32_t vo = od.vj[bj] + static_cast<uint32_t>(bi * 32 + gr * 8 + w) * od.rstride;
+  __builtin_amdgcn_raw_buffer_store_b32(out[(b * 4 + gr) * 2 + w], od.rc, static_cast<int>(vo), 0, 0);
+}
+
+template <int T>
+__device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc, int kt,
+                                         int n_my, int dct, int drt, const W4Out& od,
+                                         const uint32_t (&out)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4]) {
+  const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
+  const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
+  const uint32_t s3 = static_cast<uint32_t>((h + 3) & 3) * kW4StageBytes;
+  const f32x16 zero = {};
+  const int k3 = cc.k * kW4K;
+  const uint32_t oob = ~static_cast<uint32_t>(k3 + L.kchunk - g.K) & kW4Oob;
+  // step 0: MFMAs on f[0]; reads of f[1]; copies 0 .. 3 of step h + 3
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int fa = i >> 2, fb = i & 3;
+    acc[fa][fb] = mfma32x32x16(f[0].a[fa], f[0].b[fb], T == 0 ? zero : acc[fa][fb]);
+    if (i < 4) {
+      f[1].a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.a1 + s0 + i * 2048));
+    } else if (i < 8) {
+      f[1].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b1 + s0 + (i - 4) * 2048));
+    }
+    if (i % 4 == 0) w4_copy_one<T>(L, cc, i / 4, oob, k3, s3);
+    if constexpr (w4_drip(T)) {
+      if (i % 2 == 1) w4_store_one<T>(od, out, i / 2);
+    }
+  }
+  w4_pin_acc(acc);
+  // step 1: MFMAs on f[1]; reads of f[0] for step h + 1; copies 4 .. 7
+  w4_wait_vm<w4_vm_allow<T>()>();
+  w4_lds_barrier(f[1]);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int fa = i >> 2, fb = i & 3;
+    acc[fa][fb] = mfma32x32x16(f[1].a[fa], f[1].b[fb], acc[fa][fb]);
+    if (i < 4) {
+      f[0].a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.a0 + s1 + i * 2048));
+    } else if (i < 8) {
+      f[0].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b0 + s1 + (i - 4) * 2048));
+    }
+    if (i % 4 == 2) w4_copy_one<T>(L, cc, 4 + i / 4, oob, k3, s3);
+    if constexpr (w4_drip(T)) {
+      if (i % 2 == 1) w4_store_one<T>(od, out, 8 + i / 2);
+    }
+  }
+  w4_pin(f[0]);
+  w4_copy_advance(g, cc, kt, n_my, dct, drt);
+}
+
+// The whole persistent GEMM for this workgroup.  Launch with kW4Threads
+// threads, kW4Lds bytes of dynamic LDS and at most one workgroup per CU.
+__device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
+  const int G = static_cast<int>(gridDim.x);
+  const int p = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
+  if (p >= g.tiles) return;
+  const int n_my = (g.tiles - p + G - 1) / G;
+  const int kt = static_cast<int>(ceil_div(g.K, kW4K));
+  const int dct = G % g.tiles_n, drt = G / g.tiles_n;
+  const W4Lane L = w4_lane(g);
+
+  W4CopyCursor cc;
+  cc.c = W4Cursor{0, p / g.tiles_n, p % g.tiles_n};
+  cc.k = 0;
+  cc.d = w4_copy_desc(g, cc.c, n_my);
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    w4_copy(g, L, cc.d, cc.k * kW4K, L.lds + s * kW4StageBytes, L.lds + kW4BBase + s * kW4StageBytes);
+    w4_copy_advance(g, cc, kt, n_my, dct, drt);
+  }
+  W4Frags f[2];
+  f32x16 acc[4][4];
+  uint32_t out[128];
+#pragma unroll
+  for (int e = 0; e < 128; ++e) out[e] = 0u;
+  W4Cursor oc{0, p / g.tiles_n, p % g.tiles_n};
+  W4Out od = w4_out_desc(g, L, oc, false);  // nothing to store before the first tile
+  w4_wait_vm<0>();
+  w4_lds_barrier(f[1]);
+  w4_read(L.a0, L.b0, f[0]);
+  int h = 0;
+  for (int q = 0; q < n_my; ++q) {
+    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, dct, drt, od, out, f, acc);
+    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, dct, drt, od, out, f, acc);
+    h += kt;
+    od = w4_out_desc(g, L, oc, true);
+    w4_pack(acc, L.lane, out);
+    w4_next_tile(oc, dct, drt, g.tiles_n);
+  }
+  w4_store<0, 16>(od, out);
+  w4_wait_vm<0>();  // no copy may still be writing LDS when the workgroup ends
+}
+
+}  // namespace compact

@@ -29,12 +29,12 @@ struct FwdParams {
   int64_t ldy;
   uint16_t* z;
   int64_t ldz;
-  const uint16_t* pt;  // materialised P^T (r rows, K = n contiguous), or null
+  const uint16_t* pt;  // materialised P^T = bf16(pscale G^T) (r rows, K = n contiguous), or null
   int64_t ldpt;
   int64_t T, n, m, r;
   PhiloxKey key;
   int identity;
-  float zscale;      // fp32(1/sqrt(r)), 1 for the identity projection
+  float pscale;      // fp32(1/sqrt(r)) applied to G before rounding; 1 for the identity
   int tiles_y;       // column tiles covering y (m columns)
   int tiles_z;       // column tiles covering z (r columns)
 };
@@ -61,17 +61,17 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
       KMajorLoader<BN, NT> lb{p.pt, p.ldpt, p.r, p.n, col0};
       gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
     } else {
-      PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.identity};
+      PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.identity, p.pscale};
       gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
     }
-    store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.z, p.ldz, p.T, p.r, row0, col0, p.zscale);
+    store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.z, p.ldz, p.T, p.r, row0, col0, 1.0f);
   }
 }
 
-// P^T panel for the forward: out[j * ld + i] = bf16(G[i][j]) (unscaled), or the
-// identity.  One thread per quad (4 rows of one column); columns i >= n of the
-// padded rows are written as zero.
-__global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identity,
+// P^T panel for the forward: out[j * ld + i] = bf16(scale * G[i][j]), or the
+// identity (scale 1).  One thread per quad (4 rows of one column); columns
+// i >= n of the padded rows are written as zero.
+__global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identity, float scale,
                                  uint16_t* out, int64_t ld) {
   const int64_t quads_per_row = ld / 4;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -83,6 +83,7 @@ __global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identi
       for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
     } else {
       pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
+      for (int e = 0; e < 4; ++e) g[e] = g[e] * scale;
     }
     for (int e = 0; e < 4; ++e)
       if (i0 + e >= n) g[e] = 0.0f;
@@ -91,6 +92,26 @@ __global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identi
   v.x = pack_bf16x2(g[0], g[1]);
   v.y = pack_bf16x2(g[2], g[3]);
   *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
+}
+
+// out[c * ldo + i] = in[i * ldi + c] for i < rows, c < cols (bf16), through a
+// 64 x 64 LDS tile; 64 x 4 threads, each row of 64 threads reads and writes
+// 128 contiguous bytes.
+__global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* in, int64_t ldi, int64_t rows, int64_t cols,
+                                                        uint16_t* out, int64_t ldo, int tiles_c) {
+  __shared__ uint16_t tile[64][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x / tiles_c) * 64;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x % tiles_c) * 64;
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t i = r0 + y, c = c0 + tx;
+    tile[y][tx] = (i < rows && c < cols) ? in[i * ldi + c] : uint16_t(0);
+  }
+  __syncthreads();
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t c = c0 + y, i = r0 + tx;
+    if (c < cols && i < rows) out[c * ldo + i] = tile[tx][y];
+  }
 }
 
 // Unscaled fp32 stream G (n x r, leading dimension ld): the standalone P tile

@@ -1,0 +1,62 @@
+// The persistent four-wave bf16 GEMM kernel and its launcher.  Built as its
+// own translation unit with -mllvm -enable-misched=false and
+// -mllvm -enable-post-misched=false: the K-step code in gemm_w4.hpp is written
+// in issue order and must not be rescheduled.
+#include "gemm_w4_launch.hpp"
+
+#include <atomic>
+
+namespace compact {
+
+__global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) { gemm_w4_persistent(g); }
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
+std::atomic<bool> g_lds_set[kMaxDevices];   // dynamic LDS limit raised for k_gemm_w4
+
+bool fits_offsets(int64_t ld, int64_t K) {
+  // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
+  return ld > 0 && (int64_t(kW4Tile) * ld + K) * 2 < (int64_t(1) << 31);
+}
+
+}  // namespace
+
+bool gemm_w4_eligible(int64_t M, int64_t K, int64_t lda, int64_t ldb, int64_t rows_b, int64_t ldc0,
+                      int64_t cols0, int64_t ldc1, int64_t cols1) {
+  if (M < 1 || K % 8 != 0 || K < int64_t(kW4MinKTiles) * kW4K) return false;
+  if (lda % 8 != 0 || ldb % 8 != 0 || lda < K || ldb < K) return false;
+  if (!fits_offsets(lda, K) || !fits_offsets(ldb, K) || !fits_offsets(ldc0, 0)) return false;
+  if (cols0 < 1 || cols0 % 2 != 0) return false;
+  if (cols1 != 0 && (cols1 % 2 != 0 || !fits_offsets(ldc1, 0))) return false;
+  const int64_t limit = int64_t(1) << 30;
+  if (M > limit || rows_b > limit || ldc0 > limit || ldc1 > limit) return false;
+  return true;
+}
+
+hipError_t gemm_w4_launch(const W4Gemm& g, hipStream_t stream) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  int cus = g_cus[dev].load(std::memory_order_relaxed);
+  if (cus == 0) {
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cus = cus > 0 ? cus : 1;
+    g_cus[dev].store(cus, std::memory_order_relaxed);
+  }
+  if (!g_lds_set[dev].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_w4), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(kW4Lds));
+    if (e != hipSuccess) return e;
+    g_lds_set[dev].store(true, std::memory_order_release);
+  }
+  if (g.tiles <= 0) return hipSuccess;
+  const int grid = g.tiles < cus ? g.tiles : cus;
+  hipLaunchKernelGGL(k_gemm_w4, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, g);
+  return hipGetLastError();
+}
+
+}  // namespace compact

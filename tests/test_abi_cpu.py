@@ -75,9 +75,10 @@ def test_status_strings(lib):
 
 
 def test_workspace_sizes(lib):
-    # P^T panel: r rows of round_up(n, 64) bf16 values (+ alignment slack)
-    assert lib.compact_fwd_workspace_bytes(1024, 128, 1) >= 128 * 1024 * 2
-    assert lib.compact_fwd_workspace_bytes(1024, 128, 0) == 0
+    # [W^T; P^T]: round_up(m, 256) + r rows of round_up(n, 64) bf16 values
+    assert lib.compact_fwd_workspace_bytes(1024, 1000, 128, 1) >= (1024 + 128) * 1024 * 2
+    assert lib.compact_fwd_workspace_bytes(1000, 2736, 128, 1) >= (2816 + 128) * 1024 * 2
+    assert lib.compact_fwd_workspace_bytes(1024, 1024, 128, 0) == 0
     assert lib.compact_bwd_workspace_bytes(65536, 1024, 1024, 128, 1) > 128 * 1024 * 4
     assert lib.compact_step_workspace_bytes(1024, 1024, 128, 1) >= 128 * 1024 * 2
     assert lib.compact_step_workspace_bytes(256, 512, 32, 0) >= 32 * 512 * 4

@@ -51,7 +51,7 @@ def test_forward_parity(shape, use_ws):
     xd, Wd = to_dev(x, dt, ld_for(n, dt)), to_dev(W, dt, ld_for(m, dt))
     y = empty(T, m, dt, ld_for(m, dt))
     z = empty(T, r, dt, ld_for(r, dt))
-    ws = workspace(cp.fwd_workspace_bytes(n, r, CODE[dt])) if use_ws else None
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, CODE[dt])) if use_ws else None
     cp.compact_fwd(xd, Wd, y, z, seed, ws=ws)
     torch.cuda.synchronize()
     y_ref, z_ref = oc.ref_fwd(x, W, seed, r)

@@ -77,16 +77,15 @@ def test_in_gemm_stream_x_identity(dtype, use_ws, n, r, seed):
     W = to_dev(np.zeros((n, m), np.float32), dtype, ld=ld_for(m, dtype))
     y = empty(n, m, dtype, ld=ld_for(m, dtype))
     z = empty(n, r, dtype, ld=ld_for(r, dtype), fill=7.0)
-    ws = workspace(cp.fwd_workspace_bytes(n, r, cp.BF16 if dtype == "bf16" else cp.F32)) if use_ws else None
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, cp.BF16 if dtype == "bf16" else cp.F32)) if use_ws else None
     cp.compact_fwd(x, W, y, z, seed, ws=ws)
     torch.cuda.synchronize()
     got = to_np_f32(z)
     G = ps.gaussian_raw(seed, n, r)
     s = np.float32(1.0 / np.sqrt(np.float64(r)))
-    if dtype == "f32":
-        exp = G * s
-    else:
-        exp = bf16_round(bf16_round(G) * s)
+    # fp32: z = (x G) s;  bf16: P = G s is formed in fp32 and rounded to bf16
+    # once, and x = I passes it through the MFMA unchanged
+    exp = G * s if dtype == "f32" else bf16_round(G * s)
     assert np.array_equal(got.view(np.uint32), exp.astype(np.float32).view(np.uint32))
 
 
