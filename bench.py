@@ -295,7 +295,7 @@ def main():
             traffic = rec.get("bytes_per_launch")
     nl = len(wl.layers)
     roofline = {
-        "bound": "mfma", "kernel": "k_fwd_bf16 (fused [y|z] = x[W|P], incl. its P^T panel launch)",
+        "bound": "mfma", "kernel": "compact_fwd: k_gemm_w4<0> ([y|z] = x [W^T; P^T]^T) with its W^T and P^T staging launches",
         "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
         "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
         "flops_per_launch": flops["fwd"] / nl,

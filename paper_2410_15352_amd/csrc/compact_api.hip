@@ -104,12 +104,54 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
   return s;
 }
 
+// Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp): 128 x 256
+// tiles, about one workgroup per CU, splits of whole 32-token K tiles.
+SplitPlan ghat_w4_plan(int64_t tokens, int64_t r, int64_t m) {
+  SplitPlan s;
+  s.tiles_r = static_cast<int>(ceil_div(r, kGhTm));
+  s.tiles_m = static_cast<int>(ceil_div(m, kGhTn));
+  const int64_t tiles = int64_t(s.tiles_r) * s.tiles_m;
+  const int64_t ktiles = ceil_div(tokens > 0 ? tokens : 1, kGhK);
+  int64_t splits = (256 + tiles / 2) / tiles;
+  if (splits < 1) splits = 1;
+  if (splits > ktiles) splits = ktiles;
+  s.split_len = ceil_div(ktiles, splits) * kGhK;
+  s.splits = static_cast<int>(ceil_div(tokens > 0 ? tokens : 1, s.split_len));
+  return s;
+}
+
+// The transposing-read kernel handles the problem: 32-bit buffer offsets over
+// a split plus one K tile, and the partial-sum layout of its plan.
+bool ghat_w4_eligible(int64_t tokens, int64_t r, int64_t m, int64_t ldz, int64_t lddy) {
+  if (tokens < 1 || tokens > (int64_t(1) << 30) || r < 1 || m < 1) return false;
+  const SplitPlan sp = ghat_w4_plan(tokens, r, m);
+  const int64_t span = sp.split_len + 2 * kGhK;
+  const int64_t lim = int64_t(1) << 31;
+  return span * ldz * 2 < lim && span * lddy * 2 < lim && ldz < lim / 4 && lddy < lim / 4;
+}
+
 size_t ghat_ws_bytes(int64_t tokens, int64_t r, int64_t m) {
   const SplitPlan s = ghat_plan(tokens, r, m);
-  return size_t(s.splits) * size_t(s.tiles_r) * kGBM * size_t(s.tiles_m) * kGBN * sizeof(float);
+  const size_t a = size_t(s.splits) * size_t(s.tiles_r) * kGBM * size_t(s.tiles_m) * kGBN * sizeof(float);
+  const SplitPlan w = ghat_w4_plan(tokens, r, m);
+  const size_t b = size_t(w.splits) * size_t(w.tiles_r) * kGhTm * size_t(w.tiles_m) * kGhTn * sizeof(float);
+  return a > b ? a : b;  // either path may run (the choice depends on the leading dimensions)
 }
 
 int64_t pt_ld(int64_t n) { return round_up(n, kBK); }
+
+// G[j][c] = sum over splits, in order, of part[s][j][c].
+int launch_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t plane, int64_t r, int64_t m, float* G,
+                         hipStream_t s) {
+  if (m % 4 == 0 && aligned16(G)) {
+    hipLaunchKernelGGL(k_splitk_reduce4, dim3(static_cast<uint32_t>(ceil_div(r * (m / 4), 256))), dim3(256), 0, s,
+                       part, splits, ldp, plane, r, m, G);
+  } else {
+    hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s, part,
+                       splits, ldp, plane, r, m, G);
+  }
+  return check_launch("G^ reduce");
+}
 
 // Forward operand of the persistent GEMM, K = n contiguous: rows 0 .. m-1 hold
 // W^T, rows round_up(m, 256) .. + r - 1 hold P^T (rows in between are never
@@ -270,7 +312,7 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
     if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
     g.tiles = static_cast<int>(tiles);
-    const hipError_t e = gemm_w4_launch(g, s);
+    const hipError_t e = gemm_w4_launch(g, W4Use::kForward, s);
     if (e != hipSuccess) return fail(COMPACT_EHIP, "forward GEMM (bf16): %s", hipGetErrorString(e));
     return ok();
   }
@@ -366,7 +408,7 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
     if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
     g.tiles = static_cast<int>(tiles);
-    const hipError_t e = gemm_w4_launch(g, s);
+    const hipError_t e = gemm_w4_launch(g, W4Use::kDx, s);
     if (e != hipSuccess) return fail(COMPACT_EHIP, "dx GEMM (bf16): %s", hipGetErrorString(e));
   } else if (dx != nullptr) {
     DxParams p{};
@@ -381,7 +423,20 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), kGemmLds, s, p);
     if ((st = check_launch("dx (bf16)"))) return st;
   }
-  if (G != nullptr) {
+  if (G != nullptr && ghat_w4_eligible(tokens, r, m, ldz, lddy)) {
+    const SplitPlan sp = ghat_w4_plan(tokens, r, m);
+    GhatW4Params p{};
+    p.z = static_cast<const uint16_t*>(z); p.ldz = static_cast<int>(ldz);
+    p.dy = static_cast<const uint16_t*>(dy); p.lddy = static_cast<int>(lddy);
+    p.part = static_cast<float*>(align_ws(ws));
+    p.T = static_cast<int>(tokens); p.r = static_cast<int>(r); p.m = static_cast<int>(m);
+    p.tiles_r = sp.tiles_r; p.tiles_m = sp.tiles_m; p.splits = sp.splits;
+    p.split_len = static_cast<int>(sp.split_len);
+    const hipError_t e = ghat_w4_launch(p, s);
+    if (e != hipSuccess) return fail(COMPACT_EHIP, "G^ split-K (bf16): %s", hipGetErrorString(e));
+    const int64_t ldp = int64_t(sp.tiles_m) * kGhTn, plane = int64_t(sp.tiles_r) * kGhTm * ldp;
+    if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, s))) return st;
+  } else if (G != nullptr) {
     const SplitPlan sp = ghat_plan(tokens, r, m);
     GhatParams p{};
     p.z = static_cast<const uint16_t*>(z); p.ldz = ldz;
@@ -394,14 +449,7 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
                        dim3(kGThreads), kGhatLds, s, p);
     if ((st = check_launch("G^ split-K (bf16)"))) return st;
     const int64_t ldp = int64_t(sp.tiles_m) * kGBN, plane = int64_t(sp.tiles_r) * kGBM * ldp;
-    if (m % 4 == 0 && aligned16(G)) {
-      hipLaunchKernelGGL(k_splitk_reduce4, dim3(static_cast<uint32_t>(ceil_div(r * (m / 4), 256))), dim3(256), 0, s,
-                         static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
-    } else {
-      hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s,
-                         static_cast<const float*>(p.part), sp.splits, ldp, plane, r, m, G);
-    }
-    if ((st = check_launch("G^ reduce"))) return st;
+    if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, s))) return st;
   }
   return ok();
 }

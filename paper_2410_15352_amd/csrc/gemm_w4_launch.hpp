@@ -1,8 +1,11 @@
-// Host entry into the persistent four-wave GEMM (kernels_w4.hip, a separate
-// translation unit compiled with the machine scheduler off, see gemm_w4.hpp).
+// Host entries into the kernels of kernels_w4.hip, a separate translation
+// unit compiled with the machine scheduler off (their K steps are written in
+// issue order): the persistent four-wave GEMM (gemm_w4.hpp) and the split-K
+// G^ kernel (gemm_ghat.hpp).
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include "gemm_ghat.hpp"
 #include "gemm_w4.hpp"
 
 namespace compact {
@@ -12,7 +15,13 @@ namespace compact {
 bool gemm_w4_eligible(int64_t M, int64_t K, int64_t lda, int64_t ldb, int64_t rows_b, int64_t ldc0,
                       int64_t cols0, int64_t ldc1, int64_t cols1);
 
+// Which pass a launch serves (each has its own kernel instantiation).
+enum class W4Use { kForward, kDx };
+
 // Launches C = A B^T on `stream`, one workgroup per CU (at most one per tile).
-hipError_t gemm_w4_launch(const W4Gemm& g, hipStream_t stream);
+hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream);
+
+// G^ partials: one workgroup per (split, column tile, row tile).
+hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream);
 
 }  // namespace compact

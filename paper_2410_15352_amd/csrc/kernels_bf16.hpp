@@ -95,22 +95,48 @@ __global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identi
 }
 
 // out[c * ldo + i] = in[i * ldi + c] for i < rows, c < cols (bf16), through a
-// 64 x 64 LDS tile; 64 x 4 threads, each row of 64 threads reads and writes
-// 128 contiguous bytes.
+// 64 x 64 LDS tile.  256 threads; each moves two 16-byte chunks: loads 8
+// consecutive columns of one row, scatters them down the transposed tile, and
+// stores 8 consecutive rows of one output row.  ldi and ldo are multiples of 8
+// and both pointers 16-byte aligned; partial chunks at the edges go element
+// by element.
 __global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* in, int64_t ldi, int64_t rows, int64_t cols,
                                                         uint16_t* out, int64_t ldo, int tiles_c) {
-  __shared__ uint16_t tile[64][65];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];  // tile[c][i]; rows padded to 144 bytes
+  const int t = threadIdx.x;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x / tiles_c) * 64;
   const int64_t c0 = static_cast<int64_t>(blockIdx.x % tiles_c) * 64;
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t i = r0 + y, c = c0 + tx;
-    tile[y][tx] = (i < rows && c < cols) ? in[i * ldi + c] : uint16_t(0);
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int id = t + 256 * p, i = id >> 3, cc = (id & 7) * 8;
+    const int64_t gi = r0 + i, gc = c0 + cc;
+    uint16_t v[8];
+    if (gi < rows && gc + 8 <= cols) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(in + gi * ldi + gc);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] = static_cast<uint16_t>(w[e]);
+        v[2 * e + 1] = static_cast<uint16_t>(w[e] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (gi < rows && gc + e < cols) ? in[gi * ldi + gc + e] : uint16_t(0);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tile[cc + e][i] = v[e];
   }
   __syncthreads();
-  for (int y = ty; y < 64; y += 4) {
-    const int64_t c = c0 + y, i = r0 + tx;
-    if (c < cols && i < rows) out[c * ldo + i] = tile[tx][y];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int id = t + 256 * p, c = id >> 3, ii = (id & 7) * 8;
+    const int64_t gc = c0 + c, gi = r0 + ii;
+    if (gc >= cols) continue;
+    const u32x4 w = *reinterpret_cast<const u32x4*>(&tile[c][ii]);
+    if (gi + 8 <= rows) {
+      *reinterpret_cast<u32x4*>(out + gc * ldo + gi) = w;
+    } else {
+      for (int e = 0; e < 8 && gi + e < rows; ++e) out[gc * ldo + gi + e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+    }
   }
 }
 

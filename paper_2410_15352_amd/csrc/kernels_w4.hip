@@ -8,13 +8,20 @@
 
 namespace compact {
 
-__global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) { gemm_w4_persistent(g); }
+// One instantiation per use, so that profiles report the forward and the dx
+// GEMM separately.
+template <int USE>
+__global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
+  gemm_w4_persistent(g);
+}
+
+__global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) { ghat_w4(p); }
 
 namespace {
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
-std::atomic<bool> g_lds_set[kMaxDevices];   // dynamic LDS limit raised for k_gemm_w4
+std::atomic<bool> g_lds_set[kMaxDevices][3];  // dynamic LDS limit raised: k_gemm_w4<0>, <1>, k_ghat_w4
 
 bool fits_offsets(int64_t ld, int64_t K) {
   // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
@@ -35,7 +42,7 @@ bool gemm_w4_eligible(int64_t M, int64_t K, int64_t lda, int64_t ldb, int64_t ro
   return true;
 }
 
-hipError_t gemm_w4_launch(const W4Gemm& g, hipStream_t stream) {
+hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
@@ -47,15 +54,37 @@ hipError_t gemm_w4_launch(const W4Gemm& g, hipStream_t stream) {
     cus = cus > 0 ? cus : 1;
     g_cus[dev].store(cus, std::memory_order_relaxed);
   }
-  if (!g_lds_set[dev].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_gemm_w4), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            static_cast<int>(kW4Lds));
+  const int u = use == W4Use::kForward ? 0 : 1;
+  const void* fn = u == 0 ? reinterpret_cast<const void*>(k_gemm_w4<0>) : reinterpret_cast<const void*>(k_gemm_w4<1>);
+  if (!g_lds_set[dev][u].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kW4Lds));
     if (e != hipSuccess) return e;
-    g_lds_set[dev].store(true, std::memory_order_release);
+    g_lds_set[dev][u].store(true, std::memory_order_release);
   }
   if (g.tiles <= 0) return hipSuccess;
   const int grid = g.tiles < cus ? g.tiles : cus;
-  hipLaunchKernelGGL(k_gemm_w4, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, g);
+  if (u == 0) {
+    hipLaunchKernelGGL(k_gemm_w4<0>, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, g);
+  } else {
+    hipLaunchKernelGGL(k_gemm_w4<1>, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, g);
+  }
+  return hipGetLastError();
+}
+
+hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (!g_lds_set[dev][2].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_ghat_w4), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(kGhLds));
+    if (e != hipSuccess) return e;
+    g_lds_set[dev][2].store(true, std::memory_order_release);
+  }
+  const int64_t blocks = int64_t(p.tiles_r) * p.tiles_m * p.splits;
+  if (blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_ghat_w4, dim3(static_cast<uint32_t>(blocks)), dim3(256), kGhLds, stream, p);
   return hipGetLastError();
 }
 
