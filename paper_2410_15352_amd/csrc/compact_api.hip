@@ -534,9 +534,12 @@ int plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t 
   }
   p.panels = static_cast<int>(ceil_div(n, P.dec_bm));
   // Column groups per panel: more groups = more workgroups in flight but one
-  // more regeneration of the panel each.  Two suit a batch of layers; a lone
-  // layer splits further (up to 4) to fill the GPU.
-  int64_t groups = 2;
+  // more regeneration of the panel each.  In a batch of layers a workgroup
+  // takes at most 3 column tiles (wide layers would otherwise leave a few
+  // long-running workgroups at the end of the launch); a lone layer splits
+  // further (up to 4 groups) to fill the GPU.
+  int64_t groups = ceil_div(p.tiles_m, 3);
+  if (groups < 2) groups = 2;
   if (fill_gpu) {
     groups = ceil_div(512, p.panels);
     if (groups > 4) groups = 4;
@@ -643,18 +646,26 @@ int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, 
     hipLaunchKernelGGL(k_adam_batched, dim3(static_cast<uint32_t>(a.begin[a.count])), dim3(256), 0, s, a);
     if ((st = check_launch("Adam (batched)"))) return st;
   }
-  // decompression: consecutive layers with the same panel height, up to kBatchLayers per launch
+  // decompression: layers are independent, so they are grouped by panel height
+  // and LDS size (a launch's LDS size, the largest of its layers, sets how many
+  // workgroups share a CU), up to kBatchLayers per launch
+  std::vector<int32_t> order(static_cast<size_t>(count));
+  for (int32_t i = 0; i < count; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    if (plans[a].dec_bm != plans[b].dec_bm) return plans[a].dec_bm > plans[b].dec_bm;
+    return plans[a].dec_lds < plans[b].dec_lds;
+  });
   for (int32_t i0 = 0; i0 < count;) {
-    const int bm = plans[i0].dec_bm;
+    const int bm = plans[order[i0]].dec_bm;
+    const size_t lds = plans[order[i0]].dec_lds;
     DecBatch d{};
     d.count = 0;
     d.begin[0] = 0;
-    size_t lds = 0;
     int32_t i = i0;
-    while (i < count && d.count < kBatchLayers && plans[i].dec_bm == bm) {
-      d.layer[d.count] = plans[i].dp;
-      d.begin[d.count + 1] = d.begin[d.count] + plans[i].dp.panels * plans[i].dp.col_groups;
-      lds = std::max(lds, plans[i].dec_lds);
+    while (i < count && d.count < kBatchLayers && plans[order[i]].dec_bm == bm && plans[order[i]].dec_lds == lds) {
+      const StepPlan& P = plans[order[i]];
+      d.layer[d.count] = P.dp;
+      d.begin[d.count + 1] = d.begin[d.count] + P.dp.panels * P.dp.col_groups;
       ++d.count;
       ++i;
     }
