@@ -96,9 +96,12 @@ __device__ __forceinline__ u32x2 gh_tr_read(uint32_t addr) {
   return v;
 }
 
-// One transposing MN-major fragment (the layout of MNFrag in gemm_dtl.hpp):
-// rows n0 .. n0 + 31, k = kk * 16 + 8 (lane / 32) .. + 7, from a [K][ROWS]
-// stage at LDS byte address `stage`.
+// One MFMA fragment from a [K][ROWS] stage at LDS byte address `stage`: rows
+// n0 .. n0 + 31, k = kk * 16 + 8 (lane / 32) .. + 7.  In a 16-lane group the
+// transposing read hands output lane t, element j, the element t mod 4 of
+// source lane 4 j + t / 4; with source lane 4 j + q pointing at K row k0 + j,
+// columns n0 + 4 q .. + 3, lane t receives column n0 + t of K rows k0 .. k0 + 3.
+// Two such reads (h = 0, 1) give the 8 K values of the fragment.
 template <int ROWS>
 __device__ __forceinline__ u32x4 gh_frag(uint32_t stage, int n0, int kk, int lane) {
   const int g = lane >> 4, s = lane & 15;

@@ -9,7 +9,6 @@
 //                       LDS (Alg. 3, decompression and update)
 #pragma once
 #include "gemm_bf16.hpp"
-#include "gemm_dtl.hpp"
 
 namespace compact {
 
@@ -189,22 +188,6 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
   KMajorLoader<BN, NT> lb{p.W, p.ldw, p.n, p.m, col0};
   f32x16 acc[FM][FN];
   gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.m, lds, acc);
-  store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
-}
-
-// dx through the direct-to-LDS core (needs m % 8 == 0).
-template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) void k_dx_bf16_dtl(DxParams p) {
-  constexpr int NW = WGM * WGN;
-  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int rt = static_cast<int>(logical / p.tiles_n), ct = static_cast<int>(logical % p.tiles_n);
-  const int64_t row0 = static_cast<int64_t>(rt) * BM, col0 = static_cast<int64_t>(ct) * BN;
-  const KMajorDTL<BM, NW> la{p.dy, p.lddy, p.T, p.m, row0};
-  const KMajorDTL<BN, NW> lb{p.W, p.ldw, p.n, p.m, col0};
-  f32x16 acc[FM][FN];
-  gemm_mainloop_dtl<BM, BN, WGM, WGN, KMajorDTL<BM, NW>, KMajorDTL<BN, NW>, KFrag, KFrag>(la, lb, 0, p.m, lds, acc);
   store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.dx, p.lddx, p.T, p.n, row0, col0, 1.0f);
 }
 
