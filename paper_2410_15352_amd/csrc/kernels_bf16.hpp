@@ -238,7 +238,22 @@ __global__ void k_splitk_reduce4(const float* part, int splits, int64_t ldp, int
   const int64_t j = q / mq, c = (q % mq) * 4;
   const float* src = part + j * ldp + c;
   f32x4 s = {0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < splits; ++k) {
+  // sixteen loads in flight (the grid is small: r m / 1024 workgroups), then
+  // added in split order
+  int k = 0;
+  for (; k + 16 <= splits; k += 16) {
+    f32x4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = *reinterpret_cast<const f32x4*>(src + (k + u) * plane);
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      s.x = s.x + v[u].x;
+      s.y = s.y + v[u].y;
+      s.z = s.z + v[u].z;
+      s.w = s.w + v[u].w;
+    }
+  }
+  for (; k < splits; ++k) {
     const f32x4 v = *reinterpret_cast<const f32x4*>(src + k * plane);
     s.x = s.x + v.x;
     s.y = s.y + v.y;
