@@ -104,8 +104,8 @@ class Model:
         wf = max(cp.fwd_workspace_bytes(L.n, L.m, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
         wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
         wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
-        self.batch = [dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed, alpha=wl.alpha)
-                      for i, L in enumerate(wl.layers)]
+        self.batch = cp.prepare_layers([dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed,
+                                             alpha=wl.alpha) for i, L in enumerate(wl.layers)])
         wsz = max(wsz, cp.step_batched_workspace_bytes(self.batch))
         self.ws_f = torch.zeros(wf, dtype=torch.uint8, device=dev) if wf else None
         self.ws_b = torch.zeros(wb, dtype=torch.uint8, device=dev)
@@ -129,8 +129,7 @@ class Model:
     def upd_all(self, t):
         """Alg. 3 for every layer: batched Adam and decompression launches."""
         wl = self.wl
-        for i, d in enumerate(self.batch):
-            d["seed"] = self.seeds[i]
+        self.batch.set_seeds(self.seeds)
         self.cp.compact_step_batched(self.batch, t, wl.lr, wl.beta1, wl.beta2, wl.eps, ws=self.ws_s)
 
     def step(self, reseed_period):
@@ -164,8 +163,9 @@ def algorithmic(wl):
     return f, b
 
 
-def time_phases(model, torch, reps=2):
-    """Per-phase GPU time (ms per step) with HIP events on the launch stream."""
+def time_phases(model, torch, reps=2, step_reps=10):
+    """Per-phase GPU time (ms per step) with HIP events on the launch stream.
+    The step phase is short (under a millisecond), so it is repeated more."""
     n = len(model.wl.layers)
     stream = torch.cuda.current_stream()
     out = {}
@@ -181,12 +181,13 @@ def time_phases(model, torch, reps=2):
         fn()  # warm
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        k = step_reps if name == "step" else reps
         e0.record(stream)
-        for _ in range(reps):
+        for _ in range(k):
             fn()
         e1.record(stream)
         e1.synchronize()
-        out[name] = e0.elapsed_time(e1) / reps
+        out[name] = e0.elapsed_time(e1) / k
     return out
 
 
@@ -295,7 +296,7 @@ def main():
             traffic = rec.get("bytes_per_launch")
     nl = len(wl.layers)
     roofline = {
-        "bound": "mfma", "kernel": "compact_fwd: k_gemm_w4<0> ([y|z] = x [W^T; P^T]^T) with its W^T and P^T staging launches",
+        "bound": "mfma", "kernel": "compact_fwd: k_gemm_w4<0> ([y|z] = x [W^T; P^T]^T) with its W^T + P^T staging launch",
         "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
         "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
         "flops_per_launch": flops["fwd"] / nl,

@@ -21,6 +21,7 @@ PROJ = {"gaussian": 0, "identity": 1}
 
 __all__ = ["compact_fwd", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
            "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
+           "LayerBatch", "prepare_layers",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
            "saved_activation_elems", "CompactError", "library", "F32", "BF16"]
 
@@ -153,24 +154,52 @@ def _layer_array(layers):
     return arr
 
 
+class LayerBatch:
+    """The compact_layer array of compact_step_batched, marshalled once.  The
+    tensors must stay alive and in place; seeds change with set_seeds (the
+    seed schedule of Alg. 3) without rebuilding the array."""
+
+    def __init__(self, layers):
+        if not layers:
+            raise ValueError("empty layer list")
+        self.arr = _layer_array(layers)
+        self.count = len(layers)
+        self.w0 = layers[0]["W"]
+        self._keep = [dict(L) for L in layers]
+
+    def set_seeds(self, seeds):
+        if len(seeds) != self.count:
+            raise ValueError("one seed per layer")
+        for i, s_ in enumerate(seeds):
+            self.arr[i].seed = int(s_) & (2**64 - 1)
+
+
+def prepare_layers(layers):
+    return LayerBatch(layers)
+
+
+def _as_batch(layers):
+    return layers if isinstance(layers, LayerBatch) else LayerBatch(layers)
+
+
 def step_batched_workspace_bytes(layers, dtype=BF16):
-    arr = _layer_array(layers)
-    return int(_lib.load().compact_step_batched_workspace_bytes(arr, len(layers), dtype))
+    b = _as_batch(layers)
+    return int(_lib.load().compact_step_batched_workspace_bytes(b.arr, b.count, dtype))
 
 
 def compact_step_batched(layers, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, proj="gaussian",
                          ws=None, stream=None):
-    """Alg. 3 for many layers in a few launches.  layers: list of dicts with
-    keys W, G, M, V, seed and optional alpha (bf16 compute; W bf16 or fp32)."""
+    """Alg. 3 for many layers in a few launches.  layers: a LayerBatch, or a
+    list of dicts with keys W, G, M, V, seed and optional alpha (bf16
+    compute; W bf16 or fp32)."""
     lib = _lib.load()
-    if not layers:
+    if not isinstance(layers, LayerBatch) and not layers:
         return
-    arr = _layer_array(layers)
-    w_code = _dtype_code(layers[0]["W"])
+    b = _as_batch(layers)
+    w_code = _dtype_code(b.w0)
     wp, wb = _ws(ws)
-    st = lib.compact_step_batched(arr, len(layers), int(t), float(lr), float(beta1), float(beta2),
-                                  float(eps), PROJ[proj], BF16, w_code, wp, wb,
-                                  _stream(stream, layers[0]["W"]))
+    st = lib.compact_step_batched(b.arr, b.count, int(t), float(lr), float(beta1), float(beta2),
+                                  float(eps), PROJ[proj], BF16, w_code, wp, wb, _stream(stream, b.w0))
     _check("compact_step_batched", st)
 
 

@@ -47,7 +47,6 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblk) {
 
 // Several layers per launch: block b belongs to the layer l with
 // begin[l] <= b < begin[l + 1] (begin[0] = 0, begin[count] = grid size).
-constexpr int kBatchLayers = 16;
 
 __device__ __forceinline__ int batch_layer_of(const int* begin, int count, int b) {
   int lo = 0, hi = count - 1;

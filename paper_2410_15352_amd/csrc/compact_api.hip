@@ -247,10 +247,17 @@ size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t
   return ghat_ws_bytes(tokens, r, m) + kWsAlign;
 }
 
+// Step scratch of one layer: N [r][n_ld(m)] (compute dtype), then for bf16
+// compute the P^T panel [r][pt_ld(n)] bf16.
+static size_t step_layer_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
+  size_t b = round_up(static_cast<int64_t>(size_t(r) * size_t(n_ld(m)) * elem_size(dtype)), kWsAlign);
+  if (dtype == COMPACT_BF16) b += round_up(static_cast<int64_t>(size_t(r) * size_t(pt_ld(n)) * 2), kWsAlign);
+  return b;
+}
+
 size_t compact_step_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
-  (void)n;
-  if (m < 1 || r < 1) return 0;
-  return size_t(r) * size_t(n_ld(m)) * elem_size(dtype) + kWsAlign;
+  if (n < 1 || m < 1 || r < 1) return 0;
+  return step_layer_bytes(n, m, r, dtype) + kWsAlign;
 }
 
 static void* align_ws(void* ws) {
@@ -294,14 +301,15 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     // persistent GEMM over [W^T; P^T]: y in the first column tiles, z after
     uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
     const int64_t mp = round_up(m, kW4Tile);
-    const int tr = static_cast<int>(ceil_div(n, 64)), tc = static_cast<int>(ceil_div(m, 64));
-    hipLaunchKernelGGL(k_transpose_bf16, dim3(static_cast<uint32_t>(int64_t(tr) * tc)), dim3(256), 0, s,
-                       static_cast<const uint16_t*>(W), ldw, n, m, bs, ldb, tc);
-    if ((st = check_launch("W^T (bf16)"))) return st;
-    const int64_t quads = (ldb / 4) * r;
-    hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0, s,
-                       key, n, r, identity, pscale, bs + mp * ldb, ldb);
-    if ((st = check_launch("P panel (bf16)"))) return st;
+    FwdStage fs{};
+    fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = m;
+    fs.wt = bs; fs.pt = bs + mp * ldb; fs.ldb = ldb; fs.r = r;
+    fs.key = key; fs.identity = identity; fs.pscale = pscale;
+    fs.tiles_c = static_cast<int>(ceil_div(m, 64));
+    fs.pt_blocks = static_cast<int>(ceil_div((ldb / 4) * r, 256));
+    const int64_t stage_blocks = fs.pt_blocks + ceil_div(n, 64) * fs.tiles_c;
+    hipLaunchKernelGGL(k_fwd_stage_bf16, dim3(static_cast<uint32_t>(stage_blocks)), dim3(256), 0, s, fs);
+    if ((st = check_launch("W^T and P^T staging (bf16)"))) return st;
     W4Gemm g{};
     g.A = static_cast<const uint16_t*>(x); g.lda = static_cast<int>(ldx);
     g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
@@ -458,13 +466,12 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
 
 namespace {
 
-// Per-layer launch description of Alg. 3 (Adam + decompression).
+// Per-layer launch description of Alg. 3 (Adam + P^T staging, decompression).
 struct StepPlan {
-  AdamParams ap;
-  int adam_blocks;
-  DecParams dp;
-  int dec_bm;       // 64 or 32 rows per P panel; 0 = fp32 path
-  size_t dec_lds;
+  AdamLayer al;
+  int adam_blocks, pt_blocks;
+  DecW4Layer dl;
+  int dec_tiles;
 };
 
 int validate_step(const void* W, int64_t ldw, const float* G, const float* M, const float* V, int64_t n,
@@ -482,87 +489,100 @@ int validate_step(const void* W, int64_t ldw, const float* G, const float* M, co
   if (!(lr >= 0.0) || !std::isfinite(lr) || !std::isfinite(alpha)) return fail(COMPACT_EINVAL, "bad lr or alpha");
   if (dtype == COMPACT_F32 && w_dtype != COMPACT_F32)
     return fail(COMPACT_EUNSUPPORTED, "fp32 decompression needs fp32 W");
+  if (dtype == COMPACT_BF16 && !dec_w4_eligible(n, m, r, ldw, n_ld(m), pt_ld(n), w_dtype == COMPACT_F32))
+    return fail(COMPACT_EUNSUPPORTED, "decompression: shape too large for 32-bit offsets (n=%lld m=%lld r=%lld ldw=%lld)",
+                (long long)n, (long long)m, (long long)r, (long long)ldw);
   return COMPACT_OK;
 }
 
-constexpr size_t kTilesLds = 2u * 128 * kBK * sizeof(uint16_t);  // N tile stages of the decompression
+// Adam constants of one step: 1 - beta and the bias corrections formed in fp64
+// and rounded once.
+AdamConsts adam_consts(int64_t t, double beta1, double beta2, double eps, int proj, int dtype) {
+  AdamConsts c{};
+  c.b1 = static_cast<float>(beta1);
+  c.b2 = static_cast<float>(beta2);
+  c.omb1 = static_cast<float>(1.0 - beta1);
+  c.omb2 = static_cast<float>(1.0 - beta2);
+  c.bc1 = static_cast<float>(1.0 - std::pow(beta1, static_cast<double>(t)));
+  c.bc2 = static_cast<float>(1.0 - std::pow(beta2, static_cast<double>(t)));
+  c.eps = static_cast<float>(eps);
+  c.n_f32 = dtype == COMPACT_F32;
+  c.identity = proj == COMPACT_PROJ_IDENTITY;
+  return c;
+}
 
-int plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n, int64_t m, int64_t r,
-              uint64_t seed, int64_t t, double lr, double beta1, double beta2, double eps, double alpha,
-              int proj, int dtype, int w_dtype, void* Nbuf, bool fill_gpu, StepPlan& P) {
-  const int64_t ldn = n_ld(m);
-  AdamParams& ap = P.ap;
-  ap = AdamParams{};
-  ap.G = G; ap.M = M; ap.V = V; ap.N = Nbuf; ap.ldn = ldn;
-  ap.n_f32 = dtype == COMPACT_F32;
-  ap.r = r; ap.m = m;
-  ap.b1 = static_cast<float>(beta1);
-  ap.b2 = static_cast<float>(beta2);
-  ap.omb1 = static_cast<float>(1.0 - beta1);
-  ap.omb2 = static_cast<float>(1.0 - beta2);
-  ap.bc1 = static_cast<float>(1.0 - std::pow(beta1, static_cast<double>(t)));
-  ap.bc2 = static_cast<float>(1.0 - std::pow(beta2, static_cast<double>(t)));
-  ap.eps = static_cast<float>(eps);
-  const int64_t work = (m % 4 == 0) ? ceil_div(r * m, 4) : r * m;
-  int64_t ab = ceil_div(work, 256);
-  P.adam_blocks = static_cast<int>(ab > 2048 ? 2048 : (ab < 1 ? 1 : ab));
-
+// `ws` is this layer's scratch (step_layer_bytes, 256-byte aligned).
+void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n, int64_t m, int64_t r,
+               uint64_t seed, double lr, double alpha, int proj, int dtype, void* ws, StepPlan& P) {
+  const int64_t ldn = n_ld(m), ldpt = pt_ld(n);
+  char* base = static_cast<char*>(ws);
+  AdamLayer& a = P.al;
+  a = AdamLayer{};
+  a.G = G; a.M = M; a.V = V; a.N = base;
+  a.ldn = static_cast<int>(ldn);
+  a.r = static_cast<int>(r);
+  a.m = static_cast<int>(m);
+  a.n = static_cast<int>(n);
+  a.key = philox_key(seed);
+  P.adam_blocks = adam_blocks(r, m);
+  P.pt_blocks = 0;
+  P.dec_tiles = 0;
   const double coef64 = lr * alpha * (proj == COMPACT_PROJ_IDENTITY ? 1.0 : 1.0 / std::sqrt(static_cast<double>(r)));
-  DecParams& p = P.dp;
-  p = DecParams{};
-  p.W = W; p.ldw = ldw; p.w_f32 = w_dtype == COMPACT_F32;
-  p.N = static_cast<const uint16_t*>(Nbuf); p.ldn = ldn;
-  p.n = n; p.m = m; p.r = r;
-  p.r_pad = round_up(r, kBK);
-  p.key = philox_key(seed);
-  p.identity = proj == COMPACT_PROJ_IDENTITY;
-  p.coef = static_cast<float>(coef64);
-  p.tiles_m = static_cast<int>(ceil_div(m, 128));
-  P.dec_bm = 0;
-  P.dec_lds = 0;
-  if (dtype == COMPACT_F32) return COMPACT_OK;
-  const size_t panel64 = size_t(64) * (p.r_pad + 8) * sizeof(uint16_t);
-  const size_t panel32 = size_t(32) * (p.r_pad + 8) * sizeof(uint16_t);
-  if (panel64 + kTilesLds <= 100 * 1024) {
-    P.dec_bm = 64;
-    P.dec_lds = panel64 + kTilesLds;
-  } else if (panel32 + kTilesLds <= 160 * 1024) {
-    P.dec_bm = 32;
-    P.dec_lds = panel32 + kTilesLds;
-  } else {
-    return fail(COMPACT_EUNSUPPORTED, "rank r=%lld too large for the resident projection panel", (long long)r);
-  }
-  p.panels = static_cast<int>(ceil_div(n, P.dec_bm));
-  // Column groups per panel: more groups = more workgroups in flight but one
-  // more regeneration of the panel each.  In a batch of layers a workgroup
-  // takes at most 3 column tiles (wide layers would otherwise leave a few
-  // long-running workgroups at the end of the launch); a lone layer splits
-  // further (up to 4 groups) to fill the GPU.
-  int64_t groups = ceil_div(p.tiles_m, 3);
-  if (groups < 2) groups = 2;
-  if (fill_gpu) {
-    groups = ceil_div(512, p.panels);
-    if (groups > 4) groups = 4;
-  }
-  if (groups > p.tiles_m) groups = p.tiles_m;
-  if (groups < 1) groups = 1;
-  p.col_groups = static_cast<int>(groups);
-  return COMPACT_OK;
+  DecW4Layer& d = P.dl;
+  d = DecW4Layer{};
+  d.coef = static_cast<float>(coef64);
+  if (dtype != COMPACT_BF16) return;
+  uint16_t* pt = reinterpret_cast<uint16_t*>(
+      base + round_up(static_cast<int64_t>(size_t(r) * size_t(ldn) * elem_size(dtype)), kWsAlign));
+  a.pt = pt;
+  a.ldpt = static_cast<int>(ldpt);
+  P.pt_blocks = pt_blocks(r, ldpt);
+  d.W = W; d.ldw = static_cast<int>(ldw);
+  d.N = static_cast<const uint16_t*>(a.N); d.ldn = static_cast<int>(ldn);
+  d.pt = pt; d.ldpt = static_cast<int>(ldpt);
+  d.n = static_cast<int>(n); d.m = static_cast<int>(m); d.r = static_cast<int>(r);
+  d.tiles_c = static_cast<int>(ceil_div(m, kDecT));
+  P.dec_tiles = static_cast<int>(ceil_div(n, kDecT) * d.tiles_c);
 }
 
-int launch_decompress(const StepPlan& P, hipStream_t s) {
+// Adam (+ P^T staging) for every layer of `plans`, then the decompression, in
+// equal groups of at most kStepBatch layers per launch.
+int launch_step_groups(const std::vector<StepPlan>& plans, const AdamConsts& c, int dtype, int w_dtype,
+                       hipStream_t s) {
   int st;
-  const uint32_t blocks = static_cast<uint32_t>(int64_t(P.dp.panels) * P.dp.col_groups);
-  if (P.dec_bm == 64) {
-    auto fn = k_decompress_bf16<64, 128, 2, 2>;
-    if ((st = set_lds(reinterpret_cast<const void*>(fn), P.dec_lds))) return st;
-    hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), P.dec_lds, s, P.dp);
-  } else {
-    auto fn = k_decompress_bf16<32, 128, 1, 4>;
-    if ((st = set_lds(reinterpret_cast<const void*>(fn), P.dec_lds))) return st;
-    hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), P.dec_lds, s, P.dp);
+  const int count = static_cast<int>(plans.size());
+  const int groups = (count + kStepBatch - 1) / kStepBatch;
+  const int per = (count + groups - 1) / groups;
+  for (int i0 = 0; i0 < count; i0 += per) {
+    StepBatch b{};
+    b.c = c;
+    b.count = std::min(per, count - i0);
+    b.adam_begin[0] = 0;
+    b.pt_begin[0] = 0;
+    for (int j = 0; j < b.count; ++j) {
+      const StepPlan& P = plans[i0 + j];
+      b.layer[j] = P.al;
+      b.adam_begin[j + 1] = b.adam_begin[j] + P.adam_blocks;
+      b.pt_begin[j + 1] = b.pt_begin[j] + P.pt_blocks;
+    }
+    const int blocks = b.adam_begin[b.count] + b.pt_begin[b.count];
+    hipLaunchKernelGGL(k_adam_pt_batched, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, b);
+    if ((st = check_launch("Adam and P^T staging"))) return st;
   }
-  return check_launch("decompress (bf16)");
+  if (dtype != COMPACT_BF16) return COMPACT_OK;
+  static_assert(kDecBatch >= kStepBatch, "one decompression launch per Adam launch");
+  for (int i0 = 0; i0 < count; i0 += per) {
+    DecW4Batch d{};
+    d.count = std::min(per, count - i0);
+    d.begin[0] = 0;
+    for (int j = 0; j < d.count; ++j) {
+      d.layer[j] = plans[i0 + j].dl;
+      d.begin[j + 1] = d.begin[j] + plans[i0 + j].dec_tiles;
+    }
+    const hipError_t e = dec_w4_launch(d, w_dtype == COMPACT_F32, s);
+    if (e != hipSuccess) return fail(COMPACT_EHIP, "decompression launch: %s", hipGetErrorString(e));
+  }
+  return COMPACT_OK;
 }
 
 }  // namespace
@@ -579,31 +599,24 @@ int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64
   const size_t need = compact_step_workspace_bytes(n, m, r, dtype);
   if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "step workspace %zu B < %zu B", ws_bytes, need);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  StepPlan P;
-  if ((st = plan_step(W, ldw, G, M, V, n, m, r, seed, t, lr, beta1, beta2, eps, alpha, proj, dtype, w_dtype,
-                      align_ws(ws), true, P)))
-    return st;
-  hipLaunchKernelGGL(k_adam, dim3(static_cast<uint32_t>(P.adam_blocks)), dim3(256), 0, s, P.ap);
-  if ((st = check_launch("Adam"))) return st;
+  std::vector<StepPlan> plans(1);
+  plan_step(W, ldw, G, M, V, n, m, r, seed, lr, alpha, proj, dtype, align_ws(ws), plans[0]);
+  if ((st = launch_step_groups(plans, adam_consts(t, beta1, beta2, eps, proj, dtype), dtype, w_dtype, s))) return st;
   if (dtype == COMPACT_F32) {
     GemmF32Params gp{};
     gp.A = pgen_operand(seed, n, r, proj);
-    gp.B = mem_operand(static_cast<const float*>(P.ap.N), P.ap.ldn, 1, r, m);
+    gp.B = mem_operand(static_cast<const float*>(plans[0].al.N), plans[0].al.ldn, 1, r, m);
     gp.M = n; gp.N = m; gp.K = r; gp.mode = 1;
-    gp.out = static_cast<float*>(W); gp.ldo = ldw; gp.coef = P.dp.coef;
+    gp.out = static_cast<float*>(W); gp.ldo = ldw; gp.coef = plans[0].dl.coef;
     if ((st = launch_gemm_f32(gp, s, "decompress (fp32)"))) return st;
-    return ok();
   }
-  if ((st = launch_decompress(P, s))) return st;
   return ok();
 }
 
 size_t compact_step_batched_workspace_bytes(const compact_layer* layers, int32_t count, int dtype) {
   if (layers == nullptr || count <= 0) return 0;
   size_t total = kWsAlign;
-  for (int32_t i = 0; i < count; ++i)
-    total += round_up(static_cast<int64_t>(size_t(layers[i].r) * size_t(n_ld(layers[i].m)) * elem_size(dtype)),
-                      kWsAlign);
+  for (int32_t i = 0; i < count; ++i) total += step_layer_bytes(layers[i].n, layers[i].m, layers[i].r, dtype);
   return total;
 }
 
@@ -629,59 +642,10 @@ int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, 
   char* cursor = static_cast<char*>(align_ws(ws));
   for (int32_t i = 0; i < count; ++i) {
     const compact_layer& L = layers[i];
-    if ((st = plan_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, L.seed, t, lr, beta1, beta2, eps, L.alpha,
-                        proj, dtype, w_dtype, cursor, false, plans[i])))
-      return st;
-    cursor += round_up(static_cast<int64_t>(size_t(L.r) * size_t(n_ld(L.m)) * elem_size(dtype)), kWsAlign);
+    plan_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, L.seed, lr, L.alpha, proj, dtype, cursor, plans[i]);
+    cursor += step_layer_bytes(L.n, L.m, L.r, dtype);
   }
-  // Adam: up to kBatchLayers layers per launch
-  for (int32_t i0 = 0; i0 < count; i0 += kBatchLayers) {
-    AdamBatch a{};
-    a.count = std::min<int32_t>(kBatchLayers, count - i0);
-    a.begin[0] = 0;
-    for (int j = 0; j < a.count; ++j) {
-      a.layer[j] = plans[i0 + j].ap;
-      a.begin[j + 1] = a.begin[j] + plans[i0 + j].adam_blocks;
-    }
-    hipLaunchKernelGGL(k_adam_batched, dim3(static_cast<uint32_t>(a.begin[a.count])), dim3(256), 0, s, a);
-    if ((st = check_launch("Adam (batched)"))) return st;
-  }
-  // decompression: layers are independent, so they are grouped by panel height
-  // and LDS size (a launch's LDS size, the largest of its layers, sets how many
-  // workgroups share a CU), up to kBatchLayers per launch
-  std::vector<int32_t> order(static_cast<size_t>(count));
-  for (int32_t i = 0; i < count; ++i) order[i] = i;
-  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
-    if (plans[a].dec_bm != plans[b].dec_bm) return plans[a].dec_bm > plans[b].dec_bm;
-    return plans[a].dec_lds < plans[b].dec_lds;
-  });
-  for (int32_t i0 = 0; i0 < count;) {
-    const int bm = plans[order[i0]].dec_bm;
-    const size_t lds = plans[order[i0]].dec_lds;
-    DecBatch d{};
-    d.count = 0;
-    d.begin[0] = 0;
-    int32_t i = i0;
-    while (i < count && d.count < kBatchLayers && plans[order[i]].dec_bm == bm && plans[order[i]].dec_lds == lds) {
-      const StepPlan& P = plans[order[i]];
-      d.layer[d.count] = P.dp;
-      d.begin[d.count + 1] = d.begin[d.count] + P.dp.panels * P.dp.col_groups;
-      ++d.count;
-      ++i;
-    }
-    const uint32_t blocks = static_cast<uint32_t>(d.begin[d.count]);
-    if (bm == 64) {
-      auto fn = k_decompress_batched<64, 128, 2, 2>;
-      if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
-      hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), lds, s, d);
-    } else {
-      auto fn = k_decompress_batched<32, 128, 1, 4>;
-      if ((st = set_lds(reinterpret_cast<const void*>(fn), lds))) return st;
-      hipLaunchKernelGGL(fn, dim3(blocks), dim3(256), lds, s, d);
-    }
-    if ((st = check_launch("decompress (batched)"))) return st;
-    i0 = i;
-  }
+  if ((st = launch_step_groups(plans, adam_consts(t, beta1, beta2, eps, proj, dtype), dtype, w_dtype, s))) return st;
   return ok();
 }
 

@@ -20,9 +20,10 @@
 //
 // LDS (bytes from the dynamic base): stage s of z^T at 8192 s ([32][128]
 // bf16, 256-byte K rows), stage s of dL/do at 32768 + 16384 s ([32][256] bf16,
-// 512-byte K rows).  16-byte chunk c of K row k sits at c ^ (2 (k mod 4)); a
-// 16-lane group of the transposing read touches 4 K rows x 32 bytes, which
-// this swizzle puts at distinct 32-byte bank offsets.
+// 512-byte K rows).  16-byte chunk c of K row k sits at c ^ (4 (k mod 4)).
+// The transposing 64-bit read is served 32 lanes at a time; those lanes touch
+// 4 K rows x 64 bytes (4 aligned chunks per row), which this swizzle puts on
+// the 64 distinct banks.
 //
 // Edges: tokens past T read as zero (buffer range check); splits are whole K
 // tiles, so a split never reads another split's tokens.  Rows of G^ past r and
@@ -56,10 +57,10 @@ struct GhatW4Params {
 // Per-lane copy offsets.  z^T copy block q (1 KB = 4 K rows of 256 bytes):
 // lane L lands at K row 4 q + L / 16, physical chunk L % 16; dL/do block q
 // (2 K rows of 512 bytes): K row 2 q + L / 32, physical chunk L % 32.  Each
-// lane fetches the logical chunk phys ^ (2 (k mod 4)).  Offsets are bytes from
+// lane fetches the logical chunk phys ^ (4 (k mod 4)).  Offsets are bytes from
 // the operand's first token of the split and first column of the tile.
 __device__ __forceinline__ int gh_off(int ld, int krow, int chunk) {
-  return krow * ld * 2 + ((chunk ^ (2 * (krow & 3))) * 16);
+  return krow * ld * 2 + ((chunk ^ (4 * (krow & 3))) * 16);
 }
 
 __device__ __forceinline__ void gh_wait_barrier_vm9(u32x4 (&fa)[2][2], u32x4 (&fb)[2][4]) {
@@ -111,7 +112,7 @@ __device__ __forceinline__ u32x4 gh_frag(uint32_t stage, int n0, int kk, int lan
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int k = kk * 16 + (g >> 1) * 8 + 4 * h + j;
-    const int chunk = (col >> 3) ^ (2 * (k & 3));
+    const int chunk = (col >> 3) ^ (4 * (k & 3));
     const uint32_t off = static_cast<uint32_t>(k * ROWS + chunk * 8 + (col & 7));
     const u32x2 v = gh_tr_read(stage + 2u * off);
     out[2 * h] = v.x;

@@ -5,10 +5,9 @@
 //   k_dx_bf16           dx = dL/do W^T          (Alg. 2, second line)
 //   k_ghat_bf16         split-K partials of G^ = z^T dL/do (Alg. 2, first line)
 //   k_splitk_reduce     fixed-order sum of the split-K partials
-//   k_decompress_bf16   W <- W - lr alpha P N, P regenerated per row panel in
-//                       LDS (Alg. 3, decompression and update)
 #pragma once
 #include "gemm_bf16.hpp"
+#include "kernels_common.hpp"
 
 namespace compact {
 
@@ -75,22 +74,7 @@ __global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identi
   const int64_t quads_per_row = ld / 4;
   const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (q >= quads_per_row * r) return;
-  const int64_t j = q / quads_per_row, i0 = (q % quads_per_row) * 4;
-  float g[4] = {0.f, 0.f, 0.f, 0.f};
-  if (i0 < n) {
-    if (identity) {
-      for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
-    } else {
-      pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
-      for (int e = 0; e < 4; ++e) g[e] = g[e] * scale;
-    }
-    for (int e = 0; e < 4; ++e)
-      if (i0 + e >= n) g[e] = 0.0f;
-  }
-  u32x2 v;
-  v.x = pack_bf16x2(g[0], g[1]);
-  v.y = pack_bf16x2(g[2], g[3]);
-  *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
+  pstream_t_quad(key, n, identity, scale, out, ld, q / quads_per_row, (q % quads_per_row) * 4);
 }
 
 // out[c * ldo + i] = in[i * ldi + c] for i < rows, c < cols (bf16), through a
@@ -99,12 +83,12 @@ __global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identi
 // stores 8 consecutive rows of one output row.  ldi and ldo are multiples of 8
 // and both pointers 16-byte aligned; partial chunks at the edges go element
 // by element.
-__global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* in, int64_t ldi, int64_t rows, int64_t cols,
-                                                        uint16_t* out, int64_t ldo, int tiles_c) {
+__device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t ldi, int64_t rows, int64_t cols,
+                                                    uint16_t* out, int64_t ldo, int tiles_c, int block) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];  // tile[c][i]; rows padded to 144 bytes
   const int t = threadIdx.x;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x / tiles_c) * 64;
-  const int64_t c0 = static_cast<int64_t>(blockIdx.x % tiles_c) * 64;
+  const int64_t r0 = static_cast<int64_t>(block / tiles_c) * 64;
+  const int64_t c0 = static_cast<int64_t>(block % tiles_c) * 64;
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     const int id = t + 256 * p, i = id >> 3, cc = (id & 7) * 8;
@@ -136,6 +120,36 @@ __global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* in, int6
     } else {
       for (int e = 0; e < 8 && gi + e < rows; ++e) out[gc * ldo + gi + e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
     }
+  }
+}
+
+// Staging of the persistent forward GEMM's B operand in one launch: the first
+// pt_blocks workgroups write the P^T panel (one quad per thread, as
+// k_pstream_t_bf16), the rest transpose W into W^T (64 x 64 tiles).  The P
+// stream is arithmetic latency bound and the transpose memory bound, so they
+// overlap.
+struct FwdStage {
+  const uint16_t* W;
+  int64_t ldw, n, m;
+  uint16_t* wt;      // W^T [m][ldb]
+  uint16_t* pt;      // P^T [r][ldb]
+  int64_t ldb, r;
+  PhiloxKey key;
+  int identity;
+  float pscale;
+  int tiles_c;       // ceil(m / 64)
+  int pt_blocks;     // ceil(ldb / 4 * r / 256)
+};
+
+__global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
+  const int b = static_cast<int>(blockIdx.x);
+  if (b < a.pt_blocks) {
+    const int64_t qpr = a.ldb / 4;
+    const int64_t q = static_cast<int64_t>(b) * 256 + threadIdx.x;
+    if (q >= qpr * a.r) return;
+    pstream_t_quad(a.key, a.n, a.identity, a.pscale, a.pt, a.ldb, q / qpr, (q % qpr) * 4);
+  } else {
+    transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.wt, a.ldb, a.tiles_c, b - a.pt_blocks);
   }
 }
 
@@ -273,222 +287,6 @@ __global__ void k_splitk_reduce(const float* part, int splits, int64_t ldp, int6
   float s = 0.0f;
   for (int k = 0; k < splits; ++k) s += src[k * plane];
   G[e] = s;
-}
-
-// ------------------------------- update ------------------------------------
-struct DecParams {
-  void* W;              // bf16 or fp32, n x m
-  int64_t ldw;
-  int w_f32;
-  const uint16_t* N;    // r x m, bf16, leading dimension ldn (multiple of 8)
-  int64_t ldn;
-  int64_t n, m, r;
-  int64_t r_pad;        // round_up(r, 64): panel columns
-  PhiloxKey key;
-  int identity;
-  float coef;           // fp32(lr * alpha / sqrt(r))
-  int panels;           // ceil(n / BM)
-  int col_groups;       // column groups per panel
-  int tiles_m;          // ceil(m / BN)
-};
-
-// Panel layout: [BM][r_pad + 8] bf16; the +8 pad puts the rows of one MFMA
-// fragment read on distinct LDS banks (r_pad / 8 is even).
-template <int BM, int BN, int WGM, int WGN>
-__device__ __forceinline__ void decompress_block(const DecParams& p, uint32_t logical) {
-  constexpr int NT = WGM * WGN * kWave;
-  constexpr int FM = BM / WGM / 32, FN = BN / WGN / 32;
-  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
-  const int64_t ldp = p.r_pad + 8;
-  uint16_t* Ap = lds;
-  const int64_t bs0 = BM * ldp;  // N tile stages at lds + bs0 and lds + bs0 + BN * 64
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int panel = static_cast<int>(logical % p.panels), group = static_cast<int>(logical / p.panels);
-  const int64_t row0 = static_cast<int64_t>(panel) * BM;
-
-  // 1. P panel rows row0 .. row0+BM-1, all r_pad columns, generated once.
-  {
-    const int jgroups = static_cast<int>(p.r_pad / 8);
-    const int items = (BM / 4) * jgroups;
-    for (int it = tid; it < items; it += NT) {
-      const int jg = it % jgroups, qr = it / jgroups;
-      const int64_t i0 = row0 + qr * 4, j0 = static_cast<int64_t>(jg) * 8;
-      float g[8][4];
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        const int64_t j = j0 + jj;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) g[jj][e] = 0.0f;
-        if (j < p.r && i0 < p.n) {
-          if (p.identity) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) g[jj][e] = (i0 + e == j) ? 1.0f : 0.0f;
-          } else {
-            pstream_quad(p.key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g[jj]);
-          }
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        u32x4 v;
-        v.x = pack_bf16x2(g[0][e], g[1][e]);
-        v.y = pack_bf16x2(g[2][e], g[3][e]);
-        v.z = pack_bf16x2(g[4][e], g[5][e]);
-        v.w = pack_bf16x2(g[6][e], g[7][e]);
-        if (i0 + e >= p.n) v = u32x4{0u, 0u, 0u, 0u};
-        *reinterpret_cast<u32x4*>(Ap + (qr * 4 + e) * ldp + j0) = v;
-      }
-    }
-  }
-  __syncthreads();
-
-  // 2. Column tiles of this group: acc = P_panel N_tile, then W -= coef acc.
-  //    The W tile (BM x BN) is read with 16-byte loads issued before the N tile
-  //    and the MFMAs, so its latency overlaps them; coef * acc is staged in LDS
-  //    (the N stages are free after the K loop) and W is written back in 16-byte
-  //    chunks.
-  const int per = (p.tiles_m + p.col_groups - 1) / p.col_groups;
-  const int ct_begin = group * per;
-  const int ct_end = ct_begin + per < p.tiles_m ? ct_begin + per : p.tiles_m;
-  const int lr = lane & 31, lh = lane >> 5;
-  const int kt_count = static_cast<int>(p.r_pad / kBK);
-  constexpr int kWElems = 8;                                   // elements per 16-byte bf16 chunk
-  constexpr int kWChunks = BM * BN / kWElems / NT;             // bf16 chunks per thread
-  static_assert(BM * BN % (kWElems * NT) == 0, "W tile split");
-  constexpr int kCpr = BN / kWElems;                           // chunks per W-tile row
-  float* stage = reinterpret_cast<float*>(lds + bs0);          // BM x (BN + 4) fp32 after the K loop
-  constexpr int kSld = BN;
-  static_assert(BM * kSld * 4 <= 2 * BN * kBK * 2, "staging fits in the N stages");
-  for (int ct = ct_begin; ct < ct_end; ++ct) {
-    const int64_t col0 = static_cast<int64_t>(ct) * BN;
-    // (a) W tile loads (bf16: one 16-byte chunk = 8 columns; fp32: two)
-    u32x4 wreg[kWChunks][2];
-#pragma unroll
-    for (int i = 0; i < kWChunks; ++i) {
-      const int c = tid + i * NT;
-      const int row = c / kCpr, cc = c % kCpr;
-      int64_t gr = row0 + row;
-      gr = gr < p.n ? gr : p.n - 1;
-      int64_t gc = col0 + cc * kWElems;
-      const int64_t c_last = (p.m - 1) & ~int64_t(kWElems - 1);
-      gc = gc < p.m ? gc : c_last;
-      if (p.w_f32) {
-        const float* src = static_cast<const float*>(p.W) + gr * p.ldw + gc;
-        wreg[i][0] = *reinterpret_cast<const u32x4*>(src);
-        wreg[i][1] = *reinterpret_cast<const u32x4*>(src + 4);
-      } else {
-        wreg[i][0] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.W) + gr * p.ldw + gc);
-      }
-    }
-    // (b) acc = P_panel[:, k] N[k, col0 ..] over the rank
-    MNMajorLoader<BN, NT> lb{p.N, p.ldn, p.m, p.r, col0};
-    f32x16 acc[FM][FN];
-#pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.0f;
-    lb.fetch(0, tid);
-    lb.commit(lds + bs0, tid);
-    __syncthreads();
-    for (int kt = 0; kt < kt_count; ++kt) {
-      const int64_t cur = bs0 + (kt & 1) * (BN * kBK);
-      const int64_t nxt = bs0 + ((kt + 1) & 1) * (BN * kBK);
-      const bool more = kt + 1 < kt_count;
-      if (more) lb.fetch(static_cast<int64_t>(kt + 1) * kBK, tid);
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        u32x4 a[FM], b[FN];
-        const int k = kk * 16 + lh * 8;
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-          a[fm] = *reinterpret_cast<const u32x4*>(Ap + (wm * FM * 32 + fm * 32 + lr) * ldp +
-                                                  kt * kBK + k);
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn)
-          b[fn] = *reinterpret_cast<const u32x4*>(lds + cur + tile_off(wn * FN * 32 + fn * 32 + lr, k));
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32x32x16(a[fm], b[fn], acc[fm][fn]);
-      }
-      if (more) lb.commit(lds + nxt, tid);
-      __syncthreads();
-    }
-    // (c) d = coef * acc into the LDS staging tile (row-major, fp32)
-    const float coef = p.coef;
-    {
-      const int r0 = wm * (BM / WGM), c0 = wn * (BN / WGN);
-      for_each_acc(acc, lane, [&](int row, int col, float v) {
-        const float d = coef * v;
-        stage[(r0 + row) * kSld + c0 + col] = d;
-      });
-    }
-    __syncthreads();
-    // (d) W = W - d, 16-byte chunks
-#pragma unroll
-    for (int i = 0; i < kWChunks; ++i) {
-      const int c = tid + i * NT;
-      const int row = c / kCpr, cc = c % kCpr;
-      const int64_t gr = row0 + row, gc = col0 + cc * kWElems;
-      if (gr >= p.n || gc >= p.m) continue;
-      const float* dsrc = stage + row * kSld + cc * kWElems;
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(dsrc);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(dsrc + 4);
-      const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-      const int cnt = gc + kWElems <= p.m ? kWElems : static_cast<int>(p.m - gc);
-      if (p.w_f32) {
-        float* dst = static_cast<float*>(p.W) + gr * p.ldw + gc;
-        const uint32_t wbits[8] = {wreg[i][0].x, wreg[i][0].y, wreg[i][0].z, wreg[i][0].w,
-                                   wreg[i][1].x, wreg[i][1].y, wreg[i][1].z, wreg[i][1].w};
-        float out[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) out[e] = __uint_as_float(wbits[e]) - dv[e];
-        if (cnt == kWElems) {
-          *reinterpret_cast<f32x4*>(dst) = f32x4{out[0], out[1], out[2], out[3]};
-          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{out[4], out[5], out[6], out[7]};
-        } else {
-          for (int e = 0; e < cnt; ++e) dst[e] = out[e];
-        }
-      } else {
-        uint16_t* dst = static_cast<uint16_t*>(p.W) + gr * p.ldw + gc;
-        const uint32_t wp[4] = {wreg[i][0].x, wreg[i][0].y, wreg[i][0].z, wreg[i][0].w};
-        uint32_t outp[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float lo = __uint_as_float(wp[e] << 16) - dv[2 * e];
-          const float hi = __uint_as_float(wp[e] & 0xFFFF0000u) - dv[2 * e + 1];
-          outp[e] = pack_bf16x2(lo, hi);
-        }
-        if (cnt == kWElems) {
-          *reinterpret_cast<u32x4*>(dst) = u32x4{outp[0], outp[1], outp[2], outp[3]};
-        } else {
-          for (int e = 0; e < cnt; ++e) dst[e] = static_cast<uint16_t>(outp[e >> 1] >> (16 * (e & 1)));
-        }
-      }
-    }
-    __syncthreads();  // the staging tile is the next column tile's N stage
-  }
-}
-
-template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_bf16(DecParams p) {
-  decompress_block<BM, BN, WGM, WGN>(p, xcd_remap(blockIdx.x, gridDim.x));
-}
-
-struct DecBatch {
-  int count;
-  int begin[kBatchLayers + 1];
-  DecParams layer[kBatchLayers];
-};
-
-template <int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(WGM* WGN* kWave, 1) void k_decompress_batched(DecBatch d) {
-  const int b = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
-  const int l = batch_layer_of(d.begin, d.count, b);
-  decompress_block<BM, BN, WGM, WGN>(d.layer[l], static_cast<uint32_t>(b - d.begin[l]));
 }
 
 }  // namespace compact

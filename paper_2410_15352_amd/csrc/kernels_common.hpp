@@ -12,31 +12,56 @@ namespace compact {
 // N  = (M / bc1) / (sqrt(V / bc2) + eps),  bc_k = 1 - b_k^t
 // G, M, V dense r x m fp32; N written r x m with leading dimension ldn, as
 // bf16 (n_f32 == 0) or fp32.
-struct AdamParams {
+//
+// One launch serves a group of layers (same t and hyper-parameters) and also
+// stages, for each layer that needs it, the P^T panel of the decompression:
+// pt[j * ldpt + i] = bf16(G(seed, i, j)) (unscaled; zero for i >= n).  The two
+// jobs are independent; their workgroups alternate in the grid, so the
+// HBM-bound moment update and the VALU-bound P stream run side by side.
+
+// Values shared by every layer of a step.
+struct AdamConsts {
+  float b1, b2, omb1, omb2, bc1, bc2, eps;
+  int n_f32;
+  int identity;  // P is the identity (r == n)
+};
+
+struct AdamLayer {
   const float* G;
   float* M;
   float* V;
   void* N;
-  int64_t ldn;
-  int n_f32;
-  int64_t r, m;
-  float b1, b2, omb1, omb2, bc1, bc2, eps;
+  uint16_t* pt;  // P^T panel [r][ldpt], or null
+  PhiloxKey key;
+  int ldn, r, m;
+  int ldpt, n;
 };
 
-__device__ __forceinline__ void adam_one(const AdamParams& p, int64_t e, float g, float mo, float vo,
-                                         float& m1, float& v1, float& nv) {
-  m1 = p.b1 * mo + p.omb1 * g;
-  v1 = p.b2 * vo + p.omb2 * (g * g);
-  const float mhat = m1 / p.bc1;
-  const float vhat = v1 / p.bc2;
-  nv = mhat / (__builtin_sqrtf(vhat) + p.eps);
-  (void)e;
+constexpr int kStepBatch = 40;  // layers per launch (kernel argument size)
+constexpr int kAdamVec = 4;     // float4 groups per thread
+
+struct StepBatch {
+  AdamConsts c;
+  int count;
+  int adam_begin[kStepBatch + 1];  // first Adam workgroup of each layer
+  int pt_begin[kStepBatch + 1];    // first P^T workgroup of each layer
+  AdamLayer layer[kStepBatch];
+};
+static_assert(sizeof(StepBatch) <= 4096, "kernel argument size");
+
+__device__ __forceinline__ void adam_one(const AdamConsts& c, float g, float mo, float vo, float& m1, float& v1,
+                                         float& nv) {
+  m1 = c.b1 * mo + c.omb1 * g;
+  v1 = c.b2 * vo + c.omb2 * (g * g);
+  const float mhat = m1 / c.bc1;
+  const float vhat = v1 / c.bc2;
+  nv = mhat / (__builtin_sqrtf(vhat) + c.eps);
 }
 
 // Elements [4 q, 4 q + 4) for q = first, first + stride, ... (m % 4 == 0, so a
 // group of four never crosses a row), else one element per index.
-__device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, int64_t stride) {
-  const int64_t total = p.r * p.m;
+__device__ __forceinline__ void adam_range(const AdamLayer& p, const AdamConsts& k, int64_t first, int64_t stride) {
+  const int64_t total = int64_t(p.r) * p.m;
   if (p.m % 4 == 0) {
     for (int64_t q = first; q * 4 < total; q += stride) {
       const int64_t e = q * 4;
@@ -47,7 +72,7 @@ __device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, i
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float a, b, c;
-        adam_one(p, e + i, g[i], mo[i], vo[i], a, b, c);
+        adam_one(k, g[i], mo[i], vo[i], a, b, c);
         m1[i] = a;
         v1[i] = b;
         nv[i] = c;
@@ -55,7 +80,7 @@ __device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, i
       *reinterpret_cast<f32x4*>(p.M + e) = m1;
       *reinterpret_cast<f32x4*>(p.V + e) = v1;
       const int64_t j = e / p.m, c = e - j * p.m;
-      if (p.n_f32) {
+      if (k.n_f32) {
         *reinterpret_cast<f32x4*>(static_cast<float*>(p.N) + j * p.ldn + c) = nv;
       } else {
         u32x2 w;
@@ -67,11 +92,11 @@ __device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, i
   } else {
     for (int64_t e = first; e < total; e += stride) {
       float m1, v1, nv;
-      adam_one(p, e, p.G[e], p.M[e], p.V[e], m1, v1, nv);
+      adam_one(k, p.G[e], p.M[e], p.V[e], m1, v1, nv);
       p.M[e] = m1;
       p.V[e] = v1;
       const int64_t j = e / p.m, c = e - j * p.m;
-      if (p.n_f32)
+      if (k.n_f32)
         static_cast<float*>(p.N)[j * p.ldn + c] = nv;
       else
         static_cast<uint16_t*>(p.N)[j * p.ldn + c] = f32_to_bf16(nv);
@@ -79,23 +104,63 @@ __device__ __forceinline__ void adam_range(const AdamParams& p, int64_t first, i
   }
 }
 
-__global__ void k_adam(AdamParams p) {
-  adam_range(p, static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x,
-             static_cast<int64_t>(gridDim.x) * blockDim.x);
+// Adam workgroups of a layer: kAdamVec float4 groups (or elements) per thread.
+__host__ __device__ inline int adam_blocks(int64_t r, int64_t m) {
+  const int64_t work = (m % 4 == 0) ? ceil_div(r * m, 4) : r * m;
+  const int64_t b = ceil_div(work, int64_t(256) * kAdamVec);
+  return static_cast<int>(b < 1 ? 1 : b);
 }
 
-struct AdamBatch {
-  int count;
-  int begin[kBatchLayers + 1];
-  AdamParams layer[kBatchLayers];
-};
+// One quad of a P^T panel: out[j * ld + i0 .. i0 + 3] = bf16(scale G[i0 .. i0 + 3][j]),
+// or the identity (scale 1); rows i >= n are written as zero.
+__device__ __forceinline__ void pstream_t_quad(PhiloxKey key, int64_t n, int identity, float scale, uint16_t* out,
+                                               int64_t ld, int64_t j, int64_t i0) {
+  float g[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i0 < n) {
+    if (identity) {
+      for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
+    } else {
+      pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
+      for (int e = 0; e < 4; ++e) g[e] = g[e] * scale;
+    }
+    for (int e = 0; e < 4; ++e)
+      if (i0 + e >= n) g[e] = 0.0f;
+  }
+  u32x2 v;
+  v.x = pack_bf16x2(g[0], g[1]);
+  v.y = pack_bf16x2(g[2], g[3]);
+  *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
+}
 
-__global__ void k_adam_batched(AdamBatch a) {
+// P^T workgroups of a layer: one quad per thread.
+__host__ __device__ inline int pt_blocks(int64_t r, int64_t ldpt) { return static_cast<int>(ceil_div(ldpt / 4 * r, 256)); }
+
+__global__ void k_adam_pt_batched(StepBatch s) {
+  const int na = s.adam_begin[s.count], np = s.pt_begin[s.count];
+  const int k = na < np ? na : np;
   const int b = static_cast<int>(blockIdx.x);
-  const int l = batch_layer_of(a.begin, a.count, b);
-  const int nb = a.begin[l + 1] - a.begin[l];
-  adam_range(a.layer[l], static_cast<int64_t>(b - a.begin[l]) * blockDim.x + threadIdx.x,
-             static_cast<int64_t>(nb) * blockDim.x);
+  bool adam;
+  int idx;
+  if (b < 2 * k) {
+    adam = (b & 1) == 0;
+    idx = b >> 1;
+  } else {
+    adam = na > np;
+    idx = b - k;
+  }
+  if (adam) {
+    const int l = batch_layer_of(s.adam_begin, s.count, idx);
+    const int nb = s.adam_begin[l + 1] - s.adam_begin[l];
+    adam_range(s.layer[l], s.c, static_cast<int64_t>(idx - s.adam_begin[l]) * blockDim.x + threadIdx.x,
+               static_cast<int64_t>(nb) * blockDim.x);
+  } else {
+    const int l = batch_layer_of(s.pt_begin, s.count, idx);
+    const AdamLayer& p = s.layer[l];
+    const int64_t q = static_cast<int64_t>(idx - s.pt_begin[l]) * blockDim.x + threadIdx.x;
+    const int64_t qpr = p.ldpt / 4;
+    if (q >= qpr * p.r) return;
+    pstream_t_quad(p.key, p.n, s.c.identity, 1.0f, p.pt, p.ldpt, q / qpr, (q % qpr) * 4);
+  }
 }
 
 // ------------------------------- fp32 GEMM ---------------------------------

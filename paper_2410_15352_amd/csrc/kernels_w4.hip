@@ -1,4 +1,5 @@
-// The persistent four-wave bf16 GEMM kernel and its launcher.  Built as its
+// The persistent four-wave bf16 GEMM, the G^ and the decompression kernels and
+// their launchers.  Built as its
 // own translation unit with -mllvm -enable-misched=false and
 // -mllvm -enable-post-misched=false: the K-step code in gemm_w4.hpp is written
 // in issue order and must not be rescheduled.
@@ -16,6 +17,14 @@ __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
 }
 
 __global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) { ghat_w4(p); }
+
+// Three workgroups per CU for bf16 W (168 registers per lane), two for fp32 W.
+template <bool WF32>
+__global__ __launch_bounds__(256, WF32 ? 2 : 3) void k_dec_w4(DecW4Batch d) {
+  const int b = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
+  const int l = batch_layer_of(d.begin, d.count, b);
+  dec_w4_tile<WF32>(d.layer[l], b - d.begin[l]);
+}
 
 namespace {
 
@@ -68,6 +77,26 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   } else {
     hipLaunchKernelGGL(k_gemm_w4<1>, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, g);
   }
+  return hipGetLastError();
+}
+
+bool dec_w4_eligible(int64_t n, int64_t m, int64_t r, int64_t ldw, int64_t ldn, int64_t ldpt, bool w_f32) {
+  const int64_t esz = w_f32 ? 4 : 2, lim = int64_t(1) << 31;
+  if (n < 1 || m < 1 || r < 1 || ldn % 8 != 0 || ldpt % 8 != 0 || ldw % 4 != 0) return false;
+  if (ldw < m || ldn < m || ldpt < n) return false;
+  // 32-bit offsets: a W tile (128 rows), and every K tile of N and P^T
+  if (int64_t(kDecT) * ldw * esz >= lim) return false;
+  if ((r + 2 * kDecK) * ldn * 2 >= lim || (r + 2 * kDecK) * ldpt * 2 >= lim) return false;
+  return n < lim && m < lim;
+}
+
+hipError_t dec_w4_launch(const DecW4Batch& d, bool w_f32, hipStream_t stream) {
+  const int blocks = d.begin[d.count];
+  if (d.count <= 0 || blocks <= 0) return hipSuccess;
+  if (w_f32)
+    hipLaunchKernelGGL(k_dec_w4<true>, dim3(static_cast<uint32_t>(blocks)), dim3(256), kDecLds, stream, d);
+  else
+    hipLaunchKernelGGL(k_dec_w4<false>, dim3(static_cast<uint32_t>(blocks)), dim3(256), kDecLds, stream, d);
   return hipGetLastError();
 }
 

@@ -145,3 +145,20 @@ def test_pstream_validation(lib):
     assert lib.compact_pstream(1, 4, 4, FAKE, 2, None) == -1
     assert lib.compact_pstream_boxmuller(None, None, None, None, 0, None) == 0
     assert lib.compact_pstream_boxmuller(None, None, None, None, 5, None) == -1
+
+
+def test_layer_batch_marshals_once_and_updates_seeds(lib):
+    torch = pytest.importorskip("torch")
+    import paper_2410_15352_amd as cp
+    layers = [dict(W=torch.empty(64, 40, dtype=torch.bfloat16), G=torch.empty(8, 40), M=torch.empty(8, 40),
+                   V=torch.empty(8, 40), seed=(i + 1) << 32, alpha=0.5) for i in range(3)]
+    b = cp.prepare_layers(layers)
+    assert b.count == 3
+    assert [b.arr[i].seed for i in range(3)] == [(i + 1) << 32 for i in range(3)]
+    assert [(b.arr[i].n, b.arr[i].m, b.arr[i].r) for i in range(3)] == [(64, 40, 8)] * 3
+    b.set_seeds([7, 8, 9])
+    assert [b.arr[i].seed for i in range(3)] == [7, 8, 9]
+    # the workspace size is the same whether the layers come as a list or a batch
+    assert cp.step_batched_workspace_bytes(b) == cp.step_batched_workspace_bytes(layers) > 0
+    with pytest.raises(ValueError):
+        b.set_seeds([1])

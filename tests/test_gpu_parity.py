@@ -33,6 +33,7 @@ SHAPES = [
     (2048, 768, 3072, 384, "bf16"),
     (777, 1024, 2736, 128, "bf16"),
     (128, 5461, 64, 682, "bf16"),
+    (150, 200, 203, 24, "bf16"),         # odd m: partial column groups in the update
 ]
 
 
