@@ -93,6 +93,42 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
 size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype);
 
 /*
+ * Forward pass of several projections that read the same input, Alg. 1 per
+ * projection (the paper compresses q, k, v of attention and gate, up of the
+ * MLP, each with its own P; they share the block input x):
+ *
+ *   for j = 0 .. count-1:  y_j = x W_j  and  z_j = x P_j
+ *
+ *   W  [n x M]       (ld ldw)  W = [W_0 | W_1 | ...]: W_j is columns
+ *                              mo_j .. mo_j + m[j] - 1, mo_j = m[0] + .. + m[j-1]
+ *   y  [tokens x M]  (ld ldy)  y_j in the same columns as W_j
+ *   z  [tokens x R]  (ld ldz)  z_j is columns ro_j .. ro_j + r[j] - 1,
+ *                              ro_j = r[0] + .. + r[j-1]
+ *   M = m[0] + .. + m[count-1], R = r[0] + .. + r[count-1]
+ *   m, r, seeds   HOST arrays of count entries (read during the call);
+ *                 P_j[i][k] = G(seeds[j], i, k) / sqrt(r[j])
+ *   count  1 .. 8; every m[j], r[j] but the last a multiple of 8 (so each
+ *          column slice starts on a 16-byte boundary)
+ *   ws, ws_bytes  optional workspace of at least
+ *          compact_fwd_group_workspace_bytes(n, count, m, r, dtype) bytes (bf16
+ *          path).  With it the call stages [W^T; P_0^T; P_1^T; ...] once and runs
+ *          one persistent GEMM for all projections (x is read once; the z
+ *          columns of all projections share output tiles); otherwise, and for
+ *          fp32, it runs compact_fwd on each column slice.
+ * Results are bitwise identical to compact_fwd on each (W_j, y_j, z_j) slice.
+ * The backward of the group needs no entry of its own: dx = dL/dx summed over
+ * the projections is compact_bwd with W and the concatenated dL/do, and each
+ * G^_j is compact_bwd on the column slices z_j and dL/do_j.
+ * Errors: COMPACT_EINVAL (count, NULL arrays, shapes), COMPACT_EALIGN,
+ * COMPACT_EWORKSPACE, COMPACT_EHIP; nothing is launched on a validation error.
+ */
+int compact_fwd_group(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy, void* z,
+                      int64_t ldz, int64_t tokens, int64_t n, int32_t count, const int64_t* m, const int64_t* r,
+                      const uint64_t* seeds, int proj, int dtype, void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_fwd_group_workspace_bytes(int64_t n, int32_t count, const int64_t* m, const int64_t* r, int dtype);
+
+/*
  * Backward pass, Alg. 2:  G^ = z^T dL/do  and  dx = dL/do W^T.
  *
  *   dy [tokens x m]  (ld lddy)  gradient of the loss with respect to y

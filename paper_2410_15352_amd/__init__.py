@@ -14,12 +14,14 @@ no fallback path.
 """
 from __future__ import annotations
 
+import ctypes
+
 from . import _lib
 
 F32, BF16 = 0, 1
 PROJ = {"gaussian": 0, "identity": 1}
 
-__all__ = ["compact_fwd", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
+__all__ = ["compact_fwd", "compact_fwd_group", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
            "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
            "LayerBatch", "prepare_layers",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
@@ -105,6 +107,35 @@ def compact_fwd(x, W, y, z, seed, proj="gaussian", ws=None, stream=None):
                          T, n, m, r, int(seed) & (2**64 - 1), PROJ[proj], _dtype_code(x),
                          wp, wb, _stream(stream, x))
     _check("compact_fwd", st)
+
+
+def _group_arrays(ms, rs, seeds=None):
+    count = len(ms)
+    if len(rs) != count or (seeds is not None and len(seeds) != count):
+        raise ValueError("one m, r (and seed) per projection")
+    m_arr = (ctypes.c_int64 * count)(*[int(v) for v in ms])
+    r_arr = (ctypes.c_int64 * count)(*[int(v) for v in rs])
+    s_arr = None if seeds is None else (ctypes.c_uint64 * count)(*[int(v) & (2**64 - 1) for v in seeds])
+    return count, m_arr, r_arr, s_arr
+
+
+def fwd_group_workspace_bytes(n, ms, rs, dtype=BF16):
+    count, m_arr, r_arr, _ = _group_arrays(ms, rs)
+    return int(_lib.load().compact_fwd_group_workspace_bytes(int(n), count, m_arr, r_arr, dtype))
+
+
+def compact_fwd_group(x, W, y, z, ms, rs, seeds, proj="gaussian", ws=None, stream=None):
+    """Alg. 1 for projections that share the input x: W = [W_0 | W_1 | ...]
+    (n, sum m), y (T, sum m), z (T, sum r); projection j uses columns
+    sum(ms[:j]) .. of W and y, columns sum(rs[:j]) .. of z and seed seeds[j].
+    Bitwise equal to compact_fwd on each column slice."""
+    lib = _lib.load()
+    T, n = x.shape
+    count, m_arr, r_arr, s_arr = _group_arrays(ms, rs, seeds)
+    wp, wb = _ws(ws)
+    st = lib.compact_fwd_group(_ptr(x), _ld(x), _ptr(W), _ld(W), _ptr(y), _ld(y), _ptr(z), _ld(z), T, n, count,
+                               m_arr, r_arr, s_arr, PROJ[proj], _dtype_code(x), wp, wb, _stream(stream, x))
+    _check("compact_fwd_group", st)
 
 
 def compact_bwd(dy, W, z, dx, G, ws=None, stream=None):

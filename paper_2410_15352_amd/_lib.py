@@ -14,6 +14,11 @@ SIGNATURES = {
     "compact_fwd": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_i64, c_i64,
                             c_i64, c_i64, c_u64, c_int, c_int, c_vp, c_size, c_vp]),
     "compact_fwd_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_int]),
+    "compact_fwd_group": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_i64, c_i64,
+                                  ctypes.c_int32, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64),
+                                  ctypes.POINTER(c_u64), c_int, c_int, c_vp, c_size, c_vp]),
+    "compact_fwd_group_workspace_bytes": (c_size, [c_i64, ctypes.c_int32, ctypes.POINTER(c_i64),
+                                                   ctypes.POINTER(c_i64), c_int]),
     "compact_bwd": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
                             c_i64, c_i64, c_i64, c_int, c_vp, c_size, c_vp]),
     "compact_bwd_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_i64, c_int]),

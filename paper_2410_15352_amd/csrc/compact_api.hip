@@ -265,6 +265,76 @@ static void* align_ws(void* ws) {
   return reinterpret_cast<void*>(a);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Projections that share one input: W = [W_0 | W_1 | ...] (n x msum), y the
+// same columns, z = [z_0 | z_1 | ...] (rsum columns).
+struct FwdGroup {
+  int count;
+  int64_t m[kMaxGroup], r[kMaxGroup];
+  uint64_t seed[kMaxGroup];
+  int64_t msum, rsum;
+};
+
+size_t fwd_group_ws_bytes(int64_t n, const FwdGroup& G) {
+  return size_t(stacked_rows(G.msum, G.rsum)) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
+}
+
+// The persistent bf16 forward over the stacked operand [W^T; pad to 256;
+// P_0^T; P_1^T; ...]: y in the first column tiles, z after.  Sets `taken`
+// to false (and launches nothing) when the persistent kernel does not take
+// the shape.
+int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy, void* z,
+                 int64_t ldz, int64_t tokens, int64_t n, const FwdGroup& G, int identity, void* ws,
+                 hipStream_t s, bool& taken) {
+  int st;
+  const int64_t ldb = pt_ld(n);
+  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, stacked_rows(G.msum, G.rsum), ldy, G.msum, ldz,
+                                            G.rsum);
+  if (!taken) return COMPACT_OK;
+  uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
+  const int64_t mp = round_up(G.msum, kW4Tile);
+  FwdStage fs{};
+  fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = G.msum;
+  fs.b = bs; fs.ldb = ldb;
+  fs.count = G.count;
+  fs.identity = identity;
+  fs.tiles_c = static_cast<int>(ceil_div(G.msum, 64));
+  fs.pt_begin[0] = 0;
+  int64_t row = mp;
+  for (int j = 0; j < G.count; ++j) {
+    fs.row_off[j] = row;
+    fs.r[j] = G.r[j];
+    fs.key[j] = philox_key(G.seed[j]);
+    fs.pscale[j] = inv_sqrt_rank(G.r[j], identity ? COMPACT_PROJ_IDENTITY : COMPACT_PROJ_GAUSSIAN);
+    fs.pt_begin[j + 1] = fs.pt_begin[j] + static_cast<int>(ceil_div((ldb / 4) * G.r[j], 256));
+    row += G.r[j];
+  }
+  const int64_t stage_blocks = fs.pt_begin[G.count] + ceil_div(n, 64) * fs.tiles_c;
+  if (stage_blocks > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "staging grid too large");
+  hipLaunchKernelGGL(k_fwd_stage_bf16, dim3(static_cast<uint32_t>(stage_blocks)), dim3(256), 0, s, fs);
+  if ((st = check_launch("W^T and P^T staging (bf16)"))) return st;
+  W4Gemm g{};
+  g.A = static_cast<const uint16_t*>(x); g.lda = static_cast<int>(ldx);
+  g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
+  g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(stacked_rows(G.msum, G.rsum));
+  g.seg[0] = W4Seg{static_cast<uint16_t*>(y), static_cast<int>(ldy), static_cast<int>(G.msum), w4_tiles(G.msum)};
+  g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(G.rsum), w4_tiles(G.rsum)};
+  g.tiles_n = g.seg[0].tiles + g.seg[1].tiles;
+  const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
+  if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
+  g.tiles = static_cast<int>(tiles);
+  const hipError_t e = gemm_w4_launch(g, W4Use::kForward, s);
+  if (e != hipSuccess) return fail(COMPACT_EHIP, "forward GEMM (bf16): %s", hipGetErrorString(e));
+  return COMPACT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy,
                 void* z, int64_t ldz, int64_t tokens, int64_t n, int64_t m, int64_t r,
                 uint64_t seed, int proj, int dtype, void* ws, size_t ws_bytes, void* stream) {
@@ -297,32 +367,12 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
   const PhiloxKey key = philox_key(seed);
   const float pscale = inv_sqrt_rank(r, proj);
   const int64_t ldb = pt_ld(n);
-  if (ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, stacked_rows(m, r), ldy, m, ldz, r)) {
-    // persistent GEMM over [W^T; P^T]: y in the first column tiles, z after
-    uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
-    const int64_t mp = round_up(m, kW4Tile);
-    FwdStage fs{};
-    fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = m;
-    fs.wt = bs; fs.pt = bs + mp * ldb; fs.ldb = ldb; fs.r = r;
-    fs.key = key; fs.identity = identity; fs.pscale = pscale;
-    fs.tiles_c = static_cast<int>(ceil_div(m, 64));
-    fs.pt_blocks = static_cast<int>(ceil_div((ldb / 4) * r, 256));
-    const int64_t stage_blocks = fs.pt_blocks + ceil_div(n, 64) * fs.tiles_c;
-    hipLaunchKernelGGL(k_fwd_stage_bf16, dim3(static_cast<uint32_t>(stage_blocks)), dim3(256), 0, s, fs);
-    if ((st = check_launch("W^T and P^T staging (bf16)"))) return st;
-    W4Gemm g{};
-    g.A = static_cast<const uint16_t*>(x); g.lda = static_cast<int>(ldx);
-    g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
-    g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(stacked_rows(m, r));
-    g.seg[0] = W4Seg{static_cast<uint16_t*>(y), static_cast<int>(ldy), static_cast<int>(m), w4_tiles(m)};
-    g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(r), w4_tiles(r)};
-    g.tiles_n = g.seg[0].tiles + g.seg[1].tiles;
-    const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
-    if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
-    g.tiles = static_cast<int>(tiles);
-    const hipError_t e = gemm_w4_launch(g, W4Use::kForward, s);
-    if (e != hipSuccess) return fail(COMPACT_EHIP, "forward GEMM (bf16): %s", hipGetErrorString(e));
-    return ok();
+  {
+    FwdGroup G{};
+    G.count = 1; G.m[0] = m; G.r[0] = r; G.seed[0] = seed; G.msum = m; G.rsum = r;
+    bool taken = false;
+    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, identity, ws, s, taken))) return st;
+    if (taken) return ok();
   }
 
   FwdParams p{};
@@ -353,6 +403,71 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), kGemmLds, s, p);
   }
   if ((st = check_launch("fused forward (bf16)"))) return st;
+  return ok();
+}
+
+size_t compact_fwd_group_workspace_bytes(int64_t n, int32_t count, const int64_t* m, const int64_t* r, int dtype) {
+  if (dtype != COMPACT_BF16 || n < 1 || count < 1 || count > kMaxGroup || m == nullptr || r == nullptr) return 0;
+  FwdGroup G{};
+  G.count = count;
+  for (int j = 0; j < count; ++j) {
+    if (m[j] < 1 || r[j] < 1) return 0;
+    G.msum += m[j];
+    G.rsum += r[j];
+  }
+  return fwd_group_ws_bytes(n, G);
+}
+
+int compact_fwd_group(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy, void* z,
+                      int64_t ldz, int64_t tokens, int64_t n, int32_t count, const int64_t* m, const int64_t* r,
+                      const uint64_t* seeds, int proj, int dtype, void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
+  if (count < 1 || count > kMaxGroup) return fail(COMPACT_EINVAL, "count %d not in [1, %d]", count, kMaxGroup);
+  if (m == nullptr || r == nullptr || seeds == nullptr) return fail(COMPACT_EINVAL, "m, r or seeds is NULL");
+  FwdGroup G{};
+  G.count = count;
+  for (int j = 0; j < count; ++j) {
+    if ((st = check_shape(tokens, n, m[j], r[j], proj))) {
+      const std::string msg = g_last_error;
+      return fail(st, "projection %d: %s", j, msg.c_str());
+    }
+    // every column slice but the last starts on a 16-byte boundary
+    if (j + 1 < count && (m[j] % 8 != 0 || r[j] % 8 != 0))
+      return fail(COMPACT_EALIGN, "projection %d: m=%lld and r=%lld must be multiples of 8 (all but the last)", j,
+                  (long long)m[j], (long long)r[j]);
+    G.m[j] = m[j];
+    G.r[j] = r[j];
+    G.seed[j] = seeds[j];
+    G.msum += m[j];
+    G.rsum += r[j];
+  }
+  if ((st = check_matrix("x", x, ldx, n, dtype))) return st;
+  if ((st = check_matrix("W", W, ldw, G.msum, dtype))) return st;
+  if ((st = check_matrix("y", y, ldy, G.msum, dtype))) return st;
+  if ((st = check_matrix("z", z, ldz, G.rsum, dtype))) return st;
+  const size_t need = compact_fwd_group_workspace_bytes(n, count, m, r, dtype);
+  if (ws != nullptr && ws_bytes < need) return fail(COMPACT_EWORKSPACE, "forward workspace %zu B < %zu B", ws_bytes, need);
+  if (tokens == 0) return ok();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == COMPACT_BF16) {
+    bool taken = false;
+    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, proj == COMPACT_PROJ_IDENTITY, ws, s,
+                           taken)))
+      return st;
+    if (taken) return ok();
+  }
+  // otherwise one compact_fwd per projection on the column slices
+  const size_t esz = elem_size(dtype);
+  int64_t mo = 0, ro = 0;
+  for (int j = 0; j < count; ++j) {
+    if ((st = compact_fwd(x, ldx, static_cast<const char*>(W) + mo * esz, ldw, static_cast<char*>(y) + mo * esz,
+                          ldy, static_cast<char*>(z) + ro * esz, ldz, tokens, n, m[j], r[j], seeds[j], proj, dtype,
+                          ws, ws_bytes, stream)))
+      return st;
+    mo += m[j];
+    ro += r[j];
+  }
   return ok();
 }
 

@@ -10,8 +10,8 @@
 // sums the splits in a fixed order (deterministic G^).
 //
 // Pipeline as in gemm_w4.hpp: 32-token K tiles, four LDS stages, copies by
-// buffer_load_dwordx4 ... lds issued 3 K tiles ahead and spread over the
-// MFMAs, one barrier per K tile:
+// buffer_load_dwordx4 ... lds issued 3 K tiles ahead (six stages, 5 ahead, time
+// the same) and spread over the MFMAs, one barrier per K tile:
 //   step 0: read fragments (t, 1); copies 0 .. 2 of this wave for K tile
 //           t + 3; 8 MFMAs on fragments (t, 0)
 //   step 1: wait for this wave's copies of K tile t + 1 (9 later copies may
@@ -39,6 +39,8 @@ namespace compact {
 constexpr int kGhTm = 128, kGhTn = 256;  // tile: rows of G^ (r), columns (m)
 constexpr int kGhK = 32;                 // K tile (tokens)
 constexpr int kGhStages = 4;
+constexpr int kGhAhead = kGhStages - 1;  // K tiles copied ahead
+constexpr int kGhCopies = 6;             // copies per wave per K tile (2 of z^T, 4 of dL/do)
 constexpr int kGhAStage = kGhK * kGhTm * 2;  // 8 KB
 constexpr int kGhBStage = kGhK * kGhTn * 2;  // 16 KB
 constexpr int kGhBBase = kGhStages * kGhAStage;
@@ -63,12 +65,14 @@ __device__ __forceinline__ int gh_off(int ld, int krow, int chunk) {
   return krow * ld * 2 + ((chunk ^ (4 * (krow & 3))) * 16);
 }
 
-__device__ __forceinline__ void gh_wait_barrier_vm9(u32x4 (&fa)[2][2], u32x4 (&fb)[2][4]) {
-  // s_waitcnt vmcnt(9), lgkmcnt(0), then s_barrier; fragments pass through so
-  // that the MFMAs after it stay after it
-  asm volatile("s_waitcnt vmcnt(9) lgkmcnt(0)\n\ts_barrier"
+// s_waitcnt vmcnt(N), lgkmcnt(0), then s_barrier; fragments pass through so
+// that the MFMAs after it stay after it
+template <int N>
+__device__ __forceinline__ void gh_wait_barrier(u32x4 (&fa)[2][2], u32x4 (&fb)[2][4]) {
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
+  asm volatile("s_waitcnt vmcnt(%6) lgkmcnt(0)\n\ts_barrier"
                : "+v"(fa[1][0]), "+v"(fa[1][1]), "+v"(fb[1][0]), "+v"(fb[1][1]), "+v"(fb[1][2]), "+v"(fb[1][3])
-               :
+               : "n"(N)
                : "memory");
 }
 
@@ -168,7 +172,7 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& p) {
   // this split's K tiles or past T land out of range (the last split is the only
   // one whose K tiles run past T)
   auto copy = [&](int u, int c) {
-    const int st = u & 3;
+    const int st = u % kGhStages;
     const uint32_t krow_bytes_z = static_cast<uint32_t>(u) * kGhK * p.ldz * 2;
     const uint32_t krow_bytes_y = static_cast<uint32_t>(u) * kGhK * p.lddy * 2;
     const uint32_t oob = u < kt ? 0u : kW4Oob;
@@ -192,35 +196,35 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& p) {
   u32x4 fa[2][2], fb[2][4];  // [kk parity][fragment]
   if (kt > 0) {
 #pragma unroll
-    for (int u = 0; u < 3; ++u)
+    for (int u = 0; u < kGhAhead; ++u)
 #pragma unroll
-      for (int c = 0; c < 6; ++c) copy(u, c);
+      for (int c = 0; c < kGhCopies; ++c) copy(u, c);
     w4_wait_vm<0>();
     asm volatile("s_barrier" ::: "memory");
     gh_read(lbase, 0, kGhBBase, wm, wn, lane, 0, fa[0], fb[0]);
     gh_wait_frags(fa, fb);
     for (int t = 0; t < kt; ++t) {
-      const uint32_t sa = static_cast<uint32_t>(t & 3) * kGhAStage;
-      const uint32_t sb = kGhBBase + static_cast<uint32_t>(t & 3) * kGhBStage;
-      const uint32_t sa1 = static_cast<uint32_t>((t + 1) & 3) * kGhAStage;
-      const uint32_t sb1 = kGhBBase + static_cast<uint32_t>((t + 1) & 3) * kGhBStage;
+      const uint32_t st0 = static_cast<uint32_t>(t % kGhStages), st1 = static_cast<uint32_t>((t + 1) % kGhStages);
+      const uint32_t sa = st0 * kGhAStage, sb = kGhBBase + st0 * kGhBStage;
+      const uint32_t sa1 = st1 * kGhAStage, sb1 = kGhBBase + st1 * kGhBStage;
       // step 0
       gh_read(lbase, sa, sb, wm, wn, lane, 1, fa[1], fb[1]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[0][fi], fb[0][fj], acc[fi][fj]);
-        if (i % 3 == 0) copy(t + 3, i / 3);
+        if (i % 3 == 0) copy(t + kGhAhead, i / 3);
       }
       gh_pin_acc(acc);
-      // step 1
-      gh_wait_barrier_vm9(fa, fb);
+      // step 1: this wave's copies of K tile t + 1 have landed when at most the
+      // copies of the next kGhAhead - 2 K tiles and 3 of the one after are in flight
+      gh_wait_barrier<kGhCopies * (kGhAhead - 2) + 3>(fa, fb);
       gh_read(lbase, sa1, sb1, wm, wn, lane, 0, fa[0], fb[0]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[1][fi], fb[1][fj], acc[fi][fj]);
-        if (i % 3 == 0) copy(t + 3, 3 + i / 3);
+        if (i % 3 == 0) copy(t + kGhAhead, 3 + i / 3);
       }
       gh_wait_frags(fa, fb);
     }

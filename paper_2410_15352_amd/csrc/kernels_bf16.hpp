@@ -124,32 +124,39 @@ __device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t 
 }
 
 // Staging of the persistent forward GEMM's B operand in one launch: the first
-// pt_blocks workgroups write the P^T panel (one quad per thread, as
+// workgroups write the P^T panels of the projections (one quad per thread, as
 // k_pstream_t_bf16), the rest transpose W into W^T (64 x 64 tiles).  The P
 // stream is arithmetic latency bound and the transpose memory bound, so they
-// overlap.
+// overlap.  Projection j's panel P_j^T [r_j][ldb] starts at row row_off[j] of
+// the staged operand.
+constexpr int kMaxGroup = 8;  // projections sharing one input
+
 struct FwdStage {
   const uint16_t* W;
-  int64_t ldw, n, m;
-  uint16_t* wt;      // W^T [m][ldb]
-  uint16_t* pt;      // P^T [r][ldb]
-  int64_t ldb, r;
-  PhiloxKey key;
+  int64_t ldw, n, m;      // W [n x m]; m = the sum of the projections' widths
+  uint16_t* b;            // staged operand, rows of ldb elements: W^T in rows 0 .. m-1
+  int64_t ldb;
+  int count;
   int identity;
-  float pscale;
-  int tiles_c;       // ceil(m / 64)
-  int pt_blocks;     // ceil(ldb / 4 * r / 256)
+  int tiles_c;            // ceil(m / 64)
+  int pt_begin[kMaxGroup + 1];  // first P^T workgroup of each projection
+  int64_t row_off[kMaxGroup];
+  int64_t r[kMaxGroup];
+  PhiloxKey key[kMaxGroup];
+  float pscale[kMaxGroup];
 };
 
 __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
   const int b = static_cast<int>(blockIdx.x);
-  if (b < a.pt_blocks) {
+  if (b < a.pt_begin[a.count]) {
+    int j = 0;
+    while (j + 1 < a.count && a.pt_begin[j + 1] <= b) ++j;
     const int64_t qpr = a.ldb / 4;
-    const int64_t q = static_cast<int64_t>(b) * 256 + threadIdx.x;
-    if (q >= qpr * a.r) return;
-    pstream_t_quad(a.key, a.n, a.identity, a.pscale, a.pt, a.ldb, q / qpr, (q % qpr) * 4);
+    const int64_t q = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
+    if (q >= qpr * a.r[j]) return;
+    pstream_t_quad(a.key[j], a.n, a.identity, a.pscale[j], a.b + a.row_off[j] * a.ldb, a.ldb, q / qpr, (q % qpr) * 4);
   } else {
-    transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.wt, a.ldb, a.tiles_c, b - a.pt_blocks);
+    transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.b, a.ldb, a.tiles_c, b - a.pt_begin[a.count]);
   }
 }
 

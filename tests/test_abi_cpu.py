@@ -108,6 +108,49 @@ def test_fwd_validation(lib, kw, status):
     assert lib.compact_last_error()
 
 
+def _i64s(*v):
+    return (ctypes.c_int64 * len(v))(*v)
+
+
+def test_fwd_group_workspace_size(lib):
+    # [W_0^T; W_1^T; W_2^T; pad to 256; P_0^T; P_1^T; P_2^T]: one stacked operand
+    ms, rs = _i64s(1024, 1024, 1024), _i64s(128, 128, 128)
+    assert lib.compact_fwd_group_workspace_bytes(1024, 3, ms, rs, 1) == \
+        lib.compact_fwd_workspace_bytes(1024, 3072, 384, 1)
+    ms2, rs2 = _i64s(2736, 2736), _i64s(128, 128)
+    assert lib.compact_fwd_group_workspace_bytes(1024, 2, ms2, rs2, 1) == \
+        lib.compact_fwd_workspace_bytes(1024, 5472, 256, 1)
+    assert lib.compact_fwd_group_workspace_bytes(1024, 3, ms, rs, 0) == 0
+    assert lib.compact_fwd_group_workspace_bytes(1024, 0, ms, rs, 1) == 0
+    assert lib.compact_fwd_group_workspace_bytes(1024, 9, ms, rs, 1) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(count=0), -1), (dict(count=9), -1),
+    (dict(m=None), -1), (dict(r=None), -1), (dict(seeds=None), -1),
+    (dict(m=(1020, 1024, 1024)), -2),   # a slice that is not 16-byte aligned
+    (dict(r=(128, 124, 128)), -2),
+    (dict(r=(128, 128, 2000)), -1),     # r > n
+    (dict(m=(1024, 0, 1024)), -1),
+    (dict(ldw=3000), -1),               # ld < sum of m
+    (dict(ldz=376), -1),                # ld < sum of r
+    (dict(proj=1), -1),                 # identity needs r == n
+    (dict(ws=FAKE, ws_bytes=16), -4),
+])
+def test_fwd_group_validation(lib, kw, status):
+    a = dict(x=FAKE, ldx=1024, W=FAKE, ldw=3072, y=FAKE, ldy=3072, z=FAKE, ldz=384, tokens=64, n=1024,
+             count=3, m=(1024, 1024, 1024), r=(128, 128, 128), seeds=(1, 2, 3), proj=0, dtype=1, ws=None,
+             ws_bytes=0, stream=None)
+    a.update(kw)
+    arr = lambda v, t: None if v is None else (t * len(v))(*v)
+    st = lib.compact_fwd_group(a["x"], a["ldx"], a["W"], a["ldw"], a["y"], a["ldy"], a["z"], a["ldz"],
+                               a["tokens"], a["n"], a["count"], arr(a["m"], ctypes.c_int64),
+                               arr(a["r"], ctypes.c_int64), arr(a["seeds"], ctypes.c_uint64), a["proj"],
+                               a["dtype"], a["ws"], a["ws_bytes"], a["stream"])
+    assert st == status
+    assert lib.compact_last_error()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(dx=None, G=None), -1), (dict(ws=None), -4), (dict(ws_bytes=8), -4),
     (dict(lddy=1020), -1), (dict(G=FAKE + 4), -2), (dict(r=1025), -1),

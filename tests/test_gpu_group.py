@@ -1,0 +1,124 @@
+"""GPU checks of compact_fwd_group: projections that share one input (q, k, v of
+attention; gate and up of the MLP), each with its own seed and rank.
+
+* The grouped call is bitwise equal to compact_fwd on each column slice (the
+  same GEMM with the same K order), with and without the workspace, on shapes
+  the persistent kernel takes and on ragged ones it does not.
+* Each projection matches the fp64 oracle's forward (Alg. 1) within the bf16
+  tolerance.
+* The backward of a group through the existing ABI: dx from one compact_bwd over
+  the concatenated weight equals the sum over projections of the oracle's
+  dL/do_j W_j^T, and each G^_j from the column slices matches the oracle.
+"""
+import numpy as np
+import pytest
+
+from oracle import compact as oc
+from synthetic import bwd_inputs, fwd_inputs
+
+from gpu_util import dev, empty, ld_for, to_dev, to_np, workspace
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+cp = pytest.importorskip("paper_2410_15352_amd")
+
+TOL = 2e-2
+
+# (tokens, n, ms, rs): persistent-kernel shapes (n >= 320, even widths) and
+# ragged ones that run per projection
+GROUPS = [
+    (513, 512, (512, 512, 512), (128, 128, 128)),      # q, k, v
+    (777, 1024, (1376, 1376), (128, 128)),             # gate, up
+    (300, 1024, (256, 512), (64, 96)),                 # mixed widths
+    (300, 200, (136, 72), (40, 24)),                   # K < 320: per projection
+    (129, 512, (512, 203), (64, 30)),                  # odd last width: per projection
+]
+
+
+def _ids(g):
+    return "T{}-n{}-m{}-r{}".format(g[0], g[1], "+".join(map(str, g[2])), "+".join(map(str, g[3])))
+
+
+def _group_inputs(T, n, ms, data_seed):
+    x, _ = fwd_inputs(T, n, 8, "bf16", data_seed=data_seed)
+    Ws = [fwd_inputs(8, n, m, "bf16", data_seed=data_seed + 1 + j)[1] for j, m in enumerate(ms)]
+    return x, Ws
+
+
+@pytest.mark.parametrize("group", GROUPS, ids=_ids)
+@pytest.mark.parametrize("use_ws", [True, False])
+def test_group_equals_per_projection(group, use_ws):
+    T, n, ms, rs = group
+    seeds = [((j + 3) << 32) | 11 for j in range(len(ms))]
+    x, Ws = _group_inputs(T, n, ms, data_seed=T + n)
+    M, R = sum(ms), sum(rs)
+    xd = to_dev(x, "bf16", ld_for(n, "bf16"))
+    Wd = to_dev(np.concatenate(Ws, axis=1), "bf16", ld_for(M, "bf16"))
+    y = empty(T, M, "bf16", ld_for(M, "bf16"), fill=7.0)
+    z = empty(T, R, "bf16", ld_for(R, "bf16"), fill=7.0)
+    ws = workspace(cp.fwd_group_workspace_bytes(n, ms, rs)) if use_ws else None
+    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, ws=ws)
+    # reference: compact_fwd on each column slice, into separate buffers
+    y1 = empty(T, M, "bf16", ld_for(M, "bf16"), fill=-3.0)
+    z1 = empty(T, R, "bf16", ld_for(R, "bf16"), fill=-3.0)
+    mo = ro = 0
+    for j, (m, r) in enumerate(zip(ms, rs)):
+        wsj = workspace(cp.fwd_workspace_bytes(n, m, r)) if use_ws else None
+        cp.compact_fwd(xd, Wd[:, mo:mo + m], y1[:, mo:mo + m], z1[:, ro:ro + r], seeds[j], ws=wsj)
+        mo += m
+        ro += r
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y1.view(torch.int16))
+    assert torch.equal(z.view(torch.int16), z1.view(torch.int16))
+
+
+@pytest.mark.parametrize("group", GROUPS[:2], ids=_ids)
+def test_group_oracle_parity(group):
+    T, n, ms, rs = group
+    seeds = [((j + 5) << 32) | 1 for j in range(len(ms))]
+    x, Ws = _group_inputs(T, n, ms, data_seed=3 * T)
+    M, R = sum(ms), sum(rs)
+    xd = to_dev(x, "bf16", ld_for(n, "bf16"))
+    Wd = to_dev(np.concatenate(Ws, axis=1), "bf16", ld_for(M, "bf16"))
+    y = empty(T, M, "bf16", ld_for(M, "bf16"))
+    z = empty(T, R, "bf16", ld_for(R, "bf16"))
+    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, ws=workspace(cp.fwd_group_workspace_bytes(n, ms, rs)))
+    torch.cuda.synchronize()
+    yn, zn = to_np(y), to_np(z)
+    mo = ro = 0
+    for j, (m, r) in enumerate(zip(ms, rs)):
+        y_ref, z_ref = oc.ref_fwd(x, Ws[j], seeds[j], r)
+        assert oc.rel_fro(yn[:, mo:mo + m], y_ref) <= TOL
+        assert oc.rel_fro(zn[:, ro:ro + r], z_ref) <= TOL
+        mo += m
+        ro += r
+
+
+def test_group_backward_through_concatenation():
+    # q, k, v share x: dL/dx = sum_j dL/do_j W_j^T, one compact_bwd over [W_0 | W_1 | W_2]
+    T, n, ms, rs = 640, 512, (512, 512, 512), (128, 128, 128)
+    M, R = sum(ms), sum(rs)
+    parts = [bwd_inputs(T, n, m, r, "bf16", data_seed=40 + j) for j, (m, r) in enumerate(zip(ms, rs))]
+    dy_all = np.concatenate([p[0] for p in parts], axis=1)
+    z_all = np.concatenate([p[1] for p in parts], axis=1)
+    W_all = np.concatenate([p[2] for p in parts], axis=1)
+    dyd = to_dev(dy_all, "bf16", ld_for(M, "bf16"))
+    zd = to_dev(z_all, "bf16", ld_for(R, "bf16"))
+    Wd = to_dev(W_all, "bf16", ld_for(M, "bf16"))
+    dx = empty(T, n, "bf16", ld_for(n, "bf16"))
+    cp.compact_bwd(dyd, Wd, None, dx, None)
+    Gs = []
+    mo = ro = 0
+    for m, r in zip(ms, rs):
+        G = torch.empty(r, m, dtype=torch.float32, device=dev())
+        cp.compact_bwd(dyd[:, mo:mo + m], None, zd[:, ro:ro + r], None, G,
+                       ws=workspace(cp.bwd_workspace_bytes(T, n, m, r)))
+        Gs.append(G)
+        mo += m
+        ro += r
+    torch.cuda.synchronize()
+    dx_ref = sum(oc.ref_bwd(p[0], p[1], p[2])[0] for p in parts)
+    assert oc.rel_fro(to_np(dx), dx_ref) <= TOL
+    for G, p in zip(Gs, parts):
+        assert oc.rel_fro(G.cpu().numpy(), oc.ref_bwd(p[0], p[1], p[2])[1]) <= TOL
