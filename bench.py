@@ -4,8 +4,12 @@ synthetic model-shaped workload, on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload llama-350m]
 
-One step = compact_fwd over all layers, compact_bwd over all layers (reverse
-order), compact_step over all layers, on synthetic inputs resident in HBM.
+One step = the forward of every linear layer, its backward (reverse order) and
+the Adam step of every layer, on synthetic inputs resident in HBM.  Layers that
+read the same input (q, k, v; gate, up) run as one group: compact_fwd_group,
+one compact_bwd for dL/dx over the concatenated weight (the sum a shared input
+needs) and a compact_bwd per layer for its G^.  --no-group runs every layer on
+its own (compact_fwd / compact_bwd per layer, dL/dx not summed).
 Prints ONE JSON line: tokens/s, the MFMA roofline fraction of the dominant
 kernel (the fused forward GEMM), per-phase timings, activation bytes saved and
 the CPU oracle's throughput on the host cores.
@@ -38,6 +42,8 @@ def parse_args():
     ap.add_argument("--workload", default="llama-350m")
     ap.add_argument("--fwd-mode", choices=["panel", "lds"], default="panel",
                     help="panel: P^T panel in workspace; lds: P tiles regenerated in LDS")
+    ap.add_argument("--no-group", action="store_true",
+                    help="run every linear layer on its own instead of grouping layers that share an input")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=1 << 30,
                     help="token slice for the oracle timing (default: the full step)")
@@ -59,10 +65,31 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
+GROUPABLE = (("q", "k", "v"), ("gate", "up"))
+
+
+def input_groups(wl, grouped=True):
+    """Lists of layer indices that read the same input: q, k, v and gate, up of
+    one block (when grouped), every other layer on its own."""
+    out, i, L = [], 0, wl.layers
+    while i < len(L):
+        g = [i]
+        if grouped:
+            for names in GROUPABLE:
+                k = len(names)
+                if (tuple(x.name for x in L[i:i + k]) == names and
+                        all(x.block == L[i].block and x.n == L[i].n for x in L[i:i + k])):
+                    g = list(range(i, i + k))
+                    break
+        out.append(g)
+        i += len(g)
+    return out
+
+
 class Model:
     """Device buffers of every CompAct linear layer of a workload."""
 
-    def __init__(self, wl, fwd_mode):
+    def __init__(self, wl, fwd_mode, grouped=True):
         import torch
         import paper_2410_15352_amd as cp
         from synthetic import bf16_bits, bf16_round
@@ -85,23 +112,46 @@ class Model:
 
         # one activation / gradient / output buffer per distinct width (values
         # do not affect timing); everything per layer is separate
+        # one activation / gradient / output buffer per distinct width (values
+        # do not affect timing); weights, z, G^ and Adam moments are per layer.
+        # A group's weights are column slices of one [n x sum m] tensor, its z
+        # column slices of one [T x sum r] tensor.
+        self.groups = input_groups(wl, grouped)
         self.x, self.dy, self.y, self.dx = {}, {}, {}, {}
+        self.W, self.z = [None] * len(wl.layers), [None] * len(wl.layers)
+        self.Wg, self.zg, self.msum = [], [], []
+        for g in self.groups:
+            Ls = [wl.layers[i] for i in g]
+            n, M, R = Ls[0].n, sum(L.m for L in Ls), sum(L.r for L in Ls)
+            if n not in self.x:
+                self.x[n] = dev_bf16(bf16_round(rng(1234 + n).standard_normal((T, n), np.float32)), ld8(n))
+                self.dx[n] = torch.empty(T, ld8(n), dtype=torch.bfloat16, device=dev)[:, :n]
+            if M not in self.dy:
+                self.dy[M] = dev_bf16(bf16_round(0.01 * rng(4321 + M).standard_normal((T, M), np.float32)), ld8(M))
+                self.y[M] = torch.empty(T, ld8(M), dtype=torch.bfloat16, device=dev)[:, :M]
+            Wall = np.concatenate([bf16_round(0.02 * rng(1234 + L.layer_id).standard_normal((L.n, L.m), np.float32))
+                                   for L in Ls], axis=1)
+            Wg = dev_bf16(Wall, ld8(M))
+            zg = torch.empty(T, ld8(R), dtype=torch.bfloat16, device=dev)[:, :R]
+            mo = ro = 0
+            for i, L in zip(g, Ls):
+                self.W[i] = Wg[:, mo:mo + L.m]
+                self.z[i] = zg[:, ro:ro + L.r]
+                mo += L.m
+                ro += L.r
+            self.Wg.append(Wg)
+            self.zg.append(zg)
+            self.msum.append(M)
+        self.G, self.M, self.V = [], [], []
         for L in wl.layers:
-            if L.n not in self.x:
-                self.x[L.n] = dev_bf16(bf16_round(rng(1234 + L.n).standard_normal((T, L.n), np.float32)), ld8(L.n))
-                self.dx[L.n] = torch.empty(T, ld8(L.n), dtype=torch.bfloat16, device=dev)[:, :L.n]
-            if L.m not in self.dy:
-                self.dy[L.m] = dev_bf16(bf16_round(0.01 * rng(4321 + L.m).standard_normal((T, L.m), np.float32)), ld8(L.m))
-                self.y[L.m] = torch.empty(T, ld8(L.m), dtype=torch.bfloat16, device=dev)[:, :L.m]
-        self.W, self.z, self.G, self.M, self.V = [], [], [], [], []
-        for L in wl.layers:
-            g = rng(1234 + L.layer_id)
-            self.W.append(dev_bf16(bf16_round(0.02 * g.standard_normal((L.n, L.m), np.float32)), ld8(L.m)))
-            self.z.append(torch.empty(T, ld8(L.r), dtype=torch.bfloat16, device=dev)[:, :L.r])
             self.G.append(torch.empty(L.r, L.m, dtype=torch.float32, device=dev))
             self.M.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
             self.V.append(torch.zeros(L.r, L.m, dtype=torch.float32, device=dev))
-        wf = max(cp.fwd_workspace_bytes(L.n, L.m, L.r) for L in wl.layers) if fwd_mode == "panel" else 0
+        if fwd_mode == "panel":
+            wf = max(cp.fwd_group_workspace_bytes(wl.layers[g[0]].n, [wl.layers[i].m for i in g],
+                                                  [wl.layers[i].r for i in g]) for g in self.groups)
+        else:
+            wf = 0
         wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
         wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
         self.batch = cp.prepare_layers([dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed,
@@ -113,13 +163,35 @@ class Model:
         self.seeds = [L.seed for L in wl.layers]
         self.t = 0
 
-    def fwd(self, i):
-        L = self.wl.layers[i]
-        self.cp.compact_fwd(self.x[L.n], self.W[i], self.y[L.m], self.z[i], self.seeds[i], ws=self.ws_f)
+    def fwd(self, gi):
+        g = self.groups[gi]
+        Ls = [self.wl.layers[i] for i in g]
+        x, y = self.x[Ls[0].n], self.y[self.msum[gi]]
+        if len(g) == 1:
+            self.cp.compact_fwd(x, self.Wg[gi], y, self.zg[gi], self.seeds[g[0]], ws=self.ws_f)
+        else:
+            self.cp.compact_fwd_group(x, self.Wg[gi], y, self.zg[gi], [L.m for L in Ls], [L.r for L in Ls],
+                                      [self.seeds[i] for i in g], ws=self.ws_f)
 
-    def bwd(self, i):
-        L = self.wl.layers[i]
-        self.cp.compact_bwd(self.dy[L.m], self.W[i], self.z[i], self.dx[L.n], self.G[i], ws=self.ws_b)
+    def bwd_dx(self, gi):
+        """dL/dx of a group: one GEMM over its concatenated weight."""
+        g = self.groups[gi]
+        n = self.wl.layers[g[0]].n
+        self.cp.compact_bwd(self.dy[self.msum[gi]], self.Wg[gi], None, self.dx[n], None)
+
+    def bwd_ghat(self, gi):
+        """G^ of each layer of a group, from the column slices of dL/do and z."""
+        g = self.groups[gi]
+        dy = self.dy[self.msum[gi]]
+        mo = 0
+        for i in g:
+            L = self.wl.layers[i]
+            self.cp.compact_bwd(dy[:, mo:mo + L.m], None, self.z[i], None, self.G[i], ws=self.ws_b)
+            mo += L.m
+
+    def bwd(self, gi):
+        self.bwd_dx(gi)
+        self.bwd_ghat(gi)
 
     def upd(self, i, t):
         wl = self.wl
@@ -134,29 +206,33 @@ class Model:
 
     def step(self, reseed_period):
         self.t += 1
-        n = len(self.wl.layers)
-        for i in range(n):
-            self.fwd(i)
-        for i in reversed(range(n)):
-            self.bwd(i)
+        ng = len(self.groups)
+        for gi in range(ng):
+            self.fwd(gi)
+        for gi in reversed(range(ng)):
+            self.bwd(gi)
         self.upd_all(self.t)
-        for i in range(n):
+        for i in range(len(self.wl.layers)):
             self.seeds[i] = self.cp.compact_next_seed(self.seeds[i], self.t, reseed_period)
 
 
-def algorithmic(wl):
-    """Per-step algorithmic work (sums over layers), per the kernel inventory."""
+def algorithmic(wl, groups):
+    """Per-step algorithmic work (sums over launches), per the kernel inventory:
+    a group's forward and dL/dx read x (or write dL/dx) once."""
     T = wl.tokens
     f = dict(fwd=0.0, dx=0.0, ghat=0.0, dec=0.0)
     b = dict(fwd=0.0, dx=0.0, ghat=0.0, adam=0.0, dec=0.0)
+    for g in groups:
+        Ls = [wl.layers[i] for i in g]
+        n, M, R = Ls[0].n, sum(L.m for L in Ls), sum(L.r for L in Ls)
+        f["fwd"] += 2.0 * T * n * (M + R)
+        f["dx"] += 2.0 * T * n * M
+        b["fwd"] += 2.0 * (T * n + n * M + T * M + T * R)
+        b["dx"] += 2.0 * (T * M + n * M + T * n)
     for L in wl.layers:
         n, m, r = L.n, L.m, L.r
-        f["fwd"] += 2.0 * T * n * (m + r)
-        f["dx"] += 2.0 * T * n * m
         f["ghat"] += 2.0 * T * r * m
         f["dec"] += 2.0 * n * r * m
-        b["fwd"] += 2.0 * (T * n + n * m + T * m + T * r)
-        b["dx"] += 2.0 * (T * m + n * m + T * n)
         b["ghat"] += 2.0 * (T * r + T * m) + 4.0 * r * m
         b["adam"] += 22.0 * r * m
         b["dec"] += 4.0 * n * m + 2.0 * r * m
@@ -166,15 +242,13 @@ def algorithmic(wl):
 def time_phases(model, torch, reps=2, step_reps=10):
     """Per-phase GPU time (ms per step) with HIP events on the launch stream.
     The step phase is short (under a millisecond), so it is repeated more."""
-    n = len(model.wl.layers)
+    ng = len(model.groups)
     stream = torch.cuda.current_stream()
     out = {}
     phases = {
-        "fwd": lambda: [model.fwd(i) for i in range(n)],
-        "bwd_dx": lambda: [model.cp.compact_bwd(model.dy[L.m], model.W[i], None, model.dx[L.n], None)
-                           for i, L in enumerate(model.wl.layers)],
-        "bwd_ghat": lambda: [model.cp.compact_bwd(model.dy[L.m], None, model.z[i], None, model.G[i],
-                                                  ws=model.ws_b) for i, L in enumerate(model.wl.layers)],
+        "fwd": lambda: [model.fwd(gi) for gi in range(ng)],
+        "bwd_dx": lambda: [model.bwd_dx(gi) for gi in range(ng)],
+        "bwd_ghat": lambda: [model.bwd_ghat(gi) for gi in range(ng)],
         "step": lambda: model.upd_all(max(model.t, 1)),
     }
     for name, fn in phases.items():
@@ -262,7 +336,7 @@ def main():
     wl = workload(args.workload)
     T = wl.tokens
     print(f"[bench] workload {wl.name}: {len(wl.layers)} layers, {T} tokens; allocating", file=sys.stderr, flush=True)
-    model = Model(wl, args.fwd_mode)
+    model = Model(wl, args.fwd_mode, grouped=not args.no_group)
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -283,7 +357,7 @@ def main():
         print(json.dumps({"ms_per_step": ms_per_step, "tokens_per_s": T / (ms_per_step * 1e-3)}), flush=True)
         return
     phases = time_phases(model, torch)
-    flops, bytes_ = algorithmic(wl)
+    flops, bytes_ = algorithmic(wl, model.groups)
     fwd_tflops = flops["fwd"] / (phases["fwd"] * 1e-3) / 1e12
     gemm_ms = phases["fwd"] + phases["bwd_dx"] + phases["bwd_ghat"]
     gemm_frac = (flops["fwd"] + flops["dx"] + flops["ghat"]) / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
@@ -295,12 +369,13 @@ def main():
         if rec.get("src_hash") == kernel_source_hash() and rec.get("workload") == wl.name:
             traffic = rec.get("bytes_per_launch")
     nl = len(wl.layers)
+    nf = len(model.groups)  # forward launches per step
     roofline = {
-        "bound": "mfma", "kernel": "compact_fwd: k_gemm_w4<0> ([y|z] = x [W^T; P^T]^T) with its W^T + P^T staging launch",
+        "bound": "mfma", "kernel": "compact_fwd(_group): k_gemm_w4<0> ([y|z] = x [W^T; P^T]^T) with its W^T + P^T staging launch",
         "achieved": round(fwd_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
         "frac": round(fwd_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-        "flops_per_launch": flops["fwd"] / nl,
-        "avg_launch_ms": phases["fwd"] / nl,
+        "flops_per_launch": flops["fwd"] / nf,
+        "avg_launch_ms": phases["fwd"] / nf,
     }
     cpu = None
     if not args.no_cpu_baseline:
@@ -322,6 +397,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": wl.description, "tokens_per_step": T, "layers": nl,
+                   "input_groups": "q,k,v and gate,up share their input" if not args.no_group else "none",
                    "fwd_mode": args.fwd_mode, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

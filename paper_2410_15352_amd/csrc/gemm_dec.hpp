@@ -79,8 +79,8 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
   const int kt = (p.r + kDecK - 1) / kDecK;
 
   // copies: block `wave` of each operand (1 KB = 4 K rows of 256 B)
-  const __amdgpu_buffer_rsrc_t rn = w4_rsrc(p.N + c0, (static_cast<int64_t>(p.r) * p.ldn - c0) * 2);
-  const __amdgpu_buffer_rsrc_t rp = w4_rsrc(p.pt + i0, (static_cast<int64_t>(p.r) * p.ldpt - i0) * 2);
+  const __amdgpu_buffer_rsrc_t rn = w4_rsrc(p.N + c0, view_bytes(p.r, p.m, p.ldn, 0, c0, 2));
+  const __amdgpu_buffer_rsrc_t rp = w4_rsrc(p.pt + i0, view_bytes(p.r, p.n, p.ldpt, 0, i0, 2));
   const int von = gh_off(p.ldn, 4 * wave + (lane >> 4), lane & 15);
   const int vop = gh_off(p.ldpt, 4 * wave + (lane >> 4), lane & 15);
   const uint32_t lbase = __builtin_amdgcn_groupstaticsize();
@@ -108,9 +108,9 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
   // fp32) per row, and an access instruction covers 4 row segments of 64
   // bytes.  item (b, a, g, q) of this lane is row wrow(b, g) + q, columns
   // wcol(a), wcol(a) + 1.
-  const __amdgpu_buffer_rsrc_t rw =
-      w4_rsrc(static_cast<char*>(p.W) + (static_cast<int64_t>(i0) * p.ldw + c0) * kEsz,
-              ((static_cast<int64_t>(p.n) - i0) * p.ldw - c0) * kEsz);
+  // W may be a column slice of a wider matrix: the range ends at its last element
+  const __amdgpu_buffer_rsrc_t rw = w4_rsrc(static_cast<char*>(p.W) + (static_cast<int64_t>(i0) * p.ldw + c0) * kEsz,
+                                            view_bytes(p.n, p.m, p.ldw, i0, c0, kEsz));
   const int odd = lane & 1;
   const int row_l = wi * 64 + 4 * (lane >> 5) + 2 * odd, col_l = wc * 64 + (lane & 30);
   WVec wv[2][2][4][2];

@@ -150,9 +150,10 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& p) {
   const int t_end = min(t_begin + p.split_len, p.T);
   const int kt = (t_end - t_begin + kGhK - 1) / kGhK;
 
-  // buffer ranges: from the split's first token to the end of the matrix
-  const int64_t zbytes = (static_cast<int64_t>(p.T) - t_begin) * p.ldz * 2 - static_cast<int64_t>(row0) * 2;
-  const int64_t ybytes = (static_cast<int64_t>(p.T) - t_begin) * p.lddy * 2 - static_cast<int64_t>(col0) * 2;
+  // buffer ranges: from the split's first token to the last element of the
+  // matrix (z and dL/do may be column slices of wider matrices)
+  const int64_t zbytes = view_bytes(p.T, p.r, p.ldz, t_begin, row0, 2);
+  const int64_t ybytes = view_bytes(p.T, p.m, p.lddy, t_begin, col0, 2);
   const __amdgpu_buffer_rsrc_t rz = w4_rsrc(p.z + static_cast<int64_t>(t_begin) * p.ldz + row0, zbytes);
   const __amdgpu_buffer_rsrc_t ry = w4_rsrc(p.dy + static_cast<int64_t>(t_begin) * p.lddy + col0, ybytes);
   // this wave's copy blocks: z^T blocks 2 wave + {0, 1}, dL/do blocks 4 wave + {0 .. 3}

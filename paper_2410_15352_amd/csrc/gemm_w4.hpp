@@ -100,6 +100,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t w4_rsrc(const void* base, int6
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0), nrec, 0x00020000);
 }
 
+// Bytes of a row-major view [rows x cols] (ld elements per row) from element
+// (r0, c0) through its last element, rounded up to 16: a buffer range that ends
+// inside the view's own allocation also when the view is a column slice of a
+// wider matrix.  (rows - r0) * ld * esz would run past the allocation's end by
+// the slice's column offset on the last row.  The rounding stays inside the
+// row because the view starts 16-byte aligned and ld * esz is a multiple of 16;
+// rows from `rows` on are out of range.
+__host__ __device__ inline int64_t view_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t r0, int64_t c0,
+                                              int esz) {
+  const int64_t elems = (rows - 1 - r0) * ld + cols - c0;
+  return elems <= 0 ? 0 : (elems * esz + 15) & ~int64_t(15);
+}
+
 // s_waitcnt lgkmcnt(0) + s_barrier with the fragments of the following MFMAs
 // passed through it: MFMAs have no memory side effects, so without this data
 // dependence the compiler may issue them ahead of the barrier.  Global

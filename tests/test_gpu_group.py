@@ -122,3 +122,34 @@ def test_group_backward_through_concatenation():
     assert oc.rel_fro(to_np(dx), dx_ref) <= TOL
     for G, p in zip(Gs, parts):
         assert oc.rel_fro(G.cpu().numpy(), oc.ref_bwd(p[0], p[1], p[2])[1]) <= TOL
+
+
+def test_ghat_and_step_on_overhanging_column_slices():
+    # G^ and the step on the second column slice of [A | B] where the slice
+    # width (1376) is not a multiple of the kernels' column tiles, so the last
+    # tile of the slice overhangs the end of the buffer on its last row.  The
+    # results must equal those on contiguous copies, bit for bit.
+    T, n, r, m = 1000, 1024, 128, 1376
+    dy_a, z_a, W_a = bwd_inputs(T, n, m, r, "bf16", data_seed=71)
+    dy_b, z_b, W_b = bwd_inputs(T, n, m, r, "bf16", data_seed=72)
+    dy_all = to_dev(np.concatenate([dy_a, dy_b], axis=1), "bf16", 2 * m)   # ld = 2m: slice B ends the buffer
+    z_all = to_dev(np.concatenate([z_a, z_b], axis=1), "bf16", 2 * r)
+    ws = workspace(cp.bwd_workspace_bytes(T, n, m, r))
+    G_slice = torch.empty(r, m, dtype=torch.float32, device=dev())
+    G_copy = torch.empty(r, m, dtype=torch.float32, device=dev())
+    cp.compact_bwd(dy_all[:, m:], None, z_all[:, r:], None, G_slice, ws=ws)
+    cp.compact_bwd(to_dev(dy_b, "bf16"), None, to_dev(z_b, "bf16"), None, G_copy, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(G_slice, G_copy)
+
+    W_all = to_dev(np.concatenate([W_a, W_b], axis=1), "bf16", 2 * m)
+    W_copy = to_dev(W_b, "bf16")
+    M1, V1 = torch.zeros_like(G_copy), torch.zeros_like(G_copy)
+    M2, V2 = torch.zeros_like(G_copy), torch.zeros_like(G_copy)
+    wss = workspace(cp.step_workspace_bytes(n, m, r))
+    cp.compact_step(W_all[:, m:], G_copy, M1, V1, 9 << 32, 1, 1e-3, alpha=0.25, ws=wss)
+    cp.compact_step(W_copy, G_copy, M2, V2, 9 << 32, 1, 1e-3, alpha=0.25, ws=wss)
+    torch.cuda.synchronize()
+    assert torch.equal(W_all[:, m:].contiguous().view(torch.int16), W_copy.view(torch.int16))
+    # the first slice is untouched
+    assert torch.equal(W_all[:, :m].contiguous().view(torch.int16), to_dev(W_a, "bf16").view(torch.int16))
