@@ -156,6 +156,39 @@ def _cast(a, dtype):
     raise ValueError(dtype)
 
 
+def normal_bf16_blocked(rows, cols, seed, scale=1.0, block_rows=4096, threads=None, bf16=True):
+    """A (rows, cols) float32 matrix of scale * N(0, 1) values, rounded to bf16
+    (ties to even) unless bf16=False, for the full-size parity tests: row block
+    b (block_rows rows) is drawn by PCG64(seed).jumped(b + 1) in float32, the
+    blocks filled in parallel threads.  Same (rows, cols, seed, scale,
+    block_rows, bf16) -> same values, whatever the thread count."""
+    import concurrent.futures
+    import os as _os
+    out = np.empty((rows, cols), np.float32)
+    nblk = (rows + block_rows - 1) // block_rows
+    base = np.random.PCG64(seed)
+
+    def fill(b):
+        g = np.random.Generator(base.jumped(b + 1))
+        r0, r1 = b * block_rows, min(rows, (b + 1) * block_rows)
+        blk = out[r0:r1]
+        g.standard_normal(out=blk, dtype=np.float32)
+        if scale != 1.0:
+            blk *= np.float32(scale)
+        if not bf16:
+            return
+        bits = blk.view(np.uint32)
+        lsb = (bits >> np.uint32(16)) & np.uint32(1)
+        bits += np.uint32(0x7FFF)
+        bits += lsb
+        bits &= np.uint32(0xFFFF0000)
+
+    workers = threads or min(16, _os.cpu_count() or 1)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(fill, range(nblk)))
+    return out
+
+
 def fwd_inputs(T, n, m, dtype, data_seed=1234):
     """x (T, n) ~ N(0,1) and W (n, m) ~ N(0, 0.02^2), rounded to dtype."""
     g = _rng(data_seed)
