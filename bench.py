@@ -52,6 +52,12 @@ def parse_args():
                     help="skip the per-phase timing pass (for counter collection runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain copy kernel over 256 MiB first (HBM counter calibration)")
+    ap.add_argument("--model-sweep", action="store_true",
+                    help="instead of the benchmark: whole-model training steps of a LLaMA-350M-shaped model "
+                         "(baseline, CompAct r=n/4, r=n/8) over batch sizes; one JSON line per point with the "
+                         "peak allocated memory and the step time")
+    ap.add_argument("--sweep-batches", default="32,64,128,256,512",
+                    help="batch sizes (sequences of 256 tokens) for --model-sweep")
     return ap.parse_args()
 
 
@@ -316,12 +322,74 @@ def cpu_baseline(wl, t_slice, min_secs=10.0):
     }
 
 
+def model_sweep(args):
+    """Peak allocated memory and step time of whole training steps (forward,
+    backward, CompActAdam and torch's Adam) of a LLaMA-350M-shaped model in the
+    paper's pretraining setup (every block linear layer but o compressed, bf16,
+    flash attention, sequences of 256 tokens, vocabulary 32000) against the
+    same model uncompressed, over batch sizes: the measurement behind the
+    paper's peak-memory-vs-batch figure and its throughput/memory figure, on
+    synthetic tokens and random weights."""
+    import gc
+    import torch
+    import paper_2410_15352_amd as cp
+    from paper_2410_15352_amd.block import LlamaModel, block_saved_bytes, make_optimizers
+
+    cp.library()
+    vocab, d, heads, ffn, layers, seq, alpha = 32000, 1024, 16, 2736, 24, 256, 0.25
+    batches = [int(b) for b in args.sweep_batches.split(",")]
+    gen = torch.Generator(device="cuda:0").manual_seed(1234)
+    for rank in (None, d // 4, d // 8):
+        for b in batches:
+            rec = {"sweep": "llama-350m-train-step", "rank": rank, "batch": b, "seq": seq, "tokens": b * seq,
+                   "data": "synthetic", "dtype": "bf16",
+                   "allocated_before_gib": round(torch.cuda.memory_allocated() / 2**30, 3)}
+            model = opts = tokens = loss = None
+            try:
+                model = LlamaModel(vocab, d, heads, ffn, layers, rank=rank, alpha=alpha)
+                opts = make_optimizers(model, lr=1e-3, reseed_period=args.reseed_period)
+                tokens = torch.randint(0, vocab, (b, seq + 1), device="cuda:0", generator=gen)
+
+                def step():
+                    for o in opts:
+                        o.zero_grad()
+                    loss = model(tokens[:, :-1], tokens[:, 1:])
+                    loss.backward()
+                    for o in opts:
+                        o.step()
+                    return loss
+
+                for _ in range(max(1, args.warmup)):
+                    step()
+                torch.cuda.synchronize()
+                torch.cuda.reset_peak_memory_stats()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(args.steps):
+                    loss = step()
+                e1.record()
+                torch.cuda.synchronize()
+                ms = e0.elapsed_time(e1) / args.steps
+                rec.update(peak_gib=round(torch.cuda.max_memory_allocated() / 2**30, 3), ms_per_step=round(ms, 2),
+                           tokens_per_s=round(b * seq / ms * 1e3), loss=round(loss.item(), 4),
+                           saved_per_block_gib=round(block_saved_bytes(b, seq, d, heads, ffn, rank=rank) / 2**30, 4))
+            except torch.cuda.OutOfMemoryError:
+                rec["oom"] = True
+            # the last loss holds the autograd graph, whose nodes hold the model
+            del model, opts, tokens, loss
+            gc.collect()
+            torch.cuda.empty_cache()
+            print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "single-GPU build: this benchmark runs on exactly one GPU "
                                    "(no collectives); rerun with --gpus 1"}), flush=True)
         sys.exit(2)
+    if args.model_sweep:
+        return model_sweep(args)
     import torch
     import paper_2410_15352_amd as cp
     from synthetic import workload

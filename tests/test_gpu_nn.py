@@ -8,14 +8,19 @@
 * CompActAdam: bitwise the ABI's compact_step_batched on the same state, then
   the seed schedule of Alg. 3 (and, when asked, the moments zeroed at a
   re-sample).
-* A LLaMA block (RMSNorm, attention, SwiGLU; all seven linear layers CompAct,
-  q|k|v and gate|up as input groups): dL/dx and every layer's G^ against a
-  float64 CPU reference of the same block with the oracle's P (G^ = P^T x^T
-  dL/do, §3.2); and the activation memory autograd keeps for the block against
-  the same block with ordinary linear layers, where the difference must be
-  exactly the linear inputs minus the z's (Table 1).
+* The LLaMA block of the pretraining setup (paper_2410_15352_amd.block: bf16,
+  flash attention, q|k|v and gate|up as CompAct input groups, down CompAct, o
+  uncompressed; App. D): its output, dL/dx, every CompAct layer's G^ and the
+  o weight's gradient against a float64 CPU reference of the same block with
+  the oracle's P (G^ = P^T x^T dL/do, §3.2).
+* The activations autograd keeps for one block are exactly App. E's Table 7
+  list (block_saved_bytes), for the baseline, for CompAct, and for CompAct with
+  o compressed too (which adds its z: attention keeps its output anyway).
+* A small LLaMA model trains end to end (CompActAdam plus torch's Adam for the
+  rest) and fits a fixed synthetic batch.
 
-Attention runs in float32 on the GPU; every bf16 product in these tests is 2-D.
+Every bf16 product outside the attention kernel is 2-D; attention is the flash
+kernel only (no fallback to a batched-product path).
 """
 import numpy as np
 import pytest
@@ -31,6 +36,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 cp = pytest.importorskip("paper_2410_15352_amd")
 cnn = pytest.importorskip("paper_2410_15352_amd.nn")
+blk_mod = pytest.importorskip("paper_2410_15352_amd.block")
 
 TOL = 3e-2
 
@@ -156,53 +162,16 @@ def test_optimizer_equals_batched_step(reset):
                 assert torch.equal(mod.exp_avg_sq[j], state[k]["V"])
 
 
-# ---- a LLaMA block ------------------------------------------------------------------------------
+# ---- the LLaMA block and model ------------------------------------------------------------------
 
-def _rms(x, g, eps=1e-6):
-    return x * torch.rsqrt(x.square().mean(-1, keepdim=True) + eps) * g
-
-
-class _Block(torch.nn.Module):
-    """Pre-norm LLaMA block: x + o(attn(qkv(norm x))), then + down(silu(gate) * up)(norm).
-    kind "compact": the seven linear layers are CompAct (q|k|v and gate|up as
-    groups); kind "dense": bf16 weights with ordinary autograd (2-D matmuls).
-    Norms, attention and SwiGLU run in float32; linear layers take bf16."""
-
-    def __init__(self, kind, d, heads, ffn, r, Ws, seeds):
-        super().__init__()
-        self.kind, self.d, self.heads, self.ffn = kind, d, heads, ffn
-        Wqkv, Wo, Wgu, Wd = Ws
-        self.g1 = torch.ones(d, device=dev())
-        self.g2 = torch.ones(d, device=dev())
-        if kind == "compact":
-            self.qkv = cnn.CompActGroup(d, [d] * 3, [r] * 3, seeds=seeds[0:3], weight=Wqkv.clone())
-            self.o = cnn.CompActLinear(d, d, r, seed=seeds[3], weight=Wo.clone())
-            self.gu = cnn.CompActGroup(d, [ffn] * 2, [r] * 2, seeds=seeds[4:6], weight=Wgu.clone())
-            self.down = cnn.CompActLinear(ffn, d, ffn // 8, seed=seeds[6], weight=Wd.clone())
-        else:
-            self.Wqkv, self.Wo, self.Wgu, self.Wd = (torch.nn.Parameter(w.clone()) for w in Ws)
-            self.qkv = lambda h: h @ self.Wqkv
-            self.o = lambda h: h @ self.Wo
-            self.gu = lambda h: h @ self.Wgu
-            self.down = lambda h: h @ self.Wd
-
-    def forward(self, x):
-        B, S, d = x.shape
-        h = _rms(x.float(), self.g1).to(torch.bfloat16)
-        qkv = self.qkv(h.reshape(B * S, d)).float().reshape(B, S, 3, self.heads, d // self.heads)
-        q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))
-        a = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True)
-        a = a.transpose(1, 2).reshape(B * S, d).to(torch.bfloat16)
-        x1 = x.float() + self.o(a).float().reshape(B, S, d)
-        h2 = _rms(x1, self.g2).to(torch.bfloat16).reshape(B * S, d)
-        gu = self.gu(h2).float()
-        mlp = (torch.nn.functional.silu(gu[:, :self.ffn]) * gu[:, self.ffn:]).to(torch.bfloat16)
-        return x1 + self.down(mlp).float().reshape(B, S, d)
+def _rms64(x):
+    return x * torch.rsqrt(x.square().mean(-1, keepdim=True) + 1e-6)
 
 
 def _ref_block(x, Ws, heads, ffn):
-    """The block in float64 on the CPU with dense weights; returns the output
-    and, per linear layer, its input and (after backward) its output's grad."""
+    """The block in float64 on the CPU with dense weights (unit norm weights);
+    returns the output and, per linear layer, its input and output tensor
+    (whose .grad holds dL/do after backward)."""
     B, S, d = x.shape
     Wqkv, Wo, Wgu, Wd = Ws
     taps = {}
@@ -213,16 +182,16 @@ def _ref_block(x, Ws, heads, ffn):
         taps[name] = (h, out)
         return out
 
-    h = _rms(x, torch.ones(d, dtype=torch.float64)).reshape(B * S, d)
+    h = _rms64(x).reshape(B * S, d)
     qkv = lin("qkv", h, Wqkv).reshape(B, S, 3, heads, d // heads)
     q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))
     a = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True)
     a = a.transpose(1, 2).reshape(B * S, d)
-    x1 = x + lin("o", a, Wo).reshape(B, S, d)
-    h2 = _rms(x1, torch.ones(d, dtype=torch.float64)).reshape(B * S, d)
+    x5 = x + lin("o", a, Wo).reshape(B, S, d)
+    h2 = _rms64(x5).reshape(B * S, d)
     gu = lin("gu", h2, Wgu)
-    mlp = torch.nn.functional.silu(gu[:, :ffn]) * gu[:, ffn:]
-    return x1 + lin("down", mlp, Wd).reshape(B, S, d), taps
+    act = torch.nn.functional.silu(gu[:, :ffn]) * gu[:, ffn:]
+    return x5 + lin("down", act, Wd).reshape(B, S, d), taps
 
 
 def _block_weights(d, ffn, seed):
@@ -230,41 +199,44 @@ def _block_weights(d, ffn, seed):
     return [normal_bf16_blocked(a, b, seed=seed + i, scale=0.02) for i, (a, b) in enumerate(shapes)]
 
 
-def test_llama_block_gradients_against_float64_reference():
+def test_llama_block_against_float64_reference():
     B, S, d, heads, ffn, r = 2, 128, 512, 8, 1376, 64
     seeds = [((j + 1) << 32) | 77 for j in range(7)]
     Wn = _block_weights(d, ffn, seed=500)
     x_np = normal_bf16_blocked(B * S, d, seed=600).reshape(B, S, d)
     R_np = normal_bf16_blocked(B * S, d, seed=601, bf16=False).reshape(B, S, d)
-    blk = _Block("compact", d, heads, ffn, r, [_dev_bf16(w) for w in Wn], seeds)
+    blk = blk_mod.LlamaBlock(d, heads, ffn, rank=r, seeds=seeds, weights=[_dev_bf16(w) for w in Wn])
+    assert blk.rank_down == ffn * r // d
     x = _dev_bf16(x_np).requires_grad_(True)
     out = blk(x)
-    (out * torch.from_numpy(R_np).float().to(dev())).sum().backward()
+    (out.float() * torch.from_numpy(R_np).to(dev())).sum().backward()
     torch.cuda.synchronize()
 
     xr = torch.from_numpy(np.asarray(x_np, dtype=np.float64)).requires_grad_(True)
     out_r, taps = _ref_block(xr, [torch.from_numpy(np.asarray(w, dtype=np.float64)) for w in Wn], heads, ffn)
     (out_r * torch.from_numpy(np.asarray(R_np, dtype=np.float64))).sum().backward()
 
-    assert oc.rel_fro(to_np(out.detach()).reshape(B * S, d), out_r.detach().numpy().reshape(B * S, d)) <= TOL
-    assert oc.rel_fro(to_np(x.grad).reshape(B * S, d), xr.grad.numpy().reshape(B * S, d)) <= TOL
-    # G^_j = P_j^T h^T dL/do_j for every projection (§3.2), P_j from the oracle's stream
-    layers = [("qkv", blk.qkv), ("o", blk.o), ("gu", blk.gu), ("down", blk.down)]
-    for name, mod in layers:
+    flat = lambda a: a.reshape(B * S, d)
+    assert oc.rel_fro(flat(to_np(out.detach())), flat(out_r.detach().numpy())) <= TOL
+    assert oc.rel_fro(flat(to_np(x.grad)), flat(xr.grad.numpy())) <= TOL
+    # the uncompressed o: dL/dW_o = x3^T dL/do
+    a_r, o_r = taps["o"]
+    assert oc.rel_fro(to_np(blk.o.weight.grad), a_r.detach().numpy().T @ o_r.grad.numpy()) <= TOL
+    # G^_j = P_j^T x^T dL/do_j for every CompAct projection (§3.2), P_j from the oracle's stream
+    for name, mod in (("qkv", blk.qkv), ("gu", blk.gu), ("down", blk.down)):
         h, o = taps[name]
         hd, dod = h.detach().numpy(), o.grad.numpy()
         mo = 0
         for j, (m, r_j) in enumerate(zip(mod.ms, mod.rs)):
-            P = projection(mod.seeds[j], mod.n, r_j)
-            G_ref = P.T @ (hd.T @ dod[:, mo:mo + m])
+            G_ref = projection(mod.seeds[j], mod.n, r_j).T @ (hd.T @ dod[:, mo:mo + m])
             err = oc.rel_fro(mod.ghat[j].cpu().numpy(), G_ref)
             assert err <= TOL, (name, j, err)
             mo += m
 
 
-def _activation_bytes(blk, x):
-    """Bytes of the distinct storages autograd keeps for blk(x), weights and
-    module buffers excluded, and the allocator's growth over the forward."""
+def _saved_bytes(blk, x):
+    """Bytes of the distinct storages autograd keeps for blk(x), parameters and
+    module buffers (the weights) excluded, and the allocator's growth."""
     keep = {p.data_ptr() for p in blk.parameters()} | {b.data_ptr() for b in blk.buffers()}
     torch.cuda.synchronize()
     before = torch.cuda.memory_allocated()
@@ -275,34 +247,63 @@ def _activation_bytes(blk, x):
     for t in saved:
         s = t.untyped_storage()
         if s.data_ptr() not in keep:
-            storages[s.data_ptr()] = s.nbytes()
+            storages[(s.device.type, s.data_ptr())] = s.nbytes()
     del out, saved
     return sum(storages.values()), grown
 
 
-def test_llama_block_activation_memory():
+def test_llama_block_saved_activations_table7():
     # LLaMA-350M block shapes: d = 1024, 16 heads, ffn = 2736, r = d / 8; 4 x 1024 tokens
     B, S, d, heads, ffn, r = 4, 1024, 1024, 16, 2736, 128
-    T = B * S
-    seeds = [((j + 1) << 32) | 5 for j in range(7)]
     Ws = [_dev_bf16(w) for w in _block_weights(d, ffn, seed=700)]
-    x = _dev_bf16(normal_bf16_blocked(T, d, seed=701)).reshape(B, S, d).requires_grad_(True)
+    x = _dev_bf16(normal_bf16_blocked(B * S, d, seed=701)).reshape(B, S, d).requires_grad_(True)
     res = {}
-    for kind in ("dense", "compact"):
-        blk = _Block(kind, d, heads, ffn, r, Ws, seeds)
-        blk(x).sum().backward()                 # warm-up: library workspaces, allocator pools
-        res[kind] = _activation_bytes(blk, x)
+    for name, rank, co in (("baseline", None, False), ("compact", r, False), ("compact+o", r, True)):
+        blk = blk_mod.LlamaBlock(d, heads, ffn, rank=rank, compress_o=co, weights=[w.clone() for w in Ws])
+        blk(x).float().sum().backward()             # warm-up: library workspaces, allocator pools
+        saved, grown = _saved_bytes(blk, x)
+        expect = blk_mod.block_saved_bytes(B, S, d, heads, ffn, rank=rank, compress_o=co)
+        res[name] = (saved, grown, expect)
+        print(f"\n{name:10s} saved {saved / 2**20:8.2f} MiB (Table 7: {expect / 2**20:8.2f}), "
+              f"allocator growth {grown / 2**20:8.2f} MiB")
+        assert saved == expect, name
         del blk
-    # dense keeps the bf16 inputs of its four products (norm(x), attention
-    # output, norm(x1), SwiGLU output); CompAct keeps z for each projection
-    pad = lambda c: (c + 7) // 8 * 8
-    dense_in = 2 * T * (d + d + d + ffn)
-    compact_z = 2 * T * (pad(3 * r) + pad(r) + pad(2 * r) + pad(ffn // 8))
-    saved_d, grown_d = res["dense"]
-    saved_c, grown_c = res["compact"]
-    print(f"\nsaved activations: dense {saved_d / 2**20:.1f} MiB, CompAct {saved_c / 2**20:.1f} MiB; "
-          f"allocator growth {grown_d / 2**20:.1f} vs {grown_c / 2**20:.1f} MiB")
-    assert saved_d - saved_c == dense_in - compact_z
     # the caching allocator may hand out a cached block up to 1 MiB larger than
-    # asked (it does not split smaller remainders), so live bytes agree only to that
-    assert abs((grown_d - grown_c) - (dense_in - compact_z)) <= 4 * 2**20
+    # asked, so live bytes agree with the saved bytes only to a few MiB
+    for name in ("compact", "compact+o"):
+        d_saved = res["baseline"][0] - res[name][0]
+        d_grown = res["baseline"][1] - res[name][1]
+        assert abs(d_grown - d_saved) <= 4 * 2**20, name
+
+
+def _train_small(rank, steps, lr):
+    vocab, d, heads, ffn, layers = 512, 256, 4, 688, 2
+    B, S = 8, 64
+    torch.manual_seed(0)
+    model = blk_mod.LlamaModel(vocab, d, heads, ffn, layers, rank=rank)
+    opts = blk_mod.make_optimizers(model, lr=lr, reseed_period=10)
+    g = torch.Generator(device="cpu").manual_seed(5)
+    tokens = torch.randint(0, vocab, (B, S + 1), generator=g).to(dev())
+    losses = []
+    for _ in range(steps):
+        for o in opts:
+            o.zero_grad()
+        loss = model(tokens[:, :-1], tokens[:, 1:])
+        loss.backward()
+        for o in opts:
+            o.step()
+        losses.append(loss.item())
+    return model, opts, np.array(losses)
+
+
+def test_small_llama_model_trains():
+    steps, vocab = 100, 512
+    model, opts, L = _train_small(64, steps, 5e-3)
+    _, _, L_dense = _train_small(None, steps, 5e-3)
+    print("\nloss at steps 1, 25, 50, 100: CompAct r=64", [round(float(L[i]), 3) for i in (0, 24, 49, 99)],
+          " dense", [round(float(L_dense[i]), 3) for i in (0, 24, 49, 99)])
+    assert len(opts) == 2 and len(model.compact_modules()) == 3 * len(model.blocks)
+    assert np.all(np.isfinite(L))
+    assert abs(L[0] - np.log(vocab)) < 0.5           # near uniform at initialisation
+    assert L[-1] < 0.5 * L[0]                        # fits the fixed batch
+    assert model.blocks[0].qkv.seeds[0] == (1 << 32) + steps // 10   # re-sampled every 10 steps
