@@ -39,11 +39,12 @@ def _f64(a):
     return np.asarray(a, dtype=F64)
 
 
-def ref_fwd(x, W, seed: int, r: int, identity: bool = False):
-    """Alg. 1.  x: (T, n), W: (n, m) -> (o (T, m), z (T, r))."""
+def ref_fwd(x, W, seed: int, r: int, identity: bool = False, sparse_s: int = 0):
+    """Alg. 1.  x: (T, n), W: (n, m) -> (o (T, m), z (T, r)).  sparse_s > 0
+    takes the sparse JL projection with that many draws per row (§5)."""
     x, W = _f64(x), _f64(W)
     n = x.shape[1]
-    P = projection(seed, n, r, identity)
+    P = projection(seed, n, r, identity, sparse_s)
     o = x @ W
     z = x @ P
     return o, z
@@ -73,7 +74,7 @@ def ref_adam(Ghat, M, V, t: int, beta1: float, beta2: float, eps: float):
 
 def ref_step(W, Ghat, M, V, seed: int, r: int, t: int, lr: float, beta1: float,
              beta2: float, eps: float, alpha: float, identity: bool = False,
-             rho: str = "adam"):
+             rho: str = "adam", sparse_s: int = 0):
     """Alg. 3.  Returns (W_{t+1}, M_t, V_t, dW) with dW = W_{t+1} - W_t.
 
     ``rho="sgd"`` replaces the Adam normalisation by the identity (N = G^);
@@ -86,7 +87,7 @@ def ref_step(W, Ghat, M, V, seed: int, r: int, t: int, lr: float, beta1: float,
         M_t, V_t, N_t = _f64(M), _f64(V), _f64(Ghat)
     else:
         raise ValueError(rho)
-    P = projection(seed, n, r, identity)
+    P = projection(seed, n, r, identity, sparse_s)
     G_tilde = F64(alpha) * (P @ N_t)
     dW = -F64(lr) * G_tilde
     return W + dW, M_t, V_t, dW

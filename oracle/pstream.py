@@ -26,6 +26,16 @@ Element (i, j) of G (unscaled, N(0,1)):
     G[i, j] = rho * cos(theta) if i is even else rho * sin(theta)
 
 P = G / sqrt(r) (variance 1/r, the reading of §3.3 that makes P P^T ~ I).
+
+The sparse Johnson-Lindenstrauss projection (the ablation's sparse JL
+matrices, §5, after Dasgupta, Kumar and Sarlos, 2010; the paper fixes no
+parameters) uses the same generator with counter word 2 set to a tag, s
+signed unit draws per row and P = S / sqrt(s):
+    draw q of row i, q = 0 .. s-1:
+      (w0, w1, w2, w3) = Philox4x32-10((i, q >> 1, SJLT_TAG, 0), key)
+      (a, b) = (w0, w1) for even q, (w2, w3) for odd q
+      column floor(a r / 2^32), sign +1 if b < 2^31 else -1
+    S[i, c] = sum of the signs of row i's draws that land on column c.
 """
 from __future__ import annotations
 
@@ -245,10 +255,35 @@ def gaussian_element(seed: int, i: int, j: int) -> np.float32:
     return (g_even if (i & 1) == 0 else g_odd)[0]
 
 
-def projection(seed: int, n: int, r: int, identity: bool = False) -> np.ndarray:
-    """P in fp64: G / sqrt(r) (§3.3), or the identity (requires r == n)."""
+SJLT_TAG = 0x4A4C5350
+
+
+def sparse_jl_raw(seed: int, n: int, r: int, s: int) -> np.ndarray:
+    """S (n x r, float64 holding integers): the sparse JL stream, s draws per row."""
+    if s < 1:
+        raise ValueError("s >= 1 draws per row")
+    k0, k1 = seed_key(seed)
+    pairs = (s + 1) // 2
+    i = np.arange(n, dtype=U32)[:, None]
+    p = np.arange(pairs, dtype=U32)[None, :]
+    w0, w1, w2, w3 = philox4x32_10(i, p, U32(SJLT_TAG), U32(0), k0, k1)
+    # draw q = 2p takes (w0, w1) of pair p, draw q = 2p + 1 takes (w2, w3)
+    a = np.stack([w0, w2], axis=-1).reshape(n, 2 * pairs)[:, :s]
+    b = np.stack([w1, w3], axis=-1).reshape(n, 2 * pairs)[:, :s]
+    col = ((a.astype(U64) * U64(r)) >> U64(32)).astype(np.int64)
+    sign = np.where((b >> U32(31)) != 0, -1.0, 1.0)
+    S = np.zeros((n, r), dtype=np.float64)
+    np.add.at(S, (np.repeat(np.arange(n), s), col.ravel()), sign.ravel())
+    return S
+
+
+def projection(seed: int, n: int, r: int, identity: bool = False, sparse_s: int = 0) -> np.ndarray:
+    """P in fp64: G / sqrt(r) (§3.3), the identity (requires r == n), or, with
+    sparse_s = s > 0, the sparse JL projection S / sqrt(s)."""
     if identity:
         if r != n:
             raise ValueError("identity projection requires r == n")
         return np.eye(n, dtype=np.float64)
+    if sparse_s:
+        return sparse_jl_raw(seed, n, r, sparse_s) / np.sqrt(np.float64(sparse_s))
     return gaussian_raw(seed, n, r).astype(np.float64) / np.sqrt(np.float64(r))
