@@ -52,6 +52,9 @@ def parse_args():
                     help="skip the per-phase timing pass (for counter collection runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain copy kernel over 256 MiB first (HBM counter calibration)")
+    ap.add_argument("--proj", default="gaussian",
+                    help="projection: gaussian (the paper's method), or sparse-jl[:s] (the ablation's sparse JL, "
+                         "s draws per row, default 8)")
     ap.add_argument("--model-sweep", action="store_true",
                     help="instead of the benchmark: whole-model training steps of a LLaMA-350M-shaped model "
                          "(baseline, CompAct r=n/4, r=n/8) over batch sizes; one JSON line per point with the "
@@ -95,11 +98,12 @@ def input_groups(wl, grouped=True):
 class Model:
     """Device buffers of every CompAct linear layer of a workload."""
 
-    def __init__(self, wl, fwd_mode, grouped=True):
+    def __init__(self, wl, fwd_mode, grouped=True, proj="gaussian"):
         import torch
         import paper_2410_15352_amd as cp
         from synthetic import bf16_bits, bf16_round
         self.wl, self.cp, self.torch = wl, cp, torch
+        self.proj = proj
         dev = torch.device("cuda:0")
         T = wl.tokens
         assert wl.dtype == "bf16", "the benchmark workloads are bf16"
@@ -174,10 +178,10 @@ class Model:
         Ls = [self.wl.layers[i] for i in g]
         x, y = self.x[Ls[0].n], self.y[self.msum[gi]]
         if len(g) == 1:
-            self.cp.compact_fwd(x, self.Wg[gi], y, self.zg[gi], self.seeds[g[0]], ws=self.ws_f)
+            self.cp.compact_fwd(x, self.Wg[gi], y, self.zg[gi], self.seeds[g[0]], proj=self.proj, ws=self.ws_f)
         else:
             self.cp.compact_fwd_group(x, self.Wg[gi], y, self.zg[gi], [L.m for L in Ls], [L.r for L in Ls],
-                                      [self.seeds[i] for i in g], ws=self.ws_f)
+                                      [self.seeds[i] for i in g], proj=self.proj, ws=self.ws_f)
 
     def bwd_dx(self, gi):
         """dL/dx of a group: one GEMM over its concatenated weight."""
@@ -202,13 +206,14 @@ class Model:
     def upd(self, i, t):
         wl = self.wl
         self.cp.compact_step(self.W[i], self.G[i], self.M[i], self.V[i], self.seeds[i], t, wl.lr,
-                             wl.beta1, wl.beta2, wl.eps, wl.alpha, ws=self.ws_s)
+                             wl.beta1, wl.beta2, wl.eps, wl.alpha, proj=self.proj, ws=self.ws_s)
 
     def upd_all(self, t):
         """Alg. 3 for every layer: batched Adam and decompression launches."""
         wl = self.wl
         self.batch.set_seeds(self.seeds)
-        self.cp.compact_step_batched(self.batch, t, wl.lr, wl.beta1, wl.beta2, wl.eps, ws=self.ws_s)
+        self.cp.compact_step_batched(self.batch, t, wl.lr, wl.beta1, wl.beta2, wl.eps, proj=self.proj,
+                                     ws=self.ws_s)
 
     def step(self, reseed_period):
         self.t += 1
@@ -271,7 +276,7 @@ def time_phases(model, torch, reps=2, step_reps=10):
     return out
 
 
-def cpu_baseline(wl, t_slice, min_secs=10.0):
+def cpu_baseline(wl, t_slice, min_secs=10.0, sparse_s=0):
     """The oracle (numpy fp64) timed on this host's cores on a bounded sample:
     fwd + bwd + step of each distinct layer shape on t_slice tokens (the full
     step when t_slice >= tokens), repeated until min_secs of CPU work, then
@@ -299,11 +304,11 @@ def cpu_baseline(wl, t_slice, min_secs=10.0):
     while reps == 0 or spent < min_secs:
         for (n, m, r), (x, W, dy) in inputs.items():
             t0 = time.perf_counter()
-            _, z = oc.ref_fwd(x, W, 1 << 32, r)
+            _, z = oc.ref_fwd(x, W, 1 << 32, r, sparse_s=sparse_s)
             _, G = oc.ref_bwd(dy, z, W)
             t1 = time.perf_counter()
             oc.ref_step(W, G, np.zeros_like(G), np.zeros_like(G), 1 << 32, r, 1, wl.lr, wl.beta1,
-                        wl.beta2, wl.eps, wl.alpha)
+                        wl.beta2, wl.eps, wl.alpha, sparse_s=sparse_s)
             t2 = time.perf_counter()
             t_tok[(n, m, r)] += t1 - t0
             t_step[(n, m, r)] += t2 - t1
@@ -404,7 +409,7 @@ def main():
     wl = workload(args.workload)
     T = wl.tokens
     print(f"[bench] workload {wl.name}: {len(wl.layers)} layers, {T} tokens; allocating", file=sys.stderr, flush=True)
-    model = Model(wl, args.fwd_mode, grouped=not args.no_group)
+    model = Model(wl, args.fwd_mode, grouped=not args.no_group, proj=args.proj)
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -448,7 +453,9 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(wl, args.cpu_tokens)
+        code = cp.proj_code(args.proj)
+        sparse_s = ((code >> 8) or cp.SPARSE_JL_DEFAULT_S) if (code & 0xFF) == cp.PROJ["sparse-jl"] else 0
+        cpu = cpu_baseline(wl, args.cpu_tokens, sparse_s=sparse_s)
     act = [{"layer": L.name, "n": L.n, "r": L.r, "saved_bytes": 2 * T * L.r, "uncompressed_bytes": 2 * T * L.n}
            for L in wl.distinct_shapes()]
     line = {
@@ -466,7 +473,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.description, "tokens_per_step": T, "layers": nl,
                    "input_groups": "q,k,v and gate,up share their input" if not args.no_group else "none",
-                   "fwd_mode": args.fwd_mode, "parallelism": "single GPU"},
+                   "fwd_mode": args.fwd_mode, "projection": args.proj, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "phases_ms": {k: round(v, 4) for k, v in phases.items()},

@@ -62,9 +62,29 @@ typedef enum {
 typedef enum { COMPACT_F32 = 0, COMPACT_BF16 = 1 } compact_dtype;
 
 typedef enum {
-  COMPACT_PROJ_GAUSSIAN = 0, /* P = G / sqrt(r), G the seeded N(0,1) stream  */
-  COMPACT_PROJ_IDENTITY = 1  /* P = I (requires r == n): uncompressed layer  */
+  COMPACT_PROJ_GAUSSIAN = 0,  /* P = G / sqrt(r), G the seeded N(0,1) stream  */
+  COMPACT_PROJ_IDENTITY = 1,  /* P = I (requires r == n): uncompressed layer  */
+  COMPACT_PROJ_SPARSE_JL = 2  /* P = S / sqrt(s), S the seeded sparse JL
+                                 stream with s signed draws per row (below)  */
 } compact_proj;
+
+/*
+ * Sparse Johnson-Lindenstrauss projection (the ablation's sparse JL matrices,
+ * §5, after Dasgupta, Kumar and Sarlos 2010; the paper gives no parameters).
+ * The `proj` argument COMPACT_PROJ_SPARSE_JL_S(s) selects s draws per row,
+ * 1 <= s <= 64; plain COMPACT_PROJ_SPARSE_JL means s = 8.  Row i of S receives
+ * s unit draws with random signs at hashed columns (draws on one column add):
+ *   draw q of row i, 0 <= q < s:
+ *     (w0, w1, w2, w3) = Philox4x32-10((i, q >> 1, 0x4A4C5350, 0), key(seed))
+ *     (a, b) = (w0, w1) for even q, (w2, w3) for odd q
+ *     column floor(a r / 2^32), sign +1 if b < 2^31 else -1
+ * with key(seed) as for the Gaussian stream (compact_pstream).  E[P P^T] = I
+ * as for the Gaussian, so Alg. 3's decompression stays unbiased.  S holds
+ * small integers; the forward rounds P = S / sqrt(s) to bf16 once (exact for
+ * s = 1, 4, 16, 64) and the update applies 1/sqrt(s) in fp32.
+ */
+#define COMPACT_SPARSE_JL_DEFAULT_S 8
+#define COMPACT_PROJ_SPARSE_JL_S(s) (COMPACT_PROJ_SPARSE_JL | ((s) << 8))
 
 /*
  * Forward pass, Alg. 1:  y = x W  and  z = x P.
@@ -74,7 +94,8 @@ typedef enum {
  *   y  [tokens x m]  (ld ldy)  output o = x W
  *   z  [tokens x r]  (ld ldz)  compressed activation saved for the backward pass
  *   seed  layer seed; P[i][j] = G(seed, i, j) / sqrt(r) (the P stream, below)
- *   proj  COMPACT_PROJ_GAUSSIAN, or COMPACT_PROJ_IDENTITY with r == n
+ *   proj  COMPACT_PROJ_GAUSSIAN, COMPACT_PROJ_IDENTITY with r == n, or
+ *         COMPACT_PROJ_SPARSE_JL[_S(s)] (P = S / sqrt(s), above)
  *   ws, ws_bytes  optional workspace of at least
  *         compact_fwd_workspace_bytes(n, m, r, dtype) bytes (bf16 path).  With
  *         it the call stages W^T and this call's P^T (r x n, P rounded to
@@ -224,6 +245,16 @@ size_t compact_step_batched_workspace_bytes(const compact_layer* layers, int32_t
  * stream is reproducible bit for bit on any IEEE fp32 machine.
  */
 int compact_pstream(uint64_t seed, int64_t n, int64_t r, float* out, int64_t ld, void* stream);
+
+/*
+ * The unscaled stream of any projection, exported for tests: out [n x r]
+ * (ld >= r, device pointer, fp32) receives G(seed, i, j) for
+ * COMPACT_PROJ_GAUSSIAN (as compact_pstream), the identity for
+ * COMPACT_PROJ_IDENTITY (r == n), or the integer matrix S(seed, i, j) for
+ * COMPACT_PROJ_SPARSE_JL[_S(s)].  P = scale x out with scale 1/sqrt(r),
+ * 1 and 1/sqrt(s).
+ */
+int compact_projection(uint64_t seed, int64_t n, int64_t r, int proj, float* out, int64_t ld, void* stream);
 
 /*
  * Test export: the Box-Muller step of the P stream applied to arbitrary word

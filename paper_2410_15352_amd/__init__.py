@@ -19,9 +19,32 @@ import ctypes
 from . import _lib
 
 F32, BF16 = 0, 1
-PROJ = {"gaussian": 0, "identity": 1}
+PROJ = {"gaussian": 0, "identity": 1, "sparse-jl": 2}
+SPARSE_JL_DEFAULT_S = 8
 
-__all__ = ["compact_fwd", "compact_fwd_group", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
+
+def proj_code(proj):
+    """The ABI's compact_proj code of a projection: "gaussian", "identity",
+    "sparse-jl" (s = 8 draws per row), "sparse-jl:<s>", or an int code."""
+    if isinstance(proj, int):
+        return proj
+    if proj.startswith("sparse-jl:"):
+        s_ = int(proj.split(":", 1)[1])
+        if not 1 <= s_ <= 64:
+            raise ValueError("sparse-jl draws per row must be in [1, 64]")
+        return PROJ["sparse-jl"] | (s_ << 8)
+    return PROJ[proj]
+
+
+def proj_scale(proj, r):
+    """P = proj_scale x the unscaled stream (compact_projection's output)."""
+    code = proj_code(proj)
+    kind, s_ = code & 0xFF, code >> 8
+    if kind == PROJ["identity"]:
+        return 1.0
+    return 1.0 / float(s_ or SPARSE_JL_DEFAULT_S if kind == PROJ["sparse-jl"] else r) ** 0.5
+
+__all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "proj_scale", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
            "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
            "LayerBatch", "prepare_layers",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
@@ -104,7 +127,7 @@ def compact_fwd(x, W, y, z, seed, proj="gaussian", ws=None, stream=None):
     r = z.shape[1]
     wp, wb = _ws(ws)
     st = lib.compact_fwd(_ptr(x), _ld(x), _ptr(W), _ld(W), _ptr(y), _ld(y), _ptr(z), _ld(z),
-                         T, n, m, r, int(seed) & (2**64 - 1), PROJ[proj], _dtype_code(x),
+                         T, n, m, r, int(seed) & (2**64 - 1), proj_code(proj), _dtype_code(x),
                          wp, wb, _stream(stream, x))
     _check("compact_fwd", st)
 
@@ -134,7 +157,7 @@ def compact_fwd_group(x, W, y, z, ms, rs, seeds, proj="gaussian", ws=None, strea
     count, m_arr, r_arr, s_arr = _group_arrays(ms, rs, seeds)
     wp, wb = _ws(ws)
     st = lib.compact_fwd_group(_ptr(x), _ld(x), _ptr(W), _ld(W), _ptr(y), _ld(y), _ptr(z), _ld(z), T, n, count,
-                               m_arr, r_arr, s_arr, PROJ[proj], _dtype_code(x), wp, wb, _stream(stream, x))
+                               m_arr, r_arr, s_arr, proj_code(proj), _dtype_code(x), wp, wb, _stream(stream, x))
     _check("compact_fwd_group", st)
 
 
@@ -166,7 +189,7 @@ def compact_step(W, G, M, V, seed, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, alph
     wp, wb = _ws(ws)
     st = lib.compact_step(_ptr(W), _ld(W), _ptr(G), _ptr(M), _ptr(V), n, m, r,
                           int(seed) & (2**64 - 1), int(t), float(lr), float(beta1), float(beta2),
-                          float(eps), float(alpha), PROJ[proj], d_code, w_code, wp, wb,
+                          float(eps), float(alpha), proj_code(proj), d_code, w_code, wp, wb,
                           _stream(stream, W))
     _check("compact_step", st)
 
@@ -230,7 +253,7 @@ def compact_step_batched(layers, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, proj="
     w_code = _dtype_code(b.w0)
     wp, wb = _ws(ws)
     st = lib.compact_step_batched(b.arr, b.count, int(t), float(lr), float(beta1), float(beta2),
-                                  float(eps), PROJ[proj], BF16, w_code, wp, wb, _stream(stream, b.w0))
+                                  float(eps), proj_code(proj), BF16, w_code, wp, wb, _stream(stream, b.w0))
     _check("compact_step_batched", st)
 
 
@@ -241,6 +264,16 @@ def compact_pstream(seed, out, stream=None):
     st = lib.compact_pstream(int(seed) & (2**64 - 1), n, r, _ptr(out), _ld(out),
                              _stream(stream, out))
     _check("compact_pstream", st)
+
+
+def compact_projection(seed, out, proj="gaussian", stream=None):
+    """Fill out (n, r) fp32 with the unscaled stream of a projection: G, the
+    identity, or the sparse JL integers S."""
+    lib = _lib.load()
+    n, r = out.shape
+    st = lib.compact_projection(int(seed) & (2**64 - 1), n, r, proj_code(proj), _ptr(out), _ld(out),
+                                _stream(stream, out))
+    _check("compact_projection", st)
 
 
 def compact_pstream_boxmuller(a, b, g_even, g_odd, stream=None):

@@ -27,6 +27,7 @@ SIGNATURES = {
                              c_vp]),
     "compact_step_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_int]),
     "compact_pstream": (c_int, [c_u64, c_i64, c_i64, c_vp, c_i64, c_vp]),
+    "compact_projection": (c_int, [c_u64, c_i64, c_i64, c_int, c_vp, c_i64, c_vp]),
     "compact_pstream_boxmuller": (c_int, [c_vp, c_vp, c_vp, c_vp, c_i64, c_vp]),
     "compact_next_seed": (c_u64, [c_u64, c_i64, c_i64]),
     "compact_saved_activation_elems": (c_i64, [c_i64, c_i64, c_i64]),

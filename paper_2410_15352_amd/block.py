@@ -1,10 +1,10 @@
 """A LLaMA decoder block and model whose linear layers are CompAct layers, in the
-setup of the paper's pretraining experiments (App. D, App. E):
+setup of the paper's pretraining experiments (App. B, App. E):
 
 * q, k, v (one input group) and gate, up (one input group) and down are CompAct
   layers (Alg. 1-3); the attention output projection stays uncompressed,
   because its input is the attention output that flash attention keeps anyway
-  (App. D, "CompAct and FlashAttention").
+  (App. B.2, "CompAct and FlashAttention").
 * Everything runs in bf16; RMSNorm saves its input and the b x l inverse RMS
   only (Table 7 counts no type conversion); attention is flash attention.
 * With rank=None every linear layer is an ordinary bf16 layer (the baseline).
@@ -82,7 +82,7 @@ class LlamaBlock(torch.nn.Module):
     memory only where attention does not keep its output)."""
 
     def __init__(self, d, heads, ffn, rank=None, rank_down=None, seeds=None, alpha=1.0,
-                 compress_o=False, device="cuda", weights=None):
+                 compress_o=False, device="cuda", weights=None, proj="gaussian"):
         super().__init__()
         self.d, self.heads, self.ffn = d, heads, ffn
         self.rank = rank
@@ -94,17 +94,17 @@ class LlamaBlock(torch.nn.Module):
         self.norm2 = RMSNorm(d, device=device)
         if rank:
             self.qkv = CompActGroup(d, [d] * 3, [rank] * 3, seeds=seeds[0:3], alpha=alpha, device=device,
-                                    weight=Wqkv)
+                                    weight=Wqkv, proj=proj)
             self.gu = CompActGroup(d, [ffn] * 2, [rank] * 2, seeds=seeds[4:6], alpha=alpha, device=device,
-                                   weight=Wgu)
+                                   weight=Wgu, proj=proj)
             self.down = CompActLinear(ffn, d, self.rank_down, seed=seeds[6], alpha=alpha, device=device,
-                                      weight=Wdown)
+                                      weight=Wdown, proj=proj)
         else:
             self.qkv = DenseLinear(d, 3 * d, device, Wqkv)
             self.gu = DenseLinear(d, 2 * ffn, device, Wgu)
             self.down = DenseLinear(ffn, d, device, Wdown)
         if self.compress_o:
-            self.o = CompActLinear(d, d, rank, seed=seeds[3], alpha=alpha, device=device, weight=Wo)
+            self.o = CompActLinear(d, d, rank, seed=seeds[3], alpha=alpha, device=device, weight=Wo, proj=proj)
         else:
             self.o = DenseLinear(d, d, device, Wo)
 
@@ -152,11 +152,11 @@ class LlamaModel(torch.nn.Module):
     """Token embedding, n_layers blocks, final RMSNorm and the output layer
     (uncompressed), with the mean cross-entropy of next-token prediction."""
 
-    def __init__(self, vocab, d, heads, ffn, n_layers, rank=None, alpha=1.0, device="cuda"):
+    def __init__(self, vocab, d, heads, ffn, n_layers, rank=None, alpha=1.0, device="cuda", proj="gaussian"):
         super().__init__()
         self.embed = torch.nn.Parameter((0.02 * torch.randn(vocab, d, device=device)).to(torch.bfloat16))
         self.blocks = torch.nn.ModuleList(
-            LlamaBlock(d, heads, ffn, rank=rank, alpha=alpha, device=device,
+            LlamaBlock(d, heads, ffn, rank=rank, alpha=alpha, device=device, proj=proj,
                        seeds=[((7 * i + j + 1) << 32) for j in range(7)])
             for i in range(n_layers))
         self.norm = RMSNorm(d, device=device)

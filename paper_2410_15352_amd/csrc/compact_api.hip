@@ -66,8 +66,13 @@ int check_dense(const char* name, const void* p) {
 int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
   if (tokens < 0 || n < 1 || m < 1) return fail(COMPACT_EINVAL, "bad shape tokens=%lld n=%lld m=%lld", (long long)tokens, (long long)n, (long long)m);
   if (r < 1 || r > n) return fail(COMPACT_EINVAL, "rank r=%lld must satisfy 1 <= r <= n=%lld", (long long)r, (long long)n);
-  if (proj != COMPACT_PROJ_GAUSSIAN && proj != COMPACT_PROJ_IDENTITY) return fail(COMPACT_EINVAL, "unknown projection %d", proj);
-  if (proj == COMPACT_PROJ_IDENTITY && r != n) return fail(COMPACT_EINVAL, "identity projection needs r == n (r=%lld, n=%lld)", (long long)r, (long long)n);
+  const int kind = proj & 0xFF, draws = proj >> 8;
+  if (proj < 0 || (kind != COMPACT_PROJ_GAUSSIAN && kind != COMPACT_PROJ_IDENTITY && kind != COMPACT_PROJ_SPARSE_JL))
+    return fail(COMPACT_EINVAL, "unknown projection %d", proj);
+  if (kind != COMPACT_PROJ_SPARSE_JL && draws != 0) return fail(COMPACT_EINVAL, "unknown projection %d", proj);
+  if (kind == COMPACT_PROJ_SPARSE_JL && draws > kSjltMaxS)
+    return fail(COMPACT_EINVAL, "sparse projection: %d draws per row (at most %d)", draws, kSjltMaxS);
+  if (kind == COMPACT_PROJ_IDENTITY && r != n) return fail(COMPACT_EINVAL, "identity projection needs r == n (r=%lld, n=%lld)", (long long)r, (long long)n);
   if (n > (int64_t(1) << 31) || r > (int64_t(1) << 31)) return fail(COMPACT_EUNSUPPORTED, "n and r must be below 2^31");
   return COMPACT_OK;
 }
@@ -161,9 +166,25 @@ int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + r; }
 int w4_tiles(int64_t cols) { return static_cast<int>(ceil_div(cols, kW4Tile)); }
 int64_t n_ld(int64_t m) { return round_up(m, 8); }
 
-float inv_sqrt_rank(int64_t r, int proj) {
-  return proj == COMPACT_PROJ_IDENTITY ? 1.0f : static_cast<float>(1.0 / std::sqrt(static_cast<double>(r)));
+// The projection of a (validated) compact_proj code: kind, rank and, for the
+// sparse projection, the draws per row (0 in the code means the default).
+ProjDesc proj_desc(int proj, int64_t r) {
+  ProjDesc d{};
+  d.kind = proj & 0xFF;
+  d.r = static_cast<int>(r);
+  d.s = d.kind == COMPACT_PROJ_SPARSE_JL ? ((proj >> 8) != 0 ? (proj >> 8) : COMPACT_SPARSE_JL_DEFAULT_S) : 0;
+  return d;
 }
+
+// P = scale x the unscaled stream: 1/sqrt(r) for the Gaussian, 1/sqrt(s) for
+// the sparse projection, 1 for the identity.
+double proj_scale64(int proj, int64_t r) {
+  const ProjDesc d = proj_desc(proj, r);
+  if (d.kind == COMPACT_PROJ_IDENTITY) return 1.0;
+  return 1.0 / std::sqrt(static_cast<double>(d.kind == COMPACT_PROJ_SPARSE_JL ? d.s : r));
+}
+
+float proj_scale(int proj, int64_t r) { return static_cast<float>(proj_scale64(proj, r)); }
 
 int set_lds(const void* fn, size_t bytes) {
   if (bytes <= 65536) return COMPACT_OK;
@@ -199,7 +220,7 @@ OperandF32 mem_operand(const float* p, int64_t su, int64_t sv, int64_t U, int64_
 OperandF32 pgen_operand(uint64_t seed, int64_t n, int64_t r, int proj) {
   OperandF32 o{};
   o.pgen = 1;
-  o.identity = proj == COMPACT_PROJ_IDENTITY;
+  o.proj = proj_desc(proj, r);
   o.key = philox_key(seed);
   o.U = n;
   o.V = r;
@@ -287,7 +308,7 @@ size_t fwd_group_ws_bytes(int64_t n, const FwdGroup& G) {
 // to false (and launches nothing) when the persistent kernel does not take
 // the shape.
 int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy, void* z,
-                 int64_t ldz, int64_t tokens, int64_t n, const FwdGroup& G, int identity, void* ws,
+                 int64_t ldz, int64_t tokens, int64_t n, const FwdGroup& G, int proj, void* ws,
                  hipStream_t s, bool& taken) {
   int st;
   const int64_t ldb = pt_ld(n);
@@ -300,7 +321,8 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
   fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = G.msum;
   fs.b = bs; fs.ldb = ldb;
   fs.count = G.count;
-  fs.identity = identity;
+  fs.kind = proj_desc(proj, 1).kind;
+  fs.sparse_s = proj_desc(proj, 1).s;
   fs.tiles_c = static_cast<int>(ceil_div(G.msum, 64));
   fs.pt_begin[0] = 0;
   int64_t row = mp;
@@ -308,8 +330,8 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
     fs.row_off[j] = row;
     fs.r[j] = G.r[j];
     fs.key[j] = philox_key(G.seed[j]);
-    fs.pscale[j] = inv_sqrt_rank(G.r[j], identity ? COMPACT_PROJ_IDENTITY : COMPACT_PROJ_GAUSSIAN);
-    fs.pt_begin[j + 1] = fs.pt_begin[j] + static_cast<int>(ceil_div((ldb / 4) * G.r[j], 256));
+    fs.pscale[j] = proj_scale(proj, G.r[j]);
+    fs.pt_begin[j + 1] = fs.pt_begin[j] + pt_blocks(fs.kind, G.r[j], ldb);
     row += G.r[j];
   }
   const int64_t stage_blocks = fs.pt_begin[G.count] + ceil_div(n, 64) * fs.tiles_c;
@@ -349,7 +371,6 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     return fail(COMPACT_EWORKSPACE, "forward workspace %zu B < %zu B", ws_bytes, compact_fwd_workspace_bytes(n, m, r, dtype));
   if (tokens == 0) return ok();
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int identity = proj == COMPACT_PROJ_IDENTITY;
 
   if (dtype == COMPACT_F32) {
     GemmF32Params gp{};
@@ -359,19 +380,19 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
     gp.out = static_cast<float*>(y); gp.ldo = ldy; gp.scale = 1.0f;
     if ((st = launch_gemm_f32(gp, s, "forward y (fp32)"))) return st;
     gp.B = pgen_operand(seed, n, r, proj);
-    gp.N = r; gp.out = static_cast<float*>(z); gp.ldo = ldz; gp.scale = inv_sqrt_rank(r, proj);
+    gp.N = r; gp.out = static_cast<float*>(z); gp.ldo = ldz; gp.scale = proj_scale(proj, r);
     if ((st = launch_gemm_f32(gp, s, "forward z (fp32)"))) return st;
     return ok();
   }
 
   const PhiloxKey key = philox_key(seed);
-  const float pscale = inv_sqrt_rank(r, proj);
+  const float pscale = proj_scale(proj, r);
   const int64_t ldb = pt_ld(n);
   {
     FwdGroup G{};
     G.count = 1; G.m[0] = m; G.r[0] = r; G.seed[0] = seed; G.msum = m; G.rsum = r;
     bool taken = false;
-    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, identity, ws, s, taken))) return st;
+    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, proj, ws, s, taken))) return st;
     if (taken) return ok();
   }
 
@@ -382,15 +403,15 @@ int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y,
   p.z = static_cast<uint16_t*>(z); p.ldz = ldz;
   p.T = tokens; p.n = n; p.m = m; p.r = r;
   p.key = key;
-  p.identity = identity;
+  p.proj = proj_desc(proj, r);
   p.pscale = pscale;
   p.tiles_y = static_cast<int>(ceil_div(m, kBN));
   p.tiles_z = static_cast<int>(ceil_div(r, kBN));
   if (ws != nullptr) {
     uint16_t* pt = static_cast<uint16_t*>(align_ws(ws));
-    const int64_t quads = (ldb / 4) * r;
-    hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0, s,
-                       key, n, r, identity, pscale, pt, ldb);
+    const int64_t units = proj_t_units(proj_desc(proj, r).kind, r, ldb);
+    hipLaunchKernelGGL(k_pstream_t_bf16, dim3(static_cast<uint32_t>(ceil_div(units, 256))), dim3(256), 0, s,
+                       proj_desc(proj, r), key, n, pscale, pt, ldb);
     if ((st = check_launch("P panel (bf16)"))) return st;
     p.pt = pt;
     p.ldpt = ldb;
@@ -452,7 +473,7 @@ int compact_fwd_group(const void* x, int64_t ldx, const void* W, int64_t ldw, vo
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == COMPACT_BF16) {
     bool taken = false;
-    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, proj == COMPACT_PROJ_IDENTITY, ws, s,
+    if ((st = fwd_group_w4(x, ldx, W, ldw, y, ldy, z, ldz, tokens, n, G, proj, ws, s,
                            taken)))
       return st;
     if (taken) return ok();
@@ -622,7 +643,8 @@ AdamConsts adam_consts(int64_t t, double beta1, double beta2, double eps, int pr
   c.bc2 = static_cast<float>(1.0 - std::pow(beta2, static_cast<double>(t)));
   c.eps = static_cast<float>(eps);
   c.n_f32 = dtype == COMPACT_F32;
-  c.identity = proj == COMPACT_PROJ_IDENTITY;
+  c.kind = proj_desc(proj, 1).kind;
+  c.sparse_s = proj_desc(proj, 1).s;
   return c;
 }
 
@@ -642,7 +664,7 @@ void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t
   P.adam_blocks = adam_blocks(r, m);
   P.pt_blocks = 0;
   P.dec_tiles = 0;
-  const double coef64 = lr * alpha * (proj == COMPACT_PROJ_IDENTITY ? 1.0 : 1.0 / std::sqrt(static_cast<double>(r)));
+  const double coef64 = lr * alpha * proj_scale64(proj, r);
   DecW4Layer& d = P.dl;
   d = DecW4Layer{};
   d.coef = static_cast<float>(coef64);
@@ -651,7 +673,7 @@ void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t
       base + round_up(static_cast<int64_t>(size_t(r) * size_t(ldn) * elem_size(dtype)), kWsAlign));
   a.pt = pt;
   a.ldpt = static_cast<int>(ldpt);
-  P.pt_blocks = pt_blocks(r, ldpt);
+  P.pt_blocks = pt_blocks(proj_desc(proj, r).kind, r, ldpt);
   d.W = W; d.ldw = static_cast<int>(ldw);
   d.N = static_cast<const uint16_t*>(a.N); d.ldn = static_cast<int>(ldn);
   d.pt = pt; d.ldpt = static_cast<int>(ldpt);
@@ -774,6 +796,19 @@ int compact_pstream(uint64_t seed, int64_t n, int64_t r, float* out, int64_t ld,
                      static_cast<hipStream_t>(stream), philox_key(seed), n, r, out, ld);
   int st;
   if ((st = check_launch("P stream"))) return st;
+  return ok();
+}
+
+int compact_projection(uint64_t seed, int64_t n, int64_t r, int proj, float* out, int64_t ld, void* stream) {
+  int st;
+  if ((st = check_shape(0, n, 1, r, proj))) return st;
+  if (out == nullptr) return fail(COMPACT_EINVAL, "out is NULL");
+  if (ld < r) return fail(COMPACT_EINVAL, "ld < r");
+  const int64_t quads = ceil_div(n, 4) * r;
+  if (ceil_div(quads, 256) > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "n x r too large");
+  hipLaunchKernelGGL(k_projection_f32, dim3(static_cast<uint32_t>(ceil_div(quads, 256))), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), proj_desc(proj, r), philox_key(seed), n, out, ld);
+  if ((st = check_launch("projection stream"))) return st;
   return ok();
 }
 

@@ -157,10 +157,11 @@ struct MNMajorLoader {
 
 // ---------------------------------------------------------------------------
 // Projection tile generated on the fly (B operand of z = x P, K = i, N = j):
-// LDS row j holds scale * G[k0 .. k0+63][j] as bf16 (scale = 1/sqrt(r), so
-// the tile is P itself, rounded once).  One Philox call gives the four
-// consecutive rows i = 4p .. 4p+3 of column j, i.e. one 8-byte LDS store.
-// identity != 0 gives P = I instead (r == n).
+// LDS row j holds scale x stream elements (k0 .. k0+63, j) as bf16 (scale =
+// 1/sqrt(r) for the Gaussian, 1/sqrt(s) for the sparse projection, so the
+// tile is P itself, rounded once).  One Philox call gives the four
+// consecutive Gaussian rows i = 4p .. 4p+3 of column j, i.e. one 8-byte LDS
+// store.  The identity gives P = I (r == n).
 // ---------------------------------------------------------------------------
 template <int ROWS, int NT>
 struct PGenLoader {
@@ -169,7 +170,7 @@ struct PGenLoader {
   static_assert(kQuads % NT == 0, "tile does not split evenly over threads");
   PhiloxKey key;
   int64_t n, r, col0;  // K extent n, N extent r, first column of the tile
-  int identity;
+  ProjDesc proj;
   float scale;
   int64_t k_next;
 
@@ -183,14 +184,10 @@ struct PGenLoader {
       const int64_t j = col0 + row, i0 = k_next + kq * 4;
       float g[4] = {0.f, 0.f, 0.f, 0.f};
       if (j < r && i0 < n) {
-        if (identity) {
+        proj_quad(proj, key, i0, j, g);
+        const float sc = proj.kind == kProjIdentity ? 1.0f : scale;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
-        } else {
-          pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) g[e] = i0 + e >= n ? 0.0f : g[e] * scale;
-        }
+        for (int e = 0; e < 4; ++e) g[e] = i0 + e >= n ? 0.0f : g[e] * sc;
       }
       u32x2 v;
       v.x = pack_bf16x2(g[0], g[1]);

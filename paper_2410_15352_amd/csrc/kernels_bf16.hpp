@@ -31,8 +31,8 @@ struct FwdParams {
   int64_t ldpt;
   int64_t T, n, m, r;
   PhiloxKey key;
-  int identity;
-  float pscale;      // fp32(1/sqrt(r)) applied to G before rounding; 1 for the identity
+  ProjDesc proj;
+  float pscale;      // 1/sqrt(r) (Gaussian) or 1/sqrt(s) (sparse) applied before rounding; 1 for the identity
   int tiles_y;       // column tiles covering y (m columns)
   int tiles_z;       // column tiles covering z (r columns)
 };
@@ -59,22 +59,20 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
       KMajorLoader<BN, NT> lb{p.pt, p.ldpt, p.r, p.n, col0};
       gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
     } else {
-      PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.identity, p.pscale};
+      PGenLoader<BN, NT> lb{p.key, p.n, p.r, col0, p.proj, p.pscale};
       gemm_mainloop<BM, BN, WGM, WGN>(la, lb, 0, p.n, lds, acc);
     }
     store_tile_bf16_lds<BM, BN, WGM, WGN>(acc, lds, p.z, p.ldz, p.T, p.r, row0, col0, 1.0f);
   }
 }
 
-// P^T panel for the forward: out[j * ld + i] = bf16(scale * G[i][j]), or the
-// identity (scale 1).  One thread per quad (4 rows of one column); columns
-// i >= n of the padded rows are written as zero.
-__global__ void k_pstream_t_bf16(PhiloxKey key, int64_t n, int64_t r, int identity, float scale,
-                                 uint16_t* out, int64_t ld) {
-  const int64_t quads_per_row = ld / 4;
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (q >= quads_per_row * r) return;
-  pstream_t_quad(key, n, identity, scale, out, ld, q / quads_per_row, (q % quads_per_row) * 4);
+// P^T panel for the forward: out[j * ld + i] = bf16(scale x stream element
+// (i, j)), or the identity (scale 1).  One thread per quad (4 rows of one
+// column); columns i >= n of the padded rows are written as zero.
+__global__ void k_pstream_t_bf16(ProjDesc d, PhiloxKey key, int64_t n, float scale, uint16_t* out, int64_t ld) {
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (u >= proj_t_units(d.kind, d.r, ld)) return;
+  proj_t_unit(d, key, n, scale, out, ld, u);
 }
 
 // out[c * ldo + i] = in[i * ldi + c] for i < rows, c < cols (bf16), through a
@@ -137,7 +135,7 @@ struct FwdStage {
   uint16_t* b;            // staged operand, rows of ldb elements: W^T in rows 0 .. m-1
   int64_t ldb;
   int count;
-  int identity;
+  int kind, sparse_s;     // projection kind and draws per row (sparse)
   int tiles_c;            // ceil(m / 64)
   int pt_begin[kMaxGroup + 1];  // first P^T workgroup of each projection
   int64_t row_off[kMaxGroup];
@@ -151,12 +149,27 @@ __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
   if (b < a.pt_begin[a.count]) {
     int j = 0;
     while (j + 1 < a.count && a.pt_begin[j + 1] <= b) ++j;
-    const int64_t qpr = a.ldb / 4;
-    const int64_t q = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
-    if (q >= qpr * a.r[j]) return;
-    pstream_t_quad(a.key[j], a.n, a.identity, a.pscale[j], a.b + a.row_off[j] * a.ldb, a.ldb, q / qpr, (q % qpr) * 4);
+    const int64_t u = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
+    if (u >= proj_t_units(a.kind, a.r[j], a.ldb)) return;
+    proj_t_unit(ProjDesc{a.kind, static_cast<int>(a.r[j]), a.sparse_s}, a.key[j], a.n, a.pscale[j],
+                a.b + a.row_off[j] * a.ldb, a.ldb, u);
   } else {
     transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.b, a.ldb, a.tiles_c, b - a.pt_begin[a.count]);
+  }
+}
+
+// Unscaled fp32 stream of any projection (n x r, leading dimension ld), one
+// thread per quad of rows of one column: the exported test generator.
+__global__ void k_projection_f32(ProjDesc d, PhiloxKey key, int64_t n, float* out, int64_t ld) {
+  const int64_t nq = (n + 3) / 4;
+  const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (q >= nq * d.r) return;
+  const int64_t p = q % nq, j = q / nq;
+  float g[4];
+  proj_quad(d, key, 4 * p, j, g);
+  for (int e = 0; e < 4; ++e) {
+    const int64_t i = 4 * p + e;
+    if (i < n) out[i * ld + j] = g[e];
   }
 }
 

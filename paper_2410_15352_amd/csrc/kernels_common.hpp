@@ -15,7 +15,8 @@ namespace compact {
 //
 // One launch serves a group of layers (same t and hyper-parameters) and also
 // stages, for each layer that needs it, the P^T panel of the decompression:
-// pt[j * ldpt + i] = bf16(G(seed, i, j)) (unscaled; zero for i >= n).  The two
+// pt[j * ldpt + i] = bf16 of the unscaled stream element (i, j) (G, or S for
+// the sparse projection; zero for i >= n).  The two
 // jobs are independent; their workgroups alternate in the grid, so the
 // HBM-bound moment update and the VALU-bound P stream run side by side.
 
@@ -23,7 +24,8 @@ namespace compact {
 struct AdamConsts {
   float b1, b2, omb1, omb2, bc1, bc2, eps;
   int n_f32;
-  int identity;  // P is the identity (r == n)
+  int kind;      // projection kind (kProjGaussian, kProjIdentity, kProjSparse)
+  int sparse_s;  // draws per row of the sparse projection
 };
 
 struct AdamLayer {
@@ -111,18 +113,16 @@ __host__ __device__ inline int adam_blocks(int64_t r, int64_t m) {
   return static_cast<int>(b < 1 ? 1 : b);
 }
 
-// One quad of a P^T panel: out[j * ld + i0 .. i0 + 3] = bf16(scale G[i0 .. i0 + 3][j]),
-// or the identity (scale 1); rows i >= n are written as zero.
-__device__ __forceinline__ void pstream_t_quad(PhiloxKey key, int64_t n, int identity, float scale, uint16_t* out,
-                                               int64_t ld, int64_t j, int64_t i0) {
+// One quad of a P^T panel: out[j * ld + i0 .. i0 + 3] = bf16(scale x the
+// unscaled stream elements (i0 .. i0 + 3, j)) (scale 1 for the identity); rows
+// i >= n are written as zero.
+__device__ __forceinline__ void pstream_t_quad(const ProjDesc& d, PhiloxKey key, int64_t n, float scale,
+                                               uint16_t* out, int64_t ld, int64_t j, int64_t i0) {
   float g[4] = {0.f, 0.f, 0.f, 0.f};
   if (i0 < n) {
-    if (identity) {
-      for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
-    } else {
-      pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
+    proj_quad(d, key, i0, j, g);
+    if (d.kind != kProjIdentity)
       for (int e = 0; e < 4; ++e) g[e] = g[e] * scale;
-    }
     for (int e = 0; e < 4; ++e)
       if (i0 + e >= n) g[e] = 0.0f;
   }
@@ -132,8 +132,54 @@ __device__ __forceinline__ void pstream_t_quad(PhiloxKey key, int64_t n, int ide
   *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
 }
 
-// P^T workgroups of a layer: one quad per thread.
-__host__ __device__ inline int pt_blocks(int64_t r, int64_t ldpt) { return static_cast<int>(ceil_div(ldpt / 4 * r, 256)); }
+// Work units of a P^T panel [r][ld]: a quad (four rows i of one column j)
+// for the Gaussian and the identity; for the sparse projection one row i and
+// kSjltChunk consecutive columns, so that the row's s draws are made once per
+// unit rather than once per element.
+constexpr int kSjltChunk = 32;
+
+__host__ __device__ inline int64_t proj_t_units(int kind, int64_t r, int64_t ld) {
+  return kind == kProjSparse ? ld * ceil_div(r, kSjltChunk) : (ld / 4) * r;
+}
+
+// Unit u of a P^T panel: out[j * ld + i] = bf16(scale x stream element (i, j))
+// (scale 1 for the identity); rows i >= n are written as zero.
+__device__ __forceinline__ void proj_t_unit(const ProjDesc& d, PhiloxKey key, int64_t n, float scale, uint16_t* out,
+                                            int64_t ld, int64_t u) {
+  if (d.kind != kProjSparse) {
+    const int64_t qpr = ld / 4;
+    pstream_t_quad(d, key, n, scale, out, ld, u / qpr, (u % qpr) * 4);
+    return;
+  }
+  const int64_t i = u % ld, c0 = (u / ld) * kSjltChunk;
+  float acc[kSjltChunk];
+#pragma unroll
+  for (int k = 0; k < kSjltChunk; ++k) acc[k] = 0.0f;
+  if (i < n) {
+#pragma unroll 1
+    for (int q = 0; q < d.s; q += 2) {
+      uint32_t h0, h1;
+      float s0, s1;
+      sjlt_pair(key, static_cast<uint32_t>(i), static_cast<uint32_t>(q >> 1), static_cast<uint32_t>(d.r), h0, s0,
+                h1, s1);
+      if (q + 1 >= d.s) s1 = 0.0f;  // odd s: the pair's second draw is not taken
+#pragma unroll
+      for (int k = 0; k < kSjltChunk; ++k) {
+        const uint32_t c = static_cast<uint32_t>(c0 + k);
+        acc[k] += (h0 == c ? s0 : 0.0f);
+        acc[k] += (h1 == c ? s1 : 0.0f);
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kSjltChunk; ++k)
+    if (c0 + k < d.r) out[(c0 + k) * ld + i] = f32_to_bf16(acc[k] * scale);
+}
+
+// P^T workgroups of a layer: one unit per thread.
+__host__ __device__ inline int pt_blocks(int kind, int64_t r, int64_t ldpt) {
+  return static_cast<int>(ceil_div(proj_t_units(kind, r, ldpt), 256));
+}
 
 __global__ void k_adam_pt_batched(StepBatch s) {
   const int na = s.adam_begin[s.count], np = s.pt_begin[s.count];
@@ -156,32 +202,28 @@ __global__ void k_adam_pt_batched(StepBatch s) {
   } else {
     const int l = batch_layer_of(s.pt_begin, s.count, idx);
     const AdamLayer& p = s.layer[l];
-    const int64_t q = static_cast<int64_t>(idx - s.pt_begin[l]) * blockDim.x + threadIdx.x;
-    const int64_t qpr = p.ldpt / 4;
-    if (q >= qpr * p.r) return;
-    pstream_t_quad(p.key, p.n, s.c.identity, 1.0f, p.pt, p.ldpt, q / qpr, (q % qpr) * 4);
+    const int64_t u = static_cast<int64_t>(idx - s.pt_begin[l]) * blockDim.x + threadIdx.x;
+    if (u >= proj_t_units(s.c.kind, p.r, p.ldpt)) return;
+    proj_t_unit(ProjDesc{s.c.kind, p.r, s.c.sparse_s}, p.key, p.n, 1.0f, p.pt, p.ldpt, u);
   }
 }
 
 // ------------------------------- fp32 GEMM ---------------------------------
 // Operand element (u, v) = p[u * su + v * sv] for u < U, v < V (else 0), or,
-// with pgen set, the projection stream G(u, v) (u = row i < n, v = column j < r)
-// or the identity.
+// with pgen set, the unscaled projection stream element (u = row i < n,
+// v = column j < r): G, the identity or S.
 struct OperandF32 {
   const float* p;
   int64_t su, sv;
   int64_t U, V;
   int pgen;
-  int identity;
+  ProjDesc proj;
   PhiloxKey key;
 };
 
 __device__ __forceinline__ float operand_elem(const OperandF32& o, int64_t u, int64_t v) {
   if (u >= o.U || v >= o.V) return 0.0f;
-  if (o.pgen) {
-    if (o.identity) return u == v ? 1.0f : 0.0f;
-    return pstream_element(o.key, static_cast<uint32_t>(u), static_cast<uint32_t>(v));
-  }
+  if (o.pgen) return proj_element(o.proj, o.key, u, v);
   return o.p[u * o.su + v * o.sv];
 }
 

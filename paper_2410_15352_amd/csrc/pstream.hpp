@@ -34,13 +34,13 @@ __host__ __device__ inline PhiloxKey philox_key(uint64_t seed) {
   return PhiloxKey{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32)};
 }
 
-// Philox4x32-10 with counter (c0, c1, 0, 0).
+// Philox4x32-10 with counter (c0, c1, c2, 0).
 __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, PhiloxKey key,
                                               uint32_t& o0, uint32_t& o1, uint32_t& o2,
-                                              uint32_t& o3) {
+                                              uint32_t& o3, uint32_t c2 = 0u) {
   constexpr uint32_t kM0 = 0xD2511F53u, kM1 = 0xCD9E8D57u;
   constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
-  uint32_t x0 = c0, x1 = c1, x2 = 0u, x3 = 0u;
+  uint32_t x0 = c0, x1 = c1, x2 = c2, x3 = 0u;
   uint32_t k0 = key.k0, k1 = key.k1;
 #pragma unroll
   for (int round = 0; round < 10; ++round) {
@@ -184,6 +184,80 @@ __device__ __forceinline__ float pstream_element(PhiloxKey key, uint32_t i, uint
   float g[4];
   pstream_quad(key, i >> 2, j, g);
   return g[i & 3];
+}
+
+// ---------------------------------------------------------------------------
+// Sparse Johnson-Lindenstrauss projection (the sparse JL transform of
+// Dasgupta, Kumar and Sarlos, 2010, named by the paper as an alternative to the
+// Gaussian, §4 ablations and §6).  Row i of P (n x r) receives s signed unit
+// draws; draws that land on the same column add up; P = S / sqrt(s):
+//   draw q of row i, q = 0 .. s-1:
+//     (w0, w1, w2, w3) = Philox4x32-10((i, q >> 1, kSjltTag, 0), key(seed))
+//     (a, b) = (w0, w1) for even q, (w2, w3) for odd q
+//     column h = floor(a r / 2^32),  sign = +1 if b < 2^31 else -1
+//   S[i][c] = sum of the signs of the draws of row i with h = c.
+// E[P P^T] = I, as for the Gaussian: the diagonal is 1 in expectation and the
+// off-diagonal terms vanish with the independent signs.  S is small integers,
+// exact in bf16 and fp32.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kSjltTag = 0x4A4C5350u;  // counter word 2 of the sparse stream
+constexpr int kSjltMaxS = 64;
+
+// Projection kinds of the device generators (the ABI's compact_proj codes).
+enum : int { kProjGaussian = 0, kProjIdentity = 1, kProjSparse = 2 };
+
+// Draws 2p and 2p + 1 of row i: columns h0, h1 and signs (+1 / -1).
+__device__ __forceinline__ void sjlt_pair(PhiloxKey key, uint32_t i, uint32_t p, uint32_t r, uint32_t& h0,
+                                          float& s0, uint32_t& h1, float& s1) {
+  uint32_t w0, w1, w2, w3;
+  philox4x32_10(i, p, key, w0, w1, w2, w3, kSjltTag);
+  h0 = __umulhi(w0, r);
+  s0 = (w1 >> 31) ? -1.0f : 1.0f;
+  h1 = __umulhi(w2, r);
+  s1 = (w3 >> 31) ? -1.0f : 1.0f;
+}
+
+// S[i][j] (unscaled) for s draws per row.
+__device__ __forceinline__ float sjlt_element(PhiloxKey key, uint32_t i, uint32_t j, uint32_t r, int s) {
+  float v = 0.0f;
+  for (int q = 0; q < s; q += 2) {
+    uint32_t h0, h1;
+    float s0, s1;
+    sjlt_pair(key, i, static_cast<uint32_t>(q >> 1), r, h0, s0, h1, s1);
+    if (h0 == j) v += s0;
+    if (q + 1 < s && h1 == j) v += s1;
+  }
+  return v;
+}
+
+// The projection a generator draws from: its kind, the rank r (the column
+// range of the sparse hash) and the draws per row s (sparse only).
+struct ProjDesc {
+  int kind;
+  int r;
+  int s;
+};
+
+// Unscaled stream elements of rows i0 .. i0 + 3 (i0 % 4 == 0) of column j:
+// G for the Gaussian, I for the identity, S for the sparse projection.
+__device__ __forceinline__ void proj_quad(const ProjDesc& d, PhiloxKey key, int64_t i0, int64_t j, float g[4]) {
+  if (d.kind == kProjIdentity) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) g[e] = (i0 + e == j) ? 1.0f : 0.0f;
+  } else if (d.kind == kProjSparse) {
+#pragma unroll 1
+    for (int e = 0; e < 4; ++e)
+      g[e] = sjlt_element(key, static_cast<uint32_t>(i0 + e), static_cast<uint32_t>(j), static_cast<uint32_t>(d.r), d.s);
+  } else {
+    pstream_quad(key, static_cast<uint32_t>(i0 >> 2), static_cast<uint32_t>(j), g);
+  }
+}
+
+__device__ __forceinline__ float proj_element(const ProjDesc& d, PhiloxKey key, int64_t i, int64_t j) {
+  if (d.kind == kProjIdentity) return i == j ? 1.0f : 0.0f;
+  if (d.kind == kProjSparse)
+    return sjlt_element(key, static_cast<uint32_t>(i), static_cast<uint32_t>(j), static_cast<uint32_t>(d.r), d.s);
+  return pstream_element(key, static_cast<uint32_t>(i), static_cast<uint32_t>(j));
 }
 
 }  // namespace compact

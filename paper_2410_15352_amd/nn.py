@@ -74,10 +74,10 @@ class _GroupFn(torch.autograd.Function):
         z = _empty2d(T, mod.rsum, torch.bfloat16, x2.device)
         if len(mod.ms) == 1:
             ws = WorkspacePool.get(x2.device, "fwd", fwd_workspace_bytes(mod.n, mod.ms[0], mod.rs[0]))
-            compact_fwd(x2, mod.weight, y, z, mod.seeds[0], ws=ws)
+            compact_fwd(x2, mod.weight, y, z, mod.seeds[0], proj=mod.proj, ws=ws)
         else:
             ws = WorkspacePool.get(x2.device, "fwd", fwd_group_workspace_bytes(mod.n, mod.ms, mod.rs))
-            compact_fwd_group(x2, mod.weight, y, z, mod.ms, mod.rs, mod.seeds, ws=ws)
+            compact_fwd_group(x2, mod.weight, y, z, mod.ms, mod.rs, mod.seeds, proj=mod.proj, ws=ws)
         ctx.mod = mod
         ctx.save_for_backward(z)  # T x sum(r): the activation CompAct keeps instead of x
         return y
@@ -109,10 +109,12 @@ class _GroupFn(torch.autograd.Function):
 class CompActGroup(torch.nn.Module):
     """Projections j = 0 .. k-1 of one input x: y = [x W_0 | x W_1 | ...]
     (n -> sum(ms)), each with its own rank rs[j] and seed.  Every width and rank
-    but the last must be a multiple of 8 (the ABI's column slices)."""
+    but the last must be a multiple of 8 (the ABI's column slices).  proj:
+    "gaussian" (§3.3) or "sparse-jl[:s]" (the sparse JL projection of §5)."""
 
-    def __init__(self, n, ms, rs, seeds=None, alpha=1.0, device="cuda", weight=None):
+    def __init__(self, n, ms, rs, seeds=None, alpha=1.0, device="cuda", weight=None, proj="gaussian"):
         super().__init__()
+        self.proj = proj
         self.n, self.ms, self.rs = int(n), [int(m) for m in ms], [int(r) for r in rs]
         self.msum, self.rsum = sum(self.ms), sum(self.rs)
         self.alpha = float(alpha)
@@ -144,8 +146,8 @@ class CompActGroup(torch.nn.Module):
 class CompActLinear(CompActGroup):
     """One CompAct projection n -> m of rank r (Alg. 1-3)."""
 
-    def __init__(self, n, m, r, seed=None, alpha=1.0, device="cuda", weight=None):
-        super().__init__(n, [m], [r], None if seed is None else [seed], alpha, device, weight)
+    def __init__(self, n, m, r, seed=None, alpha=1.0, device="cuda", weight=None, proj="gaussian"):
+        super().__init__(n, [m], [r], None if seed is None else [seed], alpha, device, weight, proj)
 
 
 class CompActAdam:
@@ -158,6 +160,10 @@ class CompActAdam:
     def __init__(self, modules, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, reseed_period=200,
                  reset_on_reseed=False):
         self.modules = list(modules)
+        projs = {mod.proj for mod in self.modules}
+        if len(projs) != 1:
+            raise ValueError("CompActAdam steps modules of one projection kind")
+        self.proj = projs.pop()
         self.lr, self.betas, self.eps = float(lr), betas, float(eps)
         self.reseed_period = int(reseed_period)
         self.reset_on_reseed = bool(reset_on_reseed)
@@ -182,7 +188,8 @@ class CompActAdam:
             raise RuntimeError("step() before every module's backward")
         self.t += 1
         self._batch.set_seeds([mod.seeds[j] for mod, j in self._layers])
-        compact_step_batched(self._batch, self.t, self.lr, self.betas[0], self.betas[1], self.eps, ws=self._ws)
+        compact_step_batched(self._batch, self.t, self.lr, self.betas[0], self.betas[1], self.eps, proj=self.proj,
+                             ws=self._ws)
         for mod in self.modules:
             for j in range(len(mod.seeds)):
                 new = compact_next_seed(mod.seeds[j], self.t, self.reseed_period)

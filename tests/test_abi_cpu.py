@@ -91,6 +91,10 @@ FAKE = 0x100000  # an aligned non-NULL address; never dereferenced (validation f
     (dict(r=0), -1), (dict(r=2000), -1), (dict(n=0), -1), (dict(tokens=-1), -1),
     (dict(proj=1), -1),             # identity needs r == n
     (dict(proj=7), -1), (dict(dtype=5), -1),
+    (dict(proj=2 | (65 << 8)), -1),  # sparse JL: at most 64 draws per row
+    (dict(proj=4 << 8), -1),         # draws given to the Gaussian
+    (dict(proj=-1), -1),
+    (dict(proj=2 | (64 << 8), ws=FAKE, ws_bytes=16), -4),  # a valid sparse code reaches the workspace check
     (dict(ldx=1000), -1),           # ld < n
     (dict(ldx=1028), -2),           # bf16 ld not a multiple of 8
     (dict(x=FAKE + 2), -2),         # misaligned pointer
@@ -180,6 +184,16 @@ def test_step_validation(lib, kw, status):
                           a["seed"], a["t"], a["lr"], a["beta1"], a["beta2"], a["eps"], a["alpha"],
                           a["proj"], a["dtype"], a["w_dtype"], a["ws"], a["ws_bytes"], a["stream"])
     assert st == status
+
+
+def test_projection_validation(lib):
+    sparse = lambda s_: 2 | (s_ << 8)
+    assert lib.compact_projection(1, 4, 4, sparse(65), FAKE, 4, None) == -1
+    assert lib.compact_projection(1, 4, 4, sparse(8), None, 4, None) == -1
+    assert lib.compact_projection(1, 4, 4, sparse(8), FAKE, 2, None) == -1
+    assert lib.compact_projection(1, 4, 5, sparse(8), FAKE, 8, None) == -1      # r > n
+    assert lib.compact_projection(1, 4, 3, 1, FAKE, 4, None) == -1              # identity needs r == n
+    assert lib.compact_last_error()
 
 
 def test_pstream_validation(lib):

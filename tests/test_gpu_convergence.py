@@ -87,3 +87,18 @@ def test_compact_converges_like_adam():
     assert half[-1] < 0.05 * half[0]
     assert kept[-1] < 0.67 * kept[0] and reset[-1] < 0.67 * reset[0]
     assert full[-1] <= half[-1] <= kept[-1]
+
+
+def test_sparse_jl_converges_like_gaussian():
+    # §5: the sparse JL projection performs comparably to the Gaussian
+    X, Y = _problem()
+    gauss = _train(X, Y, N_IN // 8)
+    sparse = _train(X, Y, N_IN // 8, proj="sparse-jl")
+    sparse1 = _train(X, Y, N_IN // 8, proj="sparse-jl:1")
+    print(f"\nloss at step 300, r = n/8: gaussian {gauss[-1]:.3e}, sparse JL s=8 {sparse[-1]:.3e}, "
+          f"s=1 {sparse1[-1]:.3e} (from {gauss[0]:.3e})")
+    for L in (sparse, sparse1):
+        assert np.all(np.isfinite(L))
+        assert L[299] < L[199] < L[99] < L[0]
+        assert 0.5 * gauss[-1] < L[-1] < 2.0 * gauss[-1]
+

@@ -10,7 +10,7 @@
   re-sample).
 * The LLaMA block of the pretraining setup (paper_2410_15352_amd.block: bf16,
   flash attention, q|k|v and gate|up as CompAct input groups, down CompAct, o
-  uncompressed; App. D): its output, dL/dx, every CompAct layer's G^ and the
+  uncompressed; App. B.2): its output, dL/dx, every CompAct layer's G^ and the
   o weight's gradient against a float64 CPU reference of the same block with
   the oracle's P (G^ = P^T x^T dL/do, §3.2).
 * The activations autograd keeps for one block are exactly App. E's Table 7
@@ -276,11 +276,11 @@ def test_llama_block_saved_activations_table7():
         assert abs(d_grown - d_saved) <= 4 * 2**20, name
 
 
-def _train_small(rank, steps, lr):
+def _train_small(rank, steps, lr, proj="gaussian"):
     vocab, d, heads, ffn, layers = 512, 256, 4, 688, 2
     B, S = 8, 64
     torch.manual_seed(0)
-    model = blk_mod.LlamaModel(vocab, d, heads, ffn, layers, rank=rank)
+    model = blk_mod.LlamaModel(vocab, d, heads, ffn, layers, rank=rank, proj=proj)
     opts = blk_mod.make_optimizers(model, lr=lr, reseed_period=10)
     g = torch.Generator(device="cpu").manual_seed(5)
     tokens = torch.randint(0, vocab, (B, S + 1), generator=g).to(dev())
@@ -300,8 +300,11 @@ def test_small_llama_model_trains():
     steps, vocab = 100, 512
     model, opts, L = _train_small(64, steps, 5e-3)
     _, _, L_dense = _train_small(None, steps, 5e-3)
+    _, _, L_sparse = _train_small(64, steps, 5e-3, proj="sparse-jl")
     print("\nloss at steps 1, 25, 50, 100: CompAct r=64", [round(float(L[i]), 3) for i in (0, 24, 49, 99)],
+          " sparse JL", [round(float(L_sparse[i]), 3) for i in (0, 24, 49, 99)],
           " dense", [round(float(L_dense[i]), 3) for i in (0, 24, 49, 99)])
+    assert np.all(np.isfinite(L_sparse)) and L_sparse[-1] < 0.5 * L_sparse[0]
     assert len(opts) == 2 and len(model.compact_modules()) == 3 * len(model.blocks)
     assert np.all(np.isfinite(L))
     assert abs(L[0] - np.log(vocab)) < 0.5           # near uniform at initialisation

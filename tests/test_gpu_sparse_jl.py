@@ -1,0 +1,164 @@
+"""GPU parity of the sparse Johnson-Lindenstrauss projection (the ablation's
+sparse JL matrices, §5) against the fp64 oracle.
+
+* The stream: compact_projection's integer matrix S equals the oracle's,
+  entry for entry, for several (n, r, s) with ragged n, r = 1, odd s and
+  s = 64; the Gaussian kind equals compact_pstream.
+* Forward (Alg. 1) with P = S / sqrt(s): y and z against the oracle on the
+  bf16 path (with and without the workspace) and the fp32 path; y is bitwise
+  the Gaussian call's y (the projection only touches z); an input group is
+  bitwise its per-projection calls.
+* Alg. 3 with the sparse P: M, V and the update against the oracle, fp32 and
+  bf16 weights; the batched step is bitwise the per-layer step.
+"""
+import numpy as np
+import pytest
+
+from oracle import compact as oc
+from oracle.pstream import sparse_jl_raw
+from synthetic import bf16_round, fwd_inputs, step_inputs
+
+from gpu_util import dev, empty, ld_for, to_dev, to_np, to_np_f32, workspace
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+cp = pytest.importorskip("paper_2410_15352_amd")
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+CODE = {"f32": 0, "bf16": 1}
+
+
+@pytest.mark.parametrize("n,r,s,seed", [(7, 5, 3, 1), (1024, 128, 8, (9 << 32) | 77), (2736, 342, 8, 5 << 32),
+                                        (13, 1, 4, 2**64 - 1), (100, 37, 64, 123), (5461, 682, 1, 7 << 40),
+                                        (333, 64, 2, 42)])
+def test_projection_stream_bitwise(n, r, s, seed):
+    out = torch.full((n, r), 9.0, dtype=torch.float32, device=dev())
+    cp.compact_projection(seed, out, proj=f"sparse-jl:{s}")
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().astype(np.float64), sparse_jl_raw(seed, n, r, s))
+
+
+def test_projection_default_draws_and_gaussian_kind():
+    n, r, seed = 300, 48, (3 << 32) | 1
+    out = torch.empty(n, r, dtype=torch.float32, device=dev())
+    cp.compact_projection(seed, out, proj="sparse-jl")
+    g1 = torch.empty(n, r, dtype=torch.float32, device=dev())
+    g2 = torch.empty(n, r, dtype=torch.float32, device=dev())
+    cp.compact_projection(seed, g1, proj="gaussian")
+    cp.compact_pstream(seed, g2)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().astype(np.float64), sparse_jl_raw(seed, n, r, 8))
+    assert torch.equal(g1, g2)
+
+
+SHAPES = [
+    (256, 256, 512, 32, "f32"),
+    (100, 36, 20, 12, "f32"),
+    (300, 200, 136, 40, "bf16"),
+    (1000, 1376, 512, 344, "bf16"),
+    (513, 512, 1376, 128, "bf16"),
+    (777, 1024, 2736, 128, "bf16"),
+    (150, 200, 203, 24, "bf16"),
+]
+
+
+def _ids(s):
+    return "T{}-n{}-m{}-r{}-{}".format(*s)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("use_ws", [True, False])
+@pytest.mark.parametrize("s", [8, 3])
+def test_forward_parity(shape, use_ws, s):
+    T, n, m, r, dt = shape
+    if dt == "f32" and use_ws:
+        pytest.skip("no workspace mode on the fp32 path")
+    seed = (13 << 32) | 5
+    x, W = fwd_inputs(T, n, m, dt, data_seed=T + n + 1)
+    xd, Wd = to_dev(x, dt, ld_for(n, dt)), to_dev(W, dt, ld_for(m, dt))
+    y, z = empty(T, m, dt, ld_for(m, dt)), empty(T, r, dt, ld_for(r, dt))
+    yg, zg = empty(T, m, dt, ld_for(m, dt)), empty(T, r, dt, ld_for(r, dt))
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, CODE[dt])) if use_ws else None
+    cp.compact_fwd(xd, Wd, y, z, seed, proj=f"sparse-jl:{s}", ws=ws)
+    cp.compact_fwd(xd, Wd, yg, zg, seed, proj="gaussian", ws=ws)
+    torch.cuda.synchronize()
+    y_ref, z_ref = oc.ref_fwd(x, W, seed, r, sparse_s=s)
+    assert oc.rel_fro(to_np(y), y_ref) <= TOL[dt]
+    assert oc.rel_fro(to_np(z), z_ref) <= TOL[dt]
+    assert torch.equal(y.contiguous().view(torch.int32 if dt == "f32" else torch.int16),
+                       yg.contiguous().view(torch.int32 if dt == "f32" else torch.int16))
+
+
+def test_group_forward_equals_per_projection():
+    T, n, ms, rs = 513, 512, (512, 512, 512), (64, 64, 64)
+    seeds = [((j + 3) << 32) | 11 for j in range(3)]
+    x, _ = fwd_inputs(T, n, 8, "bf16", data_seed=71)
+    W = np.concatenate([fwd_inputs(8, n, m, "bf16", data_seed=72 + j)[1] for j, m in enumerate(ms)], axis=1)
+    M, R = sum(ms), sum(rs)
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(M, "bf16"))
+    y, z = empty(T, M, "bf16"), empty(T, R, "bf16")
+    y1, z1 = empty(T, M, "bf16"), empty(T, R, "bf16")
+    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, proj="sparse-jl",
+                         ws=workspace(cp.fwd_group_workspace_bytes(n, ms, rs)))
+    mo = ro = 0
+    for j, (m, r) in enumerate(zip(ms, rs)):
+        cp.compact_fwd(xd, Wd[:, mo:mo + m], y1[:, mo:mo + m], z1[:, ro:ro + r], seeds[j], proj="sparse-jl",
+                       ws=workspace(cp.fwd_workspace_bytes(n, m, r)))
+        mo += m
+        ro += r
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y1.view(torch.int16))
+    assert torch.equal(z.view(torch.int16), z1.view(torch.int16))
+    ro = 0
+    for j, r in enumerate(rs):
+        _, z_ref = oc.ref_fwd(x, W[:, :1], seeds[j], r, sparse_s=8)
+        assert oc.rel_fro(to_np(z)[:, ro:ro + r], z_ref) <= TOL["bf16"]
+        ro += r
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
+@pytest.mark.parametrize("t", [1, 3])
+def test_step_parity(shape, t):
+    _, n, m, r, dt = shape
+    s = 8
+    seed, lr, b1, b2, eps, alpha = (6 << 32) | 2, 1e-3, 0.9, 0.999, 1e-8, 0.25
+    W, G, M, V = step_inputs(n, m, r, dt, t=t, data_seed=n + r + 7)
+    Wd = to_dev(W, "f32", ld_for(m, "f32"))
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+    ws = workspace(cp.step_workspace_bytes(n, m, r, CODE[dt]))
+    cp.compact_step(Wd, Gd, Md, Vd, seed, t, lr, b1, b2, eps, alpha, proj="sparse-jl", dtype=dt, ws=ws)
+    torch.cuda.synchronize()
+    W_ref, M_ref, V_ref, dW_ref = oc.ref_step(W, G, M, V, seed, r, t, lr, b1, b2, eps, alpha, sparse_s=s)
+    dW = to_np_f32(Wd).astype(np.float64) - W.astype(np.float64)
+    assert oc.rel_fro(Md.cpu().numpy(), M_ref) <= TOL[dt]
+    assert oc.rel_fro(Vd.cpu().numpy(), V_ref) <= TOL[dt]
+    assert oc.rel_fro(dW, dW_ref) <= (TOL[dt] if dt == "bf16" else 2e-4)
+    if dt == "bf16":
+        Wb = to_dev(W, "bf16", ld_for(m, "bf16"))
+        Gd2, Md2, Vd2 = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+        cp.compact_step(Wb, Gd2, Md2, Vd2, seed, t, lr, b1, b2, eps, alpha, proj="sparse-jl", dtype="bf16", ws=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_np_f32(Wb).view(np.uint32), bf16_round(to_np_f32(Wd)).view(np.uint32))
+
+
+def test_step_batched_equals_per_layer():
+    shapes = [(512, 512, 128), (512, 1376, 128), (1376, 512, 344), (300, 200, 40)] * 3
+    layers_a, layers_b = [], []
+    for i, (n, m, r) in enumerate(shapes):
+        W, G, M, V = step_inputs(n, m, r, "bf16", t=2, data_seed=80 + i)
+        for lst in (layers_a, layers_b):
+            g, mm, v = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+            lst.append(dict(W=to_dev(W, "bf16", ld_for(m, "bf16")), G=g, M=mm, V=v, seed=((i + 1) << 32) | 9,
+                            alpha=0.25))
+    cp.compact_step_batched(layers_a, 2, 1e-3, proj="sparse-jl:4",
+                            ws=workspace(cp.step_batched_workspace_bytes(layers_a)))
+    for L in layers_b:
+        n, m = L["W"].shape
+        r = L["G"].shape[0]
+        cp.compact_step(L["W"], L["G"], L["M"], L["V"], L["seed"], 2, 1e-3, alpha=L["alpha"], proj="sparse-jl:4",
+                        ws=workspace(cp.step_workspace_bytes(n, m, r)))
+    torch.cuda.synchronize()
+    for La, Lb in zip(layers_a, layers_b):
+        assert torch.equal(La["M"], Lb["M"]) and torch.equal(La["V"], Lb["V"])
+        assert torch.equal(La["W"].view(torch.int16), Lb["W"].view(torch.int16))
