@@ -88,6 +88,7 @@ struct W4Gemm {
   W4Seg seg[2];       // seg[1].tiles == 0 when unused
   int tiles_n;        // seg[0].tiles + seg[1].tiles
   int tiles;          // ceil(M / 256) * tiles_n
+  int band_rows;      // rows of tiles per band of the walk order (>= 1)
 };
 
 typedef __attribute__((address_space(3))) void w4_lds_void;
@@ -213,19 +214,53 @@ __device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
 }
 
 // ------------------------------ tile cursor --------------------------------
-// This workgroup's tiles are p, p + G, p + 2 G, ... (G = grid size); tile
-// index x is row tile x / tiles_n, column tile x % tiles_n.
+// Walk order.  Tiles are listed band by band (band_rows rows of tiles each),
+// column by column inside a band, row by row inside a column.  The workgroups
+// of one XCD (consecutive logical ids, see xcd_remap) take one contiguous
+// stretch of that list, dealt round-robin: in every round the workgroups of an
+// XCD work on a block of about band_rows x (workgroups / band_rows) tiles,
+// whose operand row and column blocks they share through that XCD's L2.
+// A workgroup's q-th tile is list entry off + q * gx + w (gx: workgroups on
+// its XCD, w: its place among them, off: tiles of the XCDs before it).
+struct W4Walk {
+  int gx, w, off;
+};
+
+__device__ __forceinline__ W4Walk w4_walk(const W4Gemm& g, int p, int G) {
+  // xcd_remap gives XCD x the logical ids start .. start + gx - 1
+  const int q = G / kNumXcd, rem = G % kNumXcd;
+  const int x = p < (q + 1) * rem ? p / (q + 1) : rem + (p - (q + 1) * rem) / (q > 0 ? q : 1);
+  const int start = x * q + (x < rem ? x : rem);
+  const int full = g.tiles / G, rem_t = g.tiles % G;
+  W4Walk k;
+  k.gx = q + (x < rem ? 1 : 0);
+  k.w = p - start;
+  k.off = start * full + (rem_t < start ? rem_t : start);
+  return k;
+}
+
 struct W4Cursor {
   int q, rt, ct;
 };
 
-__device__ __forceinline__ void w4_next_tile(W4Cursor& c, int dct, int drt, int tiles_n) {
+// Row and column tile of the workgroup's q-th tile (clamped to the last tile
+// past the end of its list; such positions are never live).
+__device__ __forceinline__ void w4_tile_at(const W4Gemm& g, const W4Walk& k, W4Cursor& c) {
+  int i = k.off + c.q * k.gx + k.w;
+  i = i < g.tiles ? i : g.tiles - 1;
+  const int rows_total = g.tiles / g.tiles_n;
+  const int per_band = g.band_rows * g.tiles_n;
+  const int b = i / per_band;
+  const int r0 = b * g.band_rows;
+  const int rows_b = rows_total - r0 < g.band_rows ? rows_total - r0 : g.band_rows;
+  const int within = i - b * per_band;
+  c.ct = within / rows_b;
+  c.rt = r0 + within - c.ct * rows_b;
+}
+
+__device__ __forceinline__ void w4_next_tile(const W4Gemm& g, const W4Walk& k, W4Cursor& c) {
   c.q += 1;
-  c.ct += dct;
-  c.rt += drt;
-  const bool carry = c.ct >= tiles_n;
-  c.ct = carry ? c.ct - tiles_n : c.ct;
-  c.rt = carry ? c.rt + 1 : c.rt;
+  w4_tile_at(g, k, c);
 }
 
 struct W4CopyDesc {
@@ -272,12 +307,12 @@ struct W4CopyCursor {
   W4CopyDesc d;
 };
 
-__device__ __forceinline__ void w4_copy_advance(const W4Gemm& g, W4CopyCursor& cc, int kt, int n_my, int dct,
-                                                int drt) {
+__device__ __forceinline__ void w4_copy_advance(const W4Gemm& g, W4CopyCursor& cc, int kt, int n_my,
+                                                const W4Walk& wk) {
   cc.k += 1;
   if (cc.k == kt) {
     cc.k = 0;
-    w4_next_tile(cc.c, dct, drt, g.tiles_n);
+    w4_next_tile(g, wk, cc.c);
     cc.d = w4_copy_desc(g, cc.c, n_my);
   }
 }
@@ -386,7 +421,7 @@ __device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&o
 
 template <int T>
 __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc, int kt,
-                                         int n_my, int dct, int drt, const W4Out& od,
+                                         int n_my, const W4Walk& wk, const W4Out& od,
                                          const uint32_t (&out)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4]) {
   const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
   const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
@@ -428,7 +463,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
     }
   }
   w4_pin(f[0]);
-  w4_copy_advance(g, cc, kt, n_my, dct, drt);
+  w4_copy_advance(g, cc, kt, n_my, wk);
 }
 
 // The whole persistent GEMM for this workgroup.  Launch with kW4Threads
@@ -439,45 +474,47 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   if (p >= g.tiles) return;
   const int n_my = (g.tiles - p + G - 1) / G;
   const int kt = static_cast<int>(ceil_div(g.K, kW4K));
-  const int dct = G % g.tiles_n, drt = G / g.tiles_n;
+  const W4Walk wk = w4_walk(g, p, G);
   const W4Lane L = w4_lane(g);
 
   W4CopyCursor cc;
-  cc.c = W4Cursor{0, p / g.tiles_n, p % g.tiles_n};
+  cc.c = W4Cursor{0, 0, 0};
+  w4_tile_at(g, wk, cc.c);
   cc.k = 0;
   cc.d = w4_copy_desc(g, cc.c, n_my);
 #pragma unroll
   for (int s = 0; s < 3; ++s) {
     w4_copy(g, L, cc.d, cc.k * kW4K, L.lds + s * kW4StageBytes, L.lds + kW4BBase + s * kW4StageBytes);
-    w4_copy_advance(g, cc, kt, n_my, dct, drt);
+    w4_copy_advance(g, cc, kt, n_my, wk);
   }
   W4Frags f[2];
   f32x16 acc[4][4];
   uint32_t out[128];
 #pragma unroll
   for (int e = 0; e < 128; ++e) out[e] = 0u;
-  W4Cursor oc{0, p / g.tiles_n, p % g.tiles_n};
+  W4Cursor oc{0, 0, 0};
+  w4_tile_at(g, wk, oc);
   W4Out od = w4_out_desc(g, L, oc, false);  // nothing to store before the first tile
   w4_wait_vm<0>();
   w4_lds_barrier(f[1]);
   w4_read(L.a0, L.b0, f[0]);
   int h = 0;
   for (int q = 0; q < n_my; ++q) {
-    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, dct, drt, od, out, f, acc);
-    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, dct, drt, od, out, f, acc);
-    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, dct, drt, od, out, f, acc);
+    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, wk, od, out, f, acc);
+    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, wk, od, out, f, acc);
     h += kt;
     od = w4_out_desc(g, L, oc, true);
     w4_pack(acc, L.lane, out);
-    w4_next_tile(oc, dct, drt, g.tiles_n);
+    w4_next_tile(g, wk, oc);
   }
   w4_store<0, 16>(od, out);
   w4_wait_vm<0>();  // no copy may still be writing LDS when the workgroup ends
