@@ -6,10 +6,10 @@ synthetic model-shaped workload, on one MI355X.
 
 One step = the forward of every linear layer, its backward (reverse order) and
 the Adam step of every layer, on synthetic inputs resident in HBM.  Layers that
-read the same input (q, k, v; gate, up) run as one group: compact_fwd_group,
-one compact_bwd for dL/dx over the concatenated weight (the sum a shared input
-needs) and a compact_bwd per layer for its G^.  --no-group runs every layer on
-its own (compact_fwd / compact_bwd per layer, dL/dx not summed).
+read the same input (q, k, v; gate, up) run as one group: compact_fwd_group and
+compact_bwd_group (dL/dx over the concatenated weight, the sum a shared input
+needs, and every G^ of the group in one split-K launch).  --no-group runs every
+layer on its own (compact_fwd / compact_bwd per layer, dL/dx not summed).
 Prints ONE JSON line: tokens/s, the MFMA roofline fraction of the dominant
 kernel (the fused forward GEMM), per-phase timings, activation bytes saved and
 the CPU oracle's throughput on the host cores.
@@ -162,7 +162,8 @@ class Model:
                                                   [wl.layers[i].r for i in g]) for g in self.groups)
         else:
             wf = 0
-        wb = max(cp.bwd_workspace_bytes(T, L.n, L.m, L.r) for L in wl.layers)
+        wb = max(cp.bwd_group_workspace_bytes(T, wl.layers[g[0]].n, [wl.layers[i].m for i in g],
+                                              [wl.layers[i].r for i in g]) for g in self.groups)
         wsz = max(cp.step_workspace_bytes(L.n, L.m, L.r) for L in wl.layers)
         self.batch = cp.prepare_layers([dict(W=self.W[i], G=self.G[i], M=self.M[i], V=self.V[i], seed=L.seed,
                                              alpha=wl.alpha) for i, L in enumerate(wl.layers)])
@@ -183,25 +184,29 @@ class Model:
             self.cp.compact_fwd_group(x, self.Wg[gi], y, self.zg[gi], [L.m for L in Ls], [L.r for L in Ls],
                                       [self.seeds[i] for i in g], proj=self.proj, ws=self.ws_f)
 
+    def _bwd(self, gi, dx, ghat):
+        g = self.groups[gi]
+        Ls = [self.wl.layers[i] for i in g]
+        dy = self.dy[self.msum[gi]]
+        if len(g) == 1:
+            self.cp.compact_bwd(dy, self.Wg[gi] if dx else None, self.zg[gi] if ghat else None,
+                                self.dx[Ls[0].n] if dx else None, self.G[g[0]] if ghat else None, ws=self.ws_b)
+        else:
+            self.cp.compact_bwd_group(dy, self.Wg[gi] if dx else None, self.zg[gi] if ghat else None,
+                                      self.dx[Ls[0].n] if dx else None, [self.G[i] for i in g] if ghat else None,
+                                      [L.m for L in Ls], [L.r for L in Ls], ws=self.ws_b)
+
     def bwd_dx(self, gi):
         """dL/dx of a group: one GEMM over its concatenated weight."""
-        g = self.groups[gi]
-        n = self.wl.layers[g[0]].n
-        self.cp.compact_bwd(self.dy[self.msum[gi]], self.Wg[gi], None, self.dx[n], None)
+        self._bwd(gi, True, False)
 
     def bwd_ghat(self, gi):
-        """G^ of each layer of a group, from the column slices of dL/do and z."""
-        g = self.groups[gi]
-        dy = self.dy[self.msum[gi]]
-        mo = 0
-        for i in g:
-            L = self.wl.layers[i]
-            self.cp.compact_bwd(dy[:, mo:mo + L.m], None, self.z[i], None, self.G[i], ws=self.ws_b)
-            mo += L.m
+        """G^ of every layer of a group: one split-K launch over the column slices of dL/do and z."""
+        self._bwd(gi, False, True)
 
     def bwd(self, gi):
-        self.bwd_dx(gi)
-        self.bwd_ghat(gi)
+        """Alg. 2 for a group: compact_bwd(_group) computes dL/dx and every G^ in one call."""
+        self._bwd(gi, True, True)
 
     def upd(self, i, t):
         wl = self.wl

@@ -137,9 +137,9 @@ size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype);
  *          columns of all projections share output tiles); otherwise, and for
  *          fp32, it runs compact_fwd on each column slice.
  * Results are bitwise identical to compact_fwd on each (W_j, y_j, z_j) slice.
- * The backward of the group needs no entry of its own: dx = dL/dx summed over
- * the projections is compact_bwd with W and the concatenated dL/do, and each
- * G^_j is compact_bwd on the column slices z_j and dL/do_j.
+ * The backward of the group is compact_bwd_group (or compact_bwd with W and
+ * the concatenated dL/do for dx, and on the column slices z_j, dL/do_j for
+ * each G^_j).
  * Errors: COMPACT_EINVAL (count, NULL arrays, shapes), COMPACT_EALIGN,
  * COMPACT_EWORKSPACE, COMPACT_EHIP; nothing is launched on a validation error.
  */
@@ -169,6 +169,38 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
                 int64_t m, int64_t r, int dtype, void* ws, size_t ws_bytes, void* stream);
 
 size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype);
+
+/*
+ * Backward pass of an input group (the projections of one compact_fwd_group
+ * call), Alg. 2 per projection:
+ *
+ *   dx = sum over j of dL/do_j W_j^T = dL/do W^T   (the input is shared)
+ *   G^_j = z_j^T dL/do_j,  j = 0 .. count-1
+ *
+ *   dy [tokens x M]  (ld lddy)  dL/do = [dL/do_0 | dL/do_1 | ...], columns as W
+ *   W  [n x M]       (ld ldw)   W = [W_0 | W_1 | ...] (needed only for dx)
+ *   z  [tokens x R]  (ld ldz)   z = [z_0 | z_1 | ...] from compact_fwd_group
+ *   dx [tokens x n]  (ld lddx)  may be NULL to skip it
+ *   G  HOST array of count device pointers, G[j] [r[j] x m[j]] fp32 dense; the
+ *      array may be NULL to skip every G^ (not together with dx == NULL)
+ *   m, r  HOST arrays of count entries (as in compact_fwd_group: every m[j],
+ *      r[j] but the last a multiple of 8), count 1 .. 8
+ *   ws, ws_bytes  workspace of at least
+ *      compact_bwd_group_workspace_bytes(tokens, n, count, m, r, dtype) bytes
+ * bf16: one dx GEMM, then one split-K launch for every G^_j (one grid of about
+ * one workgroup per CU over all projections) and one reduction launch; the
+ * splits are summed in a fixed order, so each G^_j is deterministic (it may
+ * differ in the last bits from compact_bwd on the slices, whose token splits
+ * differ).  dx is bitwise compact_bwd's.  fp32: compact_bwd per slice.
+ * Errors: COMPACT_EINVAL, COMPACT_EALIGN, COMPACT_EWORKSPACE, COMPACT_EHIP;
+ * nothing is launched on a validation error.
+ */
+int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
+                      void* dx, int64_t lddx, float* const* G, int64_t tokens, int64_t n, int32_t count,
+                      const int64_t* m, const int64_t* r, int dtype, void* ws, size_t ws_bytes, void* stream);
+
+size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t count, const int64_t* m,
+                                         const int64_t* r, int dtype);
 
 /*
  * Optimizer step, Alg. 3 (Adam on the compressed gradient, then decompression):

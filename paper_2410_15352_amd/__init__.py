@@ -175,6 +175,36 @@ def compact_bwd(dy, W, z, dx, G, ws=None, stream=None):
     _check("compact_bwd", st)
 
 
+def bwd_group_workspace_bytes(tokens, n, ms, rs, dtype=BF16):
+    count, m_arr, r_arr, _ = _group_arrays(ms, rs)
+    return int(_lib.load().compact_bwd_group_workspace_bytes(int(tokens), int(n), count, m_arr, r_arr, dtype))
+
+
+def compact_bwd_group(dy, W, z, dx, Gs, ms, rs, ws=None, stream=None):
+    """Alg. 2 for the projections of an input group: dx = dy W^T over the
+    concatenated weight W = [W_0 | W_1 | ...] (the sum over the projections)
+    and G^_j = z_j^T dy_j for column slices dy_j (sum(ms[:j]) ..) and z_j
+    (sum(rs[:j]) ..), one split-K launch for all of them.  dx or Gs may be
+    None; Gs is a list of contiguous (r_j, m_j) fp32 tensors."""
+    import ctypes
+    lib = _lib.load()
+    T = dy.shape[0]
+    count, m_arr, r_arr, _ = _group_arrays(ms, rs)
+    n = W.shape[0] if W is not None else (dx.shape[1] if dx is not None else max(int(v) for v in rs))
+    g_arr = None
+    if Gs is not None:
+        if len(Gs) != count:
+            raise ValueError("one G per projection")
+        for G, m, r in zip(Gs, ms, rs):
+            if not G.is_contiguous() or tuple(G.shape) != (r, m):
+                raise ValueError("every G must be a contiguous (r, m) fp32 tensor")
+        g_arr = (ctypes.c_void_p * count)(*[G.data_ptr() for G in Gs])
+    wp, wb = _ws(ws)
+    st = lib.compact_bwd_group(_ptr(dy), _ld(dy), _ptr(W), _ld(W), _ptr(z), _ld(z), _ptr(dx), _ld(dx), g_arr, T,
+                               n, count, m_arr, r_arr, _dtype_code(dy), wp, wb, _stream(stream, dy))
+    _check("compact_bwd_group", st)
+
+
 def compact_step(W, G, M, V, seed, t, lr, beta1=0.9, beta2=0.999, eps=1e-8, alpha=1.0,
                  proj="gaussian", dtype=None, ws=None, stream=None):
     """Adam on the compressed gradient and W -= lr alpha P N (Alg. 3), in place."""

@@ -79,6 +79,11 @@ int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
 
 constexpr size_t kWsAlign = 256;
 
+void* align_ws(void* ws) {
+  const uintptr_t a = (reinterpret_cast<uintptr_t>(ws) + kWsAlign - 1) & ~uintptr_t(kWsAlign - 1);
+  return reinterpret_cast<void*>(a);
+}
+
 // Tile shapes of the bf16 kernels.  Forward and dx: 256 x 256 tiles, 8 waves
 // in a 4 x 2 grid (64 x 128 per wave), two LDS stages of 64 KB.  G^: 128 x 128
 // tiles, 4 waves (r is often 128 or less).
@@ -109,28 +114,50 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
   return s;
 }
 
-// Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp): 128 x 256
-// tiles, about one workgroup per CU, splits of whole 32-token K tiles.
-SplitPlan ghat_w4_plan(int64_t tokens, int64_t r, int64_t m) {
-  SplitPlan s;
-  s.tiles_r = static_cast<int>(ceil_div(r, kGhTm));
-  s.tiles_m = static_cast<int>(ceil_div(m, kGhTn));
-  const int64_t tiles = int64_t(s.tiles_r) * s.tiles_m;
+// Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp) for one or
+// more projections of the same tokens (one launch): 128 x 256 tiles, one split
+// count for all of them, at most one workgroup per CU (256 on MI355X), splits
+// of whole 32-token K tiles.  Projection j's partial sums take
+// splits x (tiles_r 128) x (tiles_m 256) fp32 at byte offset part_off[j].
+struct GhatGroupPlan {
+  int count;
+  int tiles_r[kGhMaxLayers], tiles_m[kGhMaxLayers];
+  int tiles, splits;
+  int64_t split_len;
+  size_t part_off[kGhMaxLayers], bytes;
+};
+
+GhatGroupPlan ghat_group_plan(int64_t tokens, int count, const int64_t* r, const int64_t* m) {
+  GhatGroupPlan g{};
+  g.count = count;
+  int64_t tiles = 0;
+  for (int j = 0; j < count; ++j) {
+    g.tiles_r[j] = static_cast<int>(ceil_div(r[j], kGhTm));
+    g.tiles_m[j] = static_cast<int>(ceil_div(m[j], kGhTn));
+    tiles += int64_t(g.tiles_r[j]) * g.tiles_m[j];
+  }
+  g.tiles = static_cast<int>(tiles);
   const int64_t ktiles = ceil_div(tokens > 0 ? tokens : 1, kGhK);
-  int64_t splits = (256 + tiles / 2) / tiles;
+  int64_t splits = tiles > 0 ? 256 / tiles : 1;
   if (splits < 1) splits = 1;
   if (splits > ktiles) splits = ktiles;
-  s.split_len = ceil_div(ktiles, splits) * kGhK;
-  s.splits = static_cast<int>(ceil_div(tokens > 0 ? tokens : 1, s.split_len));
-  return s;
+  g.split_len = ceil_div(ktiles, splits) * kGhK;
+  g.splits = static_cast<int>(ceil_div(tokens > 0 ? tokens : 1, g.split_len));
+  size_t off = 0;
+  for (int j = 0; j < count; ++j) {
+    g.part_off[j] = off;
+    const size_t b = size_t(g.splits) * size_t(g.tiles_r[j]) * kGhTm * size_t(g.tiles_m[j]) * kGhTn * sizeof(float);
+    off += size_t(round_up(static_cast<int64_t>(b), kWsAlign));
+  }
+  g.bytes = off;
+  return g;
 }
 
-// The transposing-read kernel handles the problem: 32-bit buffer offsets over
-// a split plus one K tile, and the partial-sum layout of its plan.
-bool ghat_w4_eligible(int64_t tokens, int64_t r, int64_t m, int64_t ldz, int64_t lddy) {
-  if (tokens < 1 || tokens > (int64_t(1) << 30) || r < 1 || m < 1) return false;
-  const SplitPlan sp = ghat_w4_plan(tokens, r, m);
-  const int64_t span = sp.split_len + 2 * kGhK;
+// The transposing-read kernel takes projection (z, dL/do) of the plan:
+// 32-bit buffer offsets over a split plus one K tile.
+bool ghat_w4_eligible(const GhatGroupPlan& g, int64_t tokens, int64_t ldz, int64_t lddy) {
+  if (tokens < 1 || tokens > (int64_t(1) << 30)) return false;
+  const int64_t span = g.split_len + 2 * kGhK;
   const int64_t lim = int64_t(1) << 31;
   return span * ldz * 2 < lim && span * lddy * 2 < lim && ldz < lim / 4 && lddy < lim / 4;
 }
@@ -138,8 +165,7 @@ bool ghat_w4_eligible(int64_t tokens, int64_t r, int64_t m, int64_t ldz, int64_t
 size_t ghat_ws_bytes(int64_t tokens, int64_t r, int64_t m) {
   const SplitPlan s = ghat_plan(tokens, r, m);
   const size_t a = size_t(s.splits) * size_t(s.tiles_r) * kGBM * size_t(s.tiles_m) * kGBN * sizeof(float);
-  const SplitPlan w = ghat_w4_plan(tokens, r, m);
-  const size_t b = size_t(w.splits) * size_t(w.tiles_r) * kGhTm * size_t(w.tiles_m) * kGhTn * sizeof(float);
+  const size_t b = ghat_group_plan(tokens, 1, &r, &m).bytes;
   return a > b ? a : b;  // either path may run (the choice depends on the leading dimensions)
 }
 
@@ -155,6 +181,47 @@ int launch_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t pla
     hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s, part,
                        splits, ldp, plane, r, m, G);
   }
+  return check_launch("G^ reduce");
+}
+
+// G^_j = z_j^T dL/do_j for the projections of a plan: one split-K launch over
+// the layer table and one reduction launch.  z[j], dy[j] may be column slices.
+int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const* z, const int64_t* ldz,
+                      const void* const* dy, const int64_t* lddy, float* const* G, const int64_t* r,
+                      const int64_t* m, void* ws, hipStream_t s) {
+  GhatW4Params p{};
+  ReduceBatch rb{};
+  char* base = static_cast<char*>(align_ws(ws));
+  p.count = rb.count = g.count;
+  p.T = static_cast<int>(tokens);
+  p.splits = rb.splits = g.splits;
+  p.split_len = static_cast<int>(g.split_len);
+  int tb = 0, rbk = 0;
+  for (int j = 0; j < g.count; ++j) {
+    GhatW4Layer& L = p.layer[j];
+    L.z = static_cast<const uint16_t*>(z[j]); L.ldz = static_cast<int>(ldz[j]);
+    L.dy = static_cast<const uint16_t*>(dy[j]); L.lddy = static_cast<int>(lddy[j]);
+    L.part = reinterpret_cast<float*>(base + g.part_off[j]);
+    L.r = static_cast<int>(r[j]); L.m = static_cast<int>(m[j]);
+    L.tiles_r = g.tiles_r[j]; L.tiles_m = g.tiles_m[j];
+    p.tile_begin[j] = tb;
+    tb += g.tiles_r[j] * g.tiles_m[j];
+    ReduceLayer& R = rb.layer[j];
+    R.part = L.part;
+    R.G = G[j];
+    R.ldp = int64_t(g.tiles_m[j]) * kGhTn;
+    R.plane = int64_t(g.tiles_r[j]) * kGhTm * R.ldp;
+    R.r = L.r; R.m = L.m;
+    R.mq = static_cast<int>(ceil_div(m[j], 4));
+    R.vec = (m[j] % 4 == 0 && aligned16(G[j])) ? 1 : 0;
+    rb.begin[j] = rbk;
+    rbk += static_cast<int>(ceil_div(r[j] * R.mq, 256));
+  }
+  p.tile_begin[g.count] = tb;
+  rb.begin[g.count] = rbk;
+  const hipError_t e = ghat_w4_launch(p, s);
+  if (e != hipSuccess) return fail(COMPACT_EHIP, "G^ split-K (bf16): %s", hipGetErrorString(e));
+  if (rbk > 0) hipLaunchKernelGGL(k_splitk_reduce_batched, dim3(static_cast<uint32_t>(rbk)), dim3(256), 0, s, rb);
   return check_launch("G^ reduce");
 }
 
@@ -279,11 +346,6 @@ static size_t step_layer_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
 size_t compact_step_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
   if (n < 1 || m < 1 || r < 1) return 0;
   return step_layer_bytes(n, m, r, dtype) + kWsAlign;
-}
-
-static void* align_ws(void* ws) {
-  const uintptr_t a = (reinterpret_cast<uintptr_t>(ws) + kWsAlign - 1) & ~uintptr_t(kWsAlign - 1);
-  return reinterpret_cast<void*>(a);
 }
 
 }  // extern "C"
@@ -567,19 +629,9 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     hipLaunchKernelGGL(fn, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), kGemmLds, s, p);
     if ((st = check_launch("dx (bf16)"))) return st;
   }
-  if (G != nullptr && ghat_w4_eligible(tokens, r, m, ldz, lddy)) {
-    const SplitPlan sp = ghat_w4_plan(tokens, r, m);
-    GhatW4Params p{};
-    p.z = static_cast<const uint16_t*>(z); p.ldz = static_cast<int>(ldz);
-    p.dy = static_cast<const uint16_t*>(dy); p.lddy = static_cast<int>(lddy);
-    p.part = static_cast<float*>(align_ws(ws));
-    p.T = static_cast<int>(tokens); p.r = static_cast<int>(r); p.m = static_cast<int>(m);
-    p.tiles_r = sp.tiles_r; p.tiles_m = sp.tiles_m; p.splits = sp.splits;
-    p.split_len = static_cast<int>(sp.split_len);
-    const hipError_t e = ghat_w4_launch(p, s);
-    if (e != hipSuccess) return fail(COMPACT_EHIP, "G^ split-K (bf16): %s", hipGetErrorString(e));
-    const int64_t ldp = int64_t(sp.tiles_m) * kGhTn, plane = int64_t(sp.tiles_r) * kGhTm * ldp;
-    if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, s))) return st;
+  const GhatGroupPlan gp = ghat_group_plan(tokens, 1, &r, &m);
+  if (G != nullptr && ghat_w4_eligible(gp, tokens, ldz, lddy)) {
+    if ((st = launch_ghat_group(gp, tokens, &z, &ldz, &dy, &lddy, &G, &r, &m, ws, s))) return st;
   } else if (G != nullptr) {
     const SplitPlan sp = ghat_plan(tokens, r, m);
     GhatParams p{};
@@ -595,6 +647,81 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     const int64_t ldp = int64_t(sp.tiles_m) * kGBN, plane = int64_t(sp.tiles_r) * kGBM * ldp;
     if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, s))) return st;
   }
+  return ok();
+}
+
+size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t count, const int64_t* m,
+                                         const int64_t* r, int dtype) {
+  if (dtype != COMPACT_BF16 || tokens < 0 || count < 1 || count > kGhMaxLayers || m == nullptr || r == nullptr)
+    return 0;
+  for (int j = 0; j < count; ++j)
+    if (m[j] < 1 || r[j] < 1) return 0;
+  // the one-launch plan, or compact_bwd on each slice when it does not apply
+  size_t need = ghat_group_plan(tokens, count, r, m).bytes;
+  for (int j = 0; j < count; ++j) need = std::max(need, ghat_ws_bytes(tokens, r[j], m[j]));
+  return need + kWsAlign;
+}
+
+int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
+                      void* dx, int64_t lddx, float* const* G, int64_t tokens, int64_t n, int32_t count,
+                      const int64_t* m, const int64_t* r, int dtype, void* ws, size_t ws_bytes, void* stream) {
+  int st;
+  if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
+  if (count < 1 || count > kGhMaxLayers) return fail(COMPACT_EINVAL, "group of %d projections (1 .. %d)", count, kGhMaxLayers);
+  if (m == nullptr || r == nullptr) return fail(COMPACT_EINVAL, "m or r array is NULL");
+  if (dx == nullptr && G == nullptr) return fail(COMPACT_EINVAL, "dx and G are both NULL");
+  int64_t msum = 0, rsum = 0;
+  for (int j = 0; j < count; ++j) {
+    if ((st = check_shape(tokens, n, m[j], r[j], COMPACT_PROJ_GAUSSIAN))) return st;
+    if (j + 1 < count && (m[j] % 8 != 0 || r[j] % 8 != 0))
+      return fail(COMPACT_EALIGN, "group member %d: m and r of all but the last projection must be multiples of 8", j);
+    if (G != nullptr && G[j] == nullptr) return fail(COMPACT_EINVAL, "G[%d] is NULL", j);
+    if (G != nullptr && (st = check_dense("G", G[j]))) return st;
+    msum += m[j];
+    rsum += r[j];
+  }
+  if ((st = check_matrix("dy", dy, lddy, msum, dtype))) return st;
+  if (dx != nullptr) {
+    if ((st = check_matrix("W", W, ldw, msum, dtype))) return st;
+    if ((st = check_matrix("dx", dx, lddx, n, dtype))) return st;
+  }
+  if (G != nullptr) {
+    if ((st = check_matrix("z", z, ldz, rsum, dtype))) return st;
+    const size_t need = compact_bwd_group_workspace_bytes(tokens, n, count, m, r, dtype);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+      return fail(COMPACT_EWORKSPACE, "backward workspace %zu B < %zu B", ws_bytes, need);
+  }
+  // dL/dx summed over the projections: one GEMM over the concatenated weight
+  if (dx != nullptr) {
+    if ((st = compact_bwd(dy, lddy, W, ldw, nullptr, ldz, dx, lddx, nullptr, tokens, n, msum, 1, dtype, nullptr,
+                          0, stream)))
+      return st;
+  }
+  if (G == nullptr) return ok();
+  const size_t esz = elem_size(dtype);
+  const void* zs[kGhMaxLayers];
+  const void* dys[kGhMaxLayers];
+  int64_t ldzs[kGhMaxLayers], lddys[kGhMaxLayers];
+  int64_t mo = 0, ro = 0;
+  for (int j = 0; j < count; ++j) {
+    zs[j] = static_cast<const char*>(z) + ro * esz;
+    dys[j] = static_cast<const char*>(dy) + mo * esz;
+    ldzs[j] = ldz;
+    lddys[j] = lddy;
+    mo += m[j];
+    ro += r[j];
+  }
+  const GhatGroupPlan gp = ghat_group_plan(tokens, count, r, m);
+  if (dtype == COMPACT_BF16 && tokens > 0 && ghat_w4_eligible(gp, tokens, ldz, lddy)) {
+    if ((st = launch_ghat_group(gp, tokens, zs, ldzs, dys, lddys, G, r, m, ws, static_cast<hipStream_t>(stream))))
+      return st;
+    return ok();
+  }
+  // otherwise G^ of each projection on its own
+  for (int j = 0; j < count; ++j)
+    if ((st = compact_bwd(dys[j], lddy, nullptr, ldw, zs[j], ldz, nullptr, lddx, G[j], tokens, n, m[j], r[j], dtype,
+                          ws, ws_bytes, stream)))
+      return st;
   return ok();
 }
 

@@ -7,7 +7,10 @@
 // Workgroup: 4 waves, output tile 128 (rows of G^) x 256 (columns), each
 // wave 64 x 128 (2 x 4 MFMA 32x32x16 fragments), over one range of tokens
 // (a split); the fp32 partial tile goes to part[split] and a separate kernel
-// sums the splits in a fixed order (deterministic G^).
+// sums the splits in a fixed order (deterministic G^).  One launch covers up
+// to 8 projections of the same tokens (a layer table): the projections of an
+// input group then share one grid of about one workgroup per CU, with fewer
+// and longer splits than a launch per projection would have.
 //
 // Pipeline as in gemm_w4.hpp: 32-token K tiles, four LDS stages, copies by
 // buffer_load_dwordx4 ... lds issued 3 K tiles ahead (six stages, 5 ahead, time
@@ -46,13 +49,25 @@ constexpr int kGhBStage = kGhK * kGhTn * 2;  // 16 KB
 constexpr int kGhBBase = kGhStages * kGhAStage;
 constexpr size_t kGhLds = size_t(kGhStages) * (kGhAStage + kGhBStage);  // 96 KB
 
-struct GhatW4Params {
-  const uint16_t* z;  // [T][ldz]
+// One projection of a launch: G^_j = z_j^T dL/do_j.  The projections of one
+// launch share the token count and the split plan; in an input group (q, k, v
+// or gate, up) z_j and dL/do_j are column slices of the group's z and dL/do.
+struct GhatW4Layer {
+  const uint16_t* z;   // [T][ldz]
   const uint16_t* dy;  // [T][lddy]
   float* part;         // [splits][tiles_r * 128][tiles_m * 256]
   int ldz, lddy;
-  int T, r, m;
-  int tiles_r, tiles_m, splits;
+  int r, m;
+  int tiles_r, tiles_m;
+};
+
+constexpr int kGhMaxLayers = 8;
+
+struct GhatW4Params {
+  GhatW4Layer layer[kGhMaxLayers];
+  int tile_begin[kGhMaxLayers + 1];  // first tile of each layer; tile_begin[count] = tiles per split
+  int count;
+  int T, splits;
   int split_len;  // tokens per split, a multiple of kGhK
 };
 
@@ -134,26 +149,30 @@ __device__ __forceinline__ void gh_read(uint32_t lbase, uint32_t sa, uint32_t sb
   for (int j = 0; j < 4; ++j) fb[j] = gh_frag<kGhTn>(lbase + sb, wn * 128 + j * 32, kk, lane);
 }
 
-// The G^ partial tile of workgroup (split, column tile, row tile).
-__device__ __forceinline__ void ghat_w4(const GhatW4Params& p) {
+// The G^ partial tile of workgroup (split, layer, column tile, row tile).
+__device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
-  // order (split, column tile, row tile): the row tiles that share dL/do columns
-  // are adjacent, hence on the same XCD at the same time
-  const int tiles = p.tiles_r * p.tiles_m;
-  const int split = static_cast<int>(logical / tiles), tile = static_cast<int>(logical % tiles);
+  // order (split, layer, column tile, row tile): the row tiles that share dL/do
+  // columns, and the column tiles of one layer that share z, are adjacent,
+  // hence on the same XCD at the same time
+  const int tiles = prm.tile_begin[prm.count];
+  const int split = static_cast<int>(logical / tiles), tile_all = static_cast<int>(logical % tiles);
+  const int li = batch_layer_of(prm.tile_begin, prm.count, tile_all);
+  const GhatW4Layer& p = prm.layer[li];
+  const int tile = tile_all - prm.tile_begin[li];
   const int ct = tile / p.tiles_r, rt = tile % p.tiles_r;
   const int row0 = rt * kGhTm, col0 = ct * kGhTn;
-  const int t_begin = split * p.split_len;
-  const int t_end = min(t_begin + p.split_len, p.T);
+  const int t_begin = split * prm.split_len;
+  const int t_end = min(t_begin + prm.split_len, prm.T);
   const int kt = (t_end - t_begin + kGhK - 1) / kGhK;
 
   // buffer ranges: from the split's first token to the last element of the
   // matrix (z and dL/do may be column slices of wider matrices)
-  const int64_t zbytes = view_bytes(p.T, p.r, p.ldz, t_begin, row0, 2);
-  const int64_t ybytes = view_bytes(p.T, p.m, p.lddy, t_begin, col0, 2);
+  const int64_t zbytes = view_bytes(prm.T, p.r, p.ldz, t_begin, row0, 2);
+  const int64_t ybytes = view_bytes(prm.T, p.m, p.lddy, t_begin, col0, 2);
   const __amdgpu_buffer_rsrc_t rz = w4_rsrc(p.z + static_cast<int64_t>(t_begin) * p.ldz + row0, zbytes);
   const __amdgpu_buffer_rsrc_t ry = w4_rsrc(p.dy + static_cast<int64_t>(t_begin) * p.lddy + col0, ybytes);
   // this wave's copy blocks: z^T blocks 2 wave + {0, 1}, dL/do blocks 4 wave + {0 .. 3}

@@ -22,7 +22,7 @@ enum class W4Use { kForward, kDx };
 // Launches C = A B^T on `stream`, one workgroup per CU (at most one per tile).
 hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream);
 
-// G^ partials: one workgroup per (split, column tile, row tile).
+// G^ partials: one workgroup per (split, layer, column tile, row tile).
 hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream);
 
 // True when the decompression kernel takes a layer of this shape and layout.

@@ -297,6 +297,63 @@ __global__ void k_splitk_reduce4(const float* part, int splits, int64_t ldp, int
   *reinterpret_cast<f32x4*>(G + j * m + c) = s;
 }
 
+// The reduction for several projections in one launch (one G^ split-K launch
+// over a layer table): thread q of layer l sums columns 4 (q mod (m/4 rounded
+// up)) .. + 3 of one row over the splits in order; the partial rows are
+// 256-column padded, so the 16-byte loads stay inside them.
+struct ReduceLayer {
+  const float* part;  // [splits][rows][ldp]
+  float* G;           // [r][m] dense
+  int64_t ldp, plane;
+  int r, m, mq;       // mq = ceil(m / 4)
+  int vec;            // m % 4 == 0 and G 16-byte aligned: 16-byte stores
+};
+
+struct ReduceBatch {
+  int count, splits;
+  int begin[9];  // first workgroup of each layer; begin[count] = grid
+  ReduceLayer layer[8];
+};
+
+__global__ void k_splitk_reduce_batched(ReduceBatch b) {
+  const int l = batch_layer_of(b.begin, b.count, static_cast<int>(blockIdx.x));
+  const ReduceLayer& p = b.layer[l];
+  const int64_t q = static_cast<int64_t>(blockIdx.x - b.begin[l]) * blockDim.x + threadIdx.x;
+  if (q >= static_cast<int64_t>(p.r) * p.mq) return;
+  const int64_t j = q / p.mq, c = (q % p.mq) * 4;
+  const float* src = p.part + j * p.ldp + c;
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (; k + 16 <= b.splits; k += 16) {
+    f32x4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = *reinterpret_cast<const f32x4*>(src + (k + u) * p.plane);
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      s.x = s.x + v[u].x;
+      s.y = s.y + v[u].y;
+      s.z = s.z + v[u].z;
+      s.w = s.w + v[u].w;
+    }
+  }
+  for (; k < b.splits; ++k) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(src + k * p.plane);
+    s.x = s.x + v.x;
+    s.y = s.y + v.y;
+    s.z = s.z + v.z;
+    s.w = s.w + v.w;
+  }
+  float* dst = p.G + j * p.m + c;
+  if (p.vec) {
+    *reinterpret_cast<f32x4*>(dst) = s;
+  } else {
+    const float e[4] = {s.x, s.y, s.z, s.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c + u < p.m) dst[u] = e[u];
+  }
+}
+
 // G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c].
 __global__ void k_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t plane,
                                 int64_t r, int64_t m, float* G) {

@@ -119,7 +119,7 @@ hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
     if (e != hipSuccess) return e;
     g_lds_set[dev][2].store(true, std::memory_order_release);
   }
-  const int64_t blocks = int64_t(p.tiles_r) * p.tiles_m * p.splits;
+  const int64_t blocks = int64_t(p.tile_begin[p.count]) * p.splits;
   if (blocks <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_ghat_w4, dim3(static_cast<uint32_t>(blocks)), dim3(256), kGhLds, stream, p);
   return hipGetLastError();

@@ -169,6 +169,44 @@ def test_bwd_validation(lib, kw, status):
     assert st == status
 
 
+def test_bwd_group_workspace_size(lib):
+    # one split-K plan for all projections; at least what each slice needs alone
+    ms, rs = _i64s(1024, 1024, 1024), _i64s(128, 128, 128)
+    need = lib.compact_bwd_group_workspace_bytes(65536, 1024, 3, ms, rs, 1)
+    assert need >= lib.compact_bwd_workspace_bytes(65536, 1024, 1024, 128, 1)
+    # 12 tiles of 128 x 256, 21 splits: 3 x 21 x 128 x 1024 fp32 partial sums (+ alignment)
+    assert need >= 3 * 21 * 128 * 1024 * 4
+    assert lib.compact_bwd_group_workspace_bytes(65536, 1024, 3, ms, rs, 0) == 0
+    assert lib.compact_bwd_group_workspace_bytes(65536, 1024, 0, ms, rs, 1) == 0
+    assert lib.compact_bwd_group_workspace_bytes(65536, 1024, 9, ms, rs, 1) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(count=0), -1), (dict(count=9), -1), (dict(m=None), -1), (dict(r=None), -1),
+    (dict(dx=None, G=None), -1),
+    (dict(m=(1020, 1024, 1024)), -2),   # a slice that is not 16-byte aligned
+    (dict(r=(128, 124, 128)), -2),
+    (dict(r=(128, 128, 2000)), -1),     # r > n
+    (dict(lddy=3000), -1),              # ld < sum of m
+    (dict(ldz=376), -1),                # ld < sum of r
+    (dict(G=(FAKE, None, FAKE)), -1),
+    (dict(G=(FAKE, FAKE + 4, FAKE)), -2),
+    (dict(ws=None), -4), (dict(ws_bytes=64), -4),
+])
+def test_bwd_group_validation(lib, kw, status):
+    a = dict(dy=FAKE, lddy=3072, W=FAKE, ldw=3072, z=FAKE, ldz=384, dx=FAKE, lddx=1024, G=(FAKE, FAKE, FAKE),
+             tokens=4096, n=1024, count=3, m=(1024, 1024, 1024), r=(128, 128, 128), dtype=1, ws=FAKE,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    arr = lambda v, t: None if v is None else (t * len(v))(*v)
+    st = lib.compact_bwd_group(a["dy"], a["lddy"], a["W"], a["ldw"], a["z"], a["ldz"], a["dx"], a["lddx"],
+                               arr(a["G"], ctypes.c_void_p), a["tokens"], a["n"], a["count"],
+                               arr(a["m"], ctypes.c_int64), arr(a["r"], ctypes.c_int64), a["dtype"], a["ws"],
+                               a["ws_bytes"], a["stream"])
+    assert st == status
+    assert lib.compact_last_error()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(t=0), -1), (dict(beta1=1.0), -1), (dict(beta2=-0.1), -1), (dict(eps=0.0), -1),
     (dict(lr=-1.0), -1), (dict(lr=float("nan")), -1), (dict(ws=None), -4),

@@ -1,10 +1,10 @@
 """Parity at the benchmark's full sizes: LLaMA-350M shapes and 65536 tokens, in
 the launch configuration the benchmark times.  q|k|v and gate|up run as input
 groups (compact_fwd_group with its workspace: one staged operand, one
-persistent GEMM); o and down run alone; dL/dx of a group is one compact_bwd
-over the concatenated weight; G^ is computed per layer on column slices; Alg. 3
-runs for all 168 layers in one compact_step_batched call on column slices of
-the group weights.
+persistent GEMM); o and down run alone; the backward of each group is one
+compact_bwd_group call (dL/dx over the concatenated weight, every G^_j of the
+group in one split-K launch); Alg. 3 runs for all 168 layers in one
+compact_step_batched call on column slices of the group weights.
 
 The oracle computes sampled outputs directly from the same seeded inputs (it
 never sees a GPU value): rows of y, z and dL/dx for sampled tokens (the last
@@ -66,16 +66,9 @@ def test_full_size_forward_backward(kind):
     else:
         cp.compact_fwd(xd, Wd, y, z, seeds[0], ws=ws_f)
     dx = empty(T, n, "bf16", ld_for(n, "bf16"))
-    cp.compact_bwd(dyd, Wd, None, dx, None)
-    ws_b = workspace(max(cp.bwd_workspace_bytes(T, n, m, r) for m, r in zip(ms, rs)))
-    Gs = []
-    mo = ro = 0
-    for m, r in zip(ms, rs):
-        G = torch.empty(r, m, dtype=torch.float32, device=dev())
-        cp.compact_bwd(dyd[:, mo:mo + m], None, z[:, ro:ro + r], None, G, ws=ws_b)
-        Gs.append(G)
-        mo += m
-        ro += r
+    Gs = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    ws_b = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs))
+    cp.compact_bwd_group(dyd, Wd, z, dx, Gs, ms, rs, ws=ws_b)
     torch.cuda.synchronize()
 
     rng = np.random.default_rng(7)

@@ -6,9 +6,15 @@ attention; gate and up of the MLP), each with its own seed and rank.
   the persistent kernel takes and on ragged ones it does not.
 * Each projection matches the fp64 oracle's forward (Alg. 1) within the bf16
   tolerance.
-* The backward of a group through the existing ABI: dx from one compact_bwd over
-  the concatenated weight equals the sum over projections of the oracle's
-  dL/do_j W_j^T, and each G^_j from the column slices matches the oracle.
+* The backward of a group through compact_bwd on the concatenated weight and
+  the column slices: dx equals the sum over projections of the oracle's
+  dL/do_j W_j^T, and each G^_j matches the oracle.
+* compact_bwd_group (one dx GEMM, one G^ launch for all projections): the same
+  oracle checks on every group shape (including fewer tokens than splits and a
+  single projection whose rank spans several row tiles), dx bitwise equal to
+  compact_bwd over the concatenated weight, each G^_j within 1e-5 of the
+  per-slice call (the token splits differ), dx-only / G^-only calls and zero
+  tokens.
 """
 import numpy as np
 import pytest
@@ -153,3 +159,89 @@ def test_ghat_and_step_on_overhanging_column_slices():
     assert torch.equal(W_all[:, m:].contiguous().view(torch.int16), W_copy.view(torch.int16))
     # the first slice is untouched
     assert torch.equal(W_all[:, :m].contiguous().view(torch.int16), to_dev(W_a, "bf16").view(torch.int16))
+
+
+def _bwd_group_inputs(T, n, ms, rs, data_seed):
+    parts = [bwd_inputs(T, n, m, r, "bf16", data_seed=data_seed + j) for j, (m, r) in enumerate(zip(ms, rs))]
+    M, R = sum(ms), sum(rs)
+    dy_all = np.concatenate([p[0] for p in parts], axis=1)
+    z_all = np.concatenate([p[1] for p in parts], axis=1)
+    W_all = np.concatenate([p[2] for p in parts], axis=1)
+    dev_t = (to_dev(dy_all, "bf16", ld_for(M, "bf16")), to_dev(z_all, "bf16", ld_for(R, "bf16")),
+             to_dev(W_all, "bf16", ld_for(M, "bf16")))
+    return parts, dev_t
+
+
+BWD_GROUPS = GROUPS + [
+    (65, 512, (512, 512, 512), (128, 128, 128)),       # fewer tokens than splits x 32
+    (2048, 2736, (1024,), (342,)),                     # one projection (down), r past one row tile
+]
+
+
+@pytest.mark.parametrize("group", BWD_GROUPS, ids=_ids)
+def test_bwd_group_oracle_parity(group):
+    # Alg. 2 per projection through one compact_bwd_group call: dx against the
+    # sum of the oracle's dL/do_j W_j^T, every G^_j against the oracle's z_j^T dL/do_j
+    T, n, ms, rs = group
+    parts, (dyd, zd, Wd) = _bwd_group_inputs(T, n, ms, rs, data_seed=90 + T)
+    dx = empty(T, n, "bf16", ld_for(n, "bf16"), fill=5.0)
+    Gs = [torch.full((r, m), 7.0, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    ws = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs))
+    cp.compact_bwd_group(dyd, Wd, zd, dx, Gs, ms, rs, ws=ws)
+    torch.cuda.synchronize()
+    dx_ref = sum(oc.ref_bwd(p[0], p[1], p[2])[0] for p in parts)
+    assert oc.rel_fro(to_np(dx), dx_ref) <= TOL
+    for G, p in zip(Gs, parts):
+        assert oc.rel_fro(G.cpu().numpy(), oc.ref_bwd(p[0], p[1], p[2])[1]) <= TOL
+
+
+@pytest.mark.parametrize("group", BWD_GROUPS, ids=_ids)
+def test_bwd_group_against_per_slice_calls(group):
+    # dx is the same GEMM as compact_bwd over the concatenated weight (bitwise);
+    # each G^_j sums the same bf16 products over other token splits (fp32)
+    T, n, ms, rs = group
+    parts, (dyd, zd, Wd) = _bwd_group_inputs(T, n, ms, rs, data_seed=7 * T)
+    dx = empty(T, n, "bf16", ld_for(n, "bf16"))
+    Gs = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dyd, Wd, zd, dx, Gs, ms, rs, ws=workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs)))
+    dx1 = empty(T, n, "bf16", ld_for(n, "bf16"))
+    cp.compact_bwd(dyd, Wd, None, dx1, None)
+    G1s = []
+    mo = ro = 0
+    for m, r in zip(ms, rs):
+        G = torch.empty(r, m, dtype=torch.float32, device=dev())
+        cp.compact_bwd(dyd[:, mo:mo + m], None, zd[:, ro:ro + r], None, G,
+                       ws=workspace(cp.bwd_workspace_bytes(T, n, m, r)))
+        G1s.append(G)
+        mo += m
+        ro += r
+    torch.cuda.synchronize()
+    assert torch.equal(dx.view(torch.int16), dx1.view(torch.int16))
+    for G, G1 in zip(Gs, G1s):
+        g, g1 = G.cpu().numpy().astype(np.float64), G1.cpu().numpy().astype(np.float64)
+        assert oc.rel_fro(g, g1) <= 1e-5
+
+
+def test_bwd_group_parts_and_empty():
+    # dx only, G^ only, and zero tokens (every G^_j is zero)
+    T, n, ms, rs = 513, 512, (512, 512, 512), (128, 128, 128)
+    parts, (dyd, zd, Wd) = _bwd_group_inputs(T, n, ms, rs, data_seed=5)
+    ws = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs))
+    dx = empty(T, n, "bf16", ld_for(n, "bf16"))
+    cp.compact_bwd_group(dyd, Wd, None, dx, None, ms, rs)
+    Gs = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dyd, None, zd, None, Gs, ms, rs, ws=ws)
+    G0 = [torch.full((r, m), 3.0, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    # zero tokens through the raw ABI (an empty torch view has no data pointer)
+    import ctypes
+    lib = cp.library()
+    st = lib.compact_bwd_group(dyd.data_ptr(), dyd.stride(0), None, 0, zd.data_ptr(), zd.stride(0), None, 0,
+                               (ctypes.c_void_p * 3)(*[G.data_ptr() for G in G0]), 0, n, 3,
+                               (ctypes.c_int64 * 3)(*ms), (ctypes.c_int64 * 3)(*rs), 1, ws.data_ptr(), ws.numel(),
+                               torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert oc.rel_fro(to_np(dx), sum(oc.ref_bwd(p[0], p[1], p[2])[0] for p in parts)) <= TOL
+    for G, p in zip(Gs, parts):
+        assert oc.rel_fro(G.cpu().numpy(), oc.ref_bwd(p[0], p[1], p[2])[1]) <= TOL
+    assert all(float(G.abs().max()) == 0.0 for G in G0)
