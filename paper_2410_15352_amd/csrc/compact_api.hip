@@ -228,7 +228,16 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
 // Forward operand of the persistent GEMM, K = n contiguous: rows 0 .. m-1 hold
 // W^T, rows round_up(m, 256) .. + r - 1 hold P^T (rows in between are never
 // read into a stored output).
-int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + r; }
+// Rows of the forward's staged B operand [W^T; pad; P^T; pad]: y and z each
+// start on a 256-row tile.
+int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + round_up(r, kW4Tile); }
+
+// A K-tiled B operand of `rows` rows and K columns fits the persistent GEMM's
+// 32-bit buffer offsets.
+bool tiled_fits(int64_t rows, int64_t K) { return ceil_div(K, kW4K) * rows * 64 < (int64_t(1) << 31); }
+
+// Workspace of the dx GEMM's K-tiled copy of W: n rows padded to 256, K = m.
+size_t dx_stage_bytes(int64_t n, int64_t m) { return size_t(round_up(n, kW4Tile)) * size_t(round_up(m, kW4K)) * 2; }
 
 int w4_tiles(int64_t cols) { return static_cast<int>(ceil_div(cols, kW4Tile)); }
 int64_t n_ld(int64_t m) { return round_up(m, 8); }
@@ -330,9 +339,9 @@ size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
 }
 
 size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype) {
-  (void)n;
-  if (dtype != COMPACT_BF16 || tokens < 0 || m < 1 || r < 1) return 0;
-  return ghat_ws_bytes(tokens, r, m) + kWsAlign;
+  if (dtype != COMPACT_BF16 || tokens < 0 || n < 1 || m < 1 || r < 1) return 0;
+  // the dx GEMM's copy of W, then (after it) the G^ partial sums
+  return std::max(ghat_ws_bytes(tokens, r, m), dx_stage_bytes(n, m)) + kWsAlign;
 }
 
 // Step scratch of one layer: N [r][n_ld(m)] (compute dtype), then for bf16
@@ -374,14 +383,15 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
                  hipStream_t s, bool& taken) {
   int st;
   const int64_t ldb = pt_ld(n);
-  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, stacked_rows(G.msum, G.rsum), ldy, G.msum, ldz,
-                                            G.rsum);
+  const int64_t rows_b = stacked_rows(G.msum, G.rsum);
+  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, rows_b, ldy, G.msum, ldz, G.rsum) &&
+          tiled_fits(rows_b, n);
   if (!taken) return COMPACT_OK;
   uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
   const int64_t mp = round_up(G.msum, kW4Tile);
   FwdStage fs{};
   fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = G.msum;
-  fs.b = bs; fs.ldb = ldb;
+  fs.b = PanelOut{bs, ldb, rows_b}; fs.ldb = ldb;
   fs.count = G.count;
   fs.kind = proj_desc(proj, 1).kind;
   fs.sparse_s = proj_desc(proj, 1).s;
@@ -403,7 +413,7 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
   W4Gemm g{};
   g.A = static_cast<const uint16_t*>(x); g.lda = static_cast<int>(ldx);
   g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
-  g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(stacked_rows(G.msum, G.rsum));
+  g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(rows_b); g.b_tiled = 1;
   g.seg[0] = W4Seg{static_cast<uint16_t*>(y), static_cast<int>(ldy), static_cast<int>(G.msum), w4_tiles(G.msum)};
   g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(G.rsum), w4_tiles(G.rsum)};
   g.tiles_n = g.seg[0].tiles + g.seg[1].tiles;
@@ -603,11 +613,21 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
   }
 
   if (dx != nullptr && gemm_w4_eligible(tokens, m, lddy, ldw, n, lddx, n, 0, 0)) {
-    // persistent GEMM: dx = dL/do W^T with W [n][m] as the K-contiguous B
+    // persistent GEMM: dx = dL/do W^T with W [n][m] as the K-contiguous B,
+    // copied into the K-tiled layout first when the workspace holds it
     W4Gemm g{};
     g.A = static_cast<const uint16_t*>(dy); g.lda = static_cast<int>(lddy);
     g.M = static_cast<int>(tokens); g.K = static_cast<int>(m);
     g.B = static_cast<const uint16_t*>(W); g.ldb = static_cast<int>(ldw); g.rows_b = static_cast<int>(n);
+    const int64_t npad = round_up(n, kW4Tile);
+    if (ws != nullptr && ws_bytes >= dx_stage_bytes(n, m) + kWsAlign && tiled_fits(npad, m)) {
+      uint16_t* wt = static_cast<uint16_t*>(align_ws(ws));
+      const int64_t units = n * (m / 8);
+      hipLaunchKernelGGL(k_stage_rows_bf16, dim3(static_cast<uint32_t>(ceil_div(units, 256))), dim3(256), 0, s,
+                         static_cast<const uint16_t*>(W), ldw, n, m, PanelOut{wt, 0, npad});
+      if ((st = check_launch("W K-tile staging (bf16)"))) return st;
+      g.B = wt; g.rows_b = static_cast<int>(npad); g.b_tiled = 1;
+    }
     g.seg[0] = W4Seg{static_cast<uint16_t*>(dx), static_cast<int>(lddx), static_cast<int>(n), w4_tiles(n)};
     g.seg[1] = W4Seg{static_cast<uint16_t*>(dx), static_cast<int>(lddx), 0, 0};
     g.tiles_n = g.seg[0].tiles;
@@ -658,7 +678,12 @@ size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t coun
     if (m[j] < 1 || r[j] < 1) return 0;
   // the one-launch plan, or compact_bwd on each slice when it does not apply
   size_t need = ghat_group_plan(tokens, count, r, m).bytes;
-  for (int j = 0; j < count; ++j) need = std::max(need, ghat_ws_bytes(tokens, r[j], m[j]));
+  int64_t msum = 0;
+  for (int j = 0; j < count; ++j) {
+    need = std::max(need, ghat_ws_bytes(tokens, r[j], m[j]));
+    msum += m[j];
+  }
+  if (n >= 1) need = std::max(need, dx_stage_bytes(n, msum));  // the dx GEMM's copy of W
   return need + kWsAlign;
 }
 
@@ -693,8 +718,8 @@ int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, 
   }
   // dL/dx summed over the projections: one GEMM over the concatenated weight
   if (dx != nullptr) {
-    if ((st = compact_bwd(dy, lddy, W, ldw, nullptr, ldz, dx, lddx, nullptr, tokens, n, msum, 1, dtype, nullptr,
-                          0, stream)))
+    if ((st = compact_bwd(dy, lddy, W, ldw, nullptr, ldz, dx, lddx, nullptr, tokens, n, msum, 1, dtype, ws,
+                          ws_bytes, stream)))
       return st;
   }
   if (G == nullptr) return ok();

@@ -53,7 +53,8 @@
 // the same check, column pairs past the last column are steered out of range.
 // Requirements (checked by the host): K % 8 == 0, K >= 320, every output
 // column count even, 256 * ld * 2 + 2 K < 2^31 for every matrix, lda and
-// ldb multiples of 8 (16-byte chunks).
+// ldb multiples of 8 (16-byte chunks); for a K-tiled B (below) the whole
+// operand below 2^31 bytes.
 #pragma once
 #include "common.hpp"
 
@@ -80,11 +81,19 @@ struct W4Seg {
   int tiles;    // ceil(cols / 256)
 };
 
+// B layouts.  Row-major: row R, element k at B[R * ldb + k].  K-tiled
+// (b_tiled != 0): the 32-element K tiles of all rows_b rows follow each other,
+// element (R, k) at B[((k / 32) * rows_b + R) * 32 + k % 32], so that the 16
+// rows one copy instruction fetches are 1 KB of contiguous memory (whole cache
+// lines) instead of 16 separate 64-byte row pieces; rows_b is then a multiple
+// of 256 and ceil(K / 32) * rows_b * 64 < 2^31.  Operands that this library
+// stages itself use it.
 struct W4Gemm {
   const uint16_t* A;  // [M][lda]
   int lda, M, K;
-  const uint16_t* B;  // [rows_b][ldb]
+  const uint16_t* B;  // [rows_b][ldb], or K-tiled
   int ldb, rows_b;
+  int b_tiled;
   W4Seg seg[2];       // seg[1].tiles == 0 when unused
   int tiles_n;        // seg[0].tiles + seg[1].tiles
   int tiles;          // ceil(M / 256) * tiles_n
@@ -174,6 +183,7 @@ struct W4Lane {
   uint32_t lds;             // dynamic LDS base
   int va[4], vb[4];         // A and B copy offsets (k = 0) of blocks 4 wave + q
   int kchunk;               // 8 * logical chunk this lane copies
+  int ksb;                  // bytes the B offsets advance per element of k0
 };
 
 // Fragment chunk of lane `lane` for step kk (0, 1), fragment 0, stage 0, in a
@@ -208,8 +218,9 @@ __device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
   for (int q = 0; q < 4; ++q) {
     const int j = L.wave * 4 + q;
     L.va[q] = w4_copy_off(g.lda, L.lane, j, L.kchunk);
-    L.vb[q] = w4_copy_off(g.ldb, L.lane, j, L.kchunk);
+    L.vb[q] = w4_copy_off(g.b_tiled ? 32 : g.ldb, L.lane, j, L.kchunk);
   }
+  L.ksb = g.b_tiled ? 2 * g.rows_b : 2;
   return L;
 }
 
@@ -273,7 +284,10 @@ __device__ __forceinline__ W4CopyDesc w4_copy_desc(const W4Gemm& g, const W4Curs
   const int64_t row0 = static_cast<int64_t>(c.rt) * kW4Tile;
   const int64_t brow0 = static_cast<int64_t>(c.ct) * kW4Tile;
   d.ra = w4_rsrc(g.A + row0 * g.lda, live ? (g.M - row0) * int64_t(g.lda) * 2 : 0);
-  d.rb = w4_rsrc(g.B + brow0 * g.ldb, live ? (g.rows_b - brow0) * int64_t(g.ldb) * 2 : 0);
+  if (g.b_tiled)
+    d.rb = w4_rsrc(g.B + brow0 * 32, live ? (ceil_div(g.K, kW4K) * g.rows_b - brow0) * 64 : 0);
+  else
+    d.rb = w4_rsrc(g.B + brow0 * g.ldb, live ? (g.rows_b - brow0) * int64_t(g.ldb) * 2 : 0);
   return d;
 }
 
@@ -293,7 +307,7 @@ __device__ __forceinline__ void w4_copy(const W4Gemm& g, const W4Lane& L, const 
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t vo = static_cast<uint32_t>(L.vb[q] + 2 * k0) | oob;
+    const uint32_t vo = static_cast<uint32_t>(L.vb[q] + L.ksb * k0) | oob;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         d.rb, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(sb + (L.wave * 4 + q) * 1024u)), 16,
         static_cast<int>(vo), 0, 0, 0);
@@ -403,7 +417,7 @@ __device__ __forceinline__ void w4_copy_one(const W4Lane& L, const W4CopyCursor&
                                             int k3, uint32_t s3) {
   const int q = c & 3;
   const bool is_a = c < 4;
-  const uint32_t vo = static_cast<uint32_t>((is_a ? L.va[q] : L.vb[q]) + 2 * k3) | oob;
+  const uint32_t vo = static_cast<uint32_t>(is_a ? L.va[q] + 2 * k3 : L.vb[q] + L.ksb * k3) | oob;
   const uint32_t dst = L.lds + (is_a ? 0u : static_cast<uint32_t>(kW4BBase)) + s3 + (L.wave * 4 + q) * 1024u;
   __builtin_amdgcn_raw_ptr_buffer_load_lds(is_a ? cc.d.ra : cc.d.rb,
                                            reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,

@@ -72,17 +72,18 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
 __global__ void k_pstream_t_bf16(ProjDesc d, PhiloxKey key, int64_t n, float scale, uint16_t* out, int64_t ld) {
   const int64_t u = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (u >= proj_t_units(d.kind, d.r, ld)) return;
-  proj_t_unit(d, key, n, scale, out, ld, u);
+  proj_t_unit(d, key, n, scale, PanelOut{out, ld, 0}, 0, ld, u);
 }
 
-// out[c * ldo + i] = in[i * ldi + c] for i < rows, c < cols (bf16), through a
-// 64 x 64 LDS tile.  256 threads; each moves two 16-byte chunks: loads 8
-// consecutive columns of one row, scatters them down the transposed tile, and
-// stores 8 consecutive rows of one output row.  ldi and ldo are multiples of 8
-// and both pointers 16-byte aligned; partial chunks at the edges go element
-// by element.
+// Element (c, i) of `out` = in[i * ldi + c] for i < rows, c < cols (bf16),
+// through a 64 x 64 LDS tile.  256 threads; each moves two 16-byte chunks:
+// loads 8 consecutive columns of one row, scatters them down the transposed
+// tile, and stores 8 consecutive rows of one output row (one 16-byte store:
+// 8-aligned runs of k stay inside a 32-wide K tile of a K-tiled panel).  ldi
+// and the panel's ld are multiples of 8 and both pointers 16-byte aligned;
+// partial chunks at the edges go element by element.
 __device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t ldi, int64_t rows, int64_t cols,
-                                                    uint16_t* out, int64_t ldo, int tiles_c, int block) {
+                                                    const PanelOut& out, int tiles_c, int block) {
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];  // tile[c][i]; rows padded to 144 bytes
   const int t = threadIdx.x;
   const int64_t r0 = static_cast<int64_t>(block / tiles_c) * 64;
@@ -114,9 +115,10 @@ __device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t 
     if (gc >= cols) continue;
     const u32x4 w = *reinterpret_cast<const u32x4*>(&tile[c][ii]);
     if (gi + 8 <= rows) {
-      *reinterpret_cast<u32x4*>(out + gc * ldo + gi) = w;
+      *reinterpret_cast<u32x4*>(panel_at(out, gc, gi)) = w;
     } else {
-      for (int e = 0; e < 8 && gi + e < rows; ++e) out[gc * ldo + gi + e] = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
+      for (int e = 0; e < 8 && gi + e < rows; ++e)
+        *panel_at(out, gc, gi + e) = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
     }
   }
 }
@@ -132,8 +134,8 @@ constexpr int kMaxGroup = 8;  // projections sharing one input
 struct FwdStage {
   const uint16_t* W;
   int64_t ldw, n, m;      // W [n x m]; m = the sum of the projections' widths
-  uint16_t* b;            // staged operand, rows of ldb elements: W^T in rows 0 .. m-1
-  int64_t ldb;
+  PanelOut b;             // staged operand (K-tiled): W^T in rows 0 .. m-1
+  int64_t ldb;            // its K extent (a multiple of 32)
   int count;
   int kind, sparse_s;     // projection kind and draws per row (sparse)
   int tiles_c;            // ceil(m / 64)
@@ -151,11 +153,24 @@ __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
     while (j + 1 < a.count && a.pt_begin[j + 1] <= b) ++j;
     const int64_t u = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
     if (u >= proj_t_units(a.kind, a.r[j], a.ldb)) return;
-    proj_t_unit(ProjDesc{a.kind, static_cast<int>(a.r[j]), a.sparse_s}, a.key[j], a.n, a.pscale[j],
-                a.b + a.row_off[j] * a.ldb, a.ldb, u);
+    proj_t_unit(ProjDesc{a.kind, static_cast<int>(a.r[j]), a.sparse_s}, a.key[j], a.n, a.pscale[j], a.b,
+                a.row_off[j], a.ldb, u);
   } else {
-    transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.b, a.ldb, a.tiles_c, b - a.pt_begin[a.count]);
+    transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.b, a.tiles_c, b - a.pt_begin[a.count]);
   }
+}
+
+// The dx GEMM's B operand, W [n x m] (row R = input feature, K = m), copied
+// into the K-tiled layout: element (R, k) of `out` = W[R * ldw + k] for R < n,
+// k < m.  One thread per 8 consecutive k of one row (m % 8 == 0): a 16-byte
+// load and a 16-byte store.
+__global__ __launch_bounds__(256) void k_stage_rows_bf16(const uint16_t* W, int64_t ldw, int64_t n, int64_t m,
+                                                         PanelOut out) {
+  const int64_t kq = m / 8;
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (u >= n * kq) return;
+  const int64_t row = u / kq, k = (u - row * kq) * 8;
+  *reinterpret_cast<u32x4*>(panel_at(out, row, k)) = *reinterpret_cast<const u32x4*>(W + row * ldw + k);
 }
 
 // Unscaled fp32 stream of any projection (n x r, leading dimension ld), one

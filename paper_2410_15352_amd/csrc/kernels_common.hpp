@@ -113,11 +113,23 @@ __host__ __device__ inline int adam_blocks(int64_t r, int64_t m) {
   return static_cast<int>(b < 1 ? 1 : b);
 }
 
-// One quad of a P^T panel: out[j * ld + i0 .. i0 + 3] = bf16(scale x the
-// unscaled stream elements (i0 .. i0 + 3, j)) (scale 1 for the identity); rows
-// i >= n are written as zero.
+// Where a staged bf16 panel keeps element (row, k): row-major p[row * ld + k]
+// (kblk == 0), or K-tiled p[((k / 32) * kblk + row) * 32 + k % 32], the layout
+// of the persistent GEMM's K-tiled B operand (kblk = its row count).
+struct PanelOut {
+  uint16_t* p;
+  int64_t ld, kblk;
+};
+
+__device__ __forceinline__ uint16_t* panel_at(const PanelOut& o, int64_t row, int64_t k) {
+  return o.kblk ? o.p + (((k >> 5) * o.kblk + row) << 5) + (k & 31) : o.p + row * o.ld + k;
+}
+
+// One quad of a P^T panel: element (row0 + j, i0 .. i0 + 3) of `out` = bf16(scale
+// x the unscaled stream elements (i0 .. i0 + 3, j)) (scale 1 for the identity);
+// rows i >= n are written as zero.
 __device__ __forceinline__ void pstream_t_quad(const ProjDesc& d, PhiloxKey key, int64_t n, float scale,
-                                               uint16_t* out, int64_t ld, int64_t j, int64_t i0) {
+                                               const PanelOut& out, int64_t row0, int64_t j, int64_t i0) {
   float g[4] = {0.f, 0.f, 0.f, 0.f};
   if (i0 < n) {
     proj_quad(d, key, i0, j, g);
@@ -129,7 +141,7 @@ __device__ __forceinline__ void pstream_t_quad(const ProjDesc& d, PhiloxKey key,
   u32x2 v;
   v.x = pack_bf16x2(g[0], g[1]);
   v.y = pack_bf16x2(g[2], g[3]);
-  *reinterpret_cast<u32x2*>(out + j * ld + i0) = v;
+  *reinterpret_cast<u32x2*>(panel_at(out, row0 + j, i0)) = v;
 }
 
 // Work units of a P^T panel [r][ld]: a quad (four rows i of one column j)
@@ -142,13 +154,14 @@ __host__ __device__ inline int64_t proj_t_units(int kind, int64_t r, int64_t ld)
   return kind == kProjSparse ? ld * ceil_div(r, kSjltChunk) : (ld / 4) * r;
 }
 
-// Unit u of a P^T panel: out[j * ld + i] = bf16(scale x stream element (i, j))
-// (scale 1 for the identity); rows i >= n are written as zero.
-__device__ __forceinline__ void proj_t_unit(const ProjDesc& d, PhiloxKey key, int64_t n, float scale, uint16_t* out,
-                                            int64_t ld, int64_t u) {
+// Unit u of a P^T panel: element (row0 + j, i) of `out` = bf16(scale x stream
+// element (i, j)) (scale 1 for the identity) for i < ld (the panel's K extent);
+// rows i >= n are written as zero.
+__device__ __forceinline__ void proj_t_unit(const ProjDesc& d, PhiloxKey key, int64_t n, float scale,
+                                            const PanelOut& out, int64_t row0, int64_t ld, int64_t u) {
   if (d.kind != kProjSparse) {
     const int64_t qpr = ld / 4;
-    pstream_t_quad(d, key, n, scale, out, ld, u / qpr, (u % qpr) * 4);
+    pstream_t_quad(d, key, n, scale, out, row0, u / qpr, (u % qpr) * 4);
     return;
   }
   const int64_t i = u % ld, c0 = (u / ld) * kSjltChunk;
@@ -173,7 +186,7 @@ __device__ __forceinline__ void proj_t_unit(const ProjDesc& d, PhiloxKey key, in
   }
 #pragma unroll
   for (int k = 0; k < kSjltChunk; ++k)
-    if (c0 + k < d.r) out[(c0 + k) * ld + i] = f32_to_bf16(acc[k] * scale);
+    if (c0 + k < d.r) *panel_at(out, row0 + c0 + k, i) = f32_to_bf16(acc[k] * scale);
 }
 
 // P^T workgroups of a layer: one unit per thread.
@@ -204,7 +217,7 @@ __global__ void k_adam_pt_batched(StepBatch s) {
     const AdamLayer& p = s.layer[l];
     const int64_t u = static_cast<int64_t>(idx - s.pt_begin[l]) * blockDim.x + threadIdx.x;
     if (u >= proj_t_units(s.c.kind, p.r, p.ldpt)) return;
-    proj_t_unit(ProjDesc{s.c.kind, p.r, s.c.sparse_s}, p.key, p.n, 1.0f, p.pt, p.ldpt, u);
+    proj_t_unit(ProjDesc{s.c.kind, p.r, s.c.sparse_s}, p.key, p.n, 1.0f, PanelOut{p.pt, p.ldpt, 0}, 0, p.ldpt, u);
   }
 }
 

@@ -53,6 +53,8 @@ def test_forward_parity(shape, use_ws):
     y = empty(T, m, dt, ld_for(m, dt))
     z = empty(T, r, dt, ld_for(r, dt))
     ws = workspace(cp.fwd_workspace_bytes(n, m, r, CODE[dt])) if use_ws else None
+    if ws is not None:
+        ws.fill_(0xFF)  # stale bytes (NaN patterns) in unwritten padding must not reach y or z
     cp.compact_fwd(xd, Wd, y, z, seed, ws=ws)
     torch.cuda.synchronize()
     y_ref, z_ref = oc.ref_fwd(x, W, seed, r)
@@ -75,6 +77,25 @@ def test_backward_parity(shape):
     dx_ref, G_ref = oc.ref_bwd(dy, z, W)
     assert oc.rel_fro(to_np(dx), dx_ref) <= TOL[dt]
     assert oc.rel_fro(G.cpu().numpy(), G_ref) <= TOL[dt]
+
+
+@pytest.mark.parametrize("shape", [s for s in SHAPES if s[4] == "bf16"], ids=_ids)
+def test_dx_staged_weight_bitwise(shape):
+    # with a workspace the dx GEMM reads a K-tiled copy of W, without one W
+    # itself: the same products in the same order, so dx is bitwise equal
+    T, n, m, r, dt = shape
+    dy, _, W = bwd_inputs(T, n, m, r, dt, data_seed=2 * T + m)
+    dyd, Wd = to_dev(dy, dt, ld_for(m, dt)), to_dev(W, dt, ld_for(m, dt))
+    dx0 = empty(T, n, dt, ld_for(n, dt), fill=1.0)
+    dx1 = empty(T, n, dt, ld_for(n, dt), fill=2.0)
+    cp.compact_bwd(dyd, Wd, None, dx0, None)
+    ws = workspace(cp.bwd_workspace_bytes(T, n, m, r, CODE[dt]))
+    ws.fill_(0xFF)  # stale bytes (NaN patterns) in the padding rows must not reach dx
+    cp.compact_bwd(dyd, Wd, None, dx1, None, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(dx0.view(torch.int16), dx1.view(torch.int16))
+    dx_ref, _ = oc.ref_bwd(dy, np.zeros((T, r)), W)
+    assert oc.rel_fro(to_np(dx1), dx_ref) <= TOL[dt]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=_ids)
