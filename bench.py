@@ -29,6 +29,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+from synthetic import input_groups  # noqa: E402  (layers that share an input)
+
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fwd_traffic.json")
@@ -72,27 +74,6 @@ def kernel_source_hash():
             h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()[:16]
-
-
-GROUPABLE = (("q", "k", "v"), ("gate", "up"))
-
-
-def input_groups(wl, grouped=True):
-    """Lists of layer indices that read the same input: q, k, v and gate, up of
-    one block (when grouped), every other layer on its own."""
-    out, i, L = [], 0, wl.layers
-    while i < len(L):
-        g = [i]
-        if grouped:
-            for names in GROUPABLE:
-                k = len(names)
-                if (tuple(x.name for x in L[i:i + k]) == names and
-                        all(x.block == L[i].block and x.n == L[i].n for x in L[i:i + k])):
-                    g = list(range(i, i + k))
-                    break
-        out.append(g)
-        i += len(g)
-    return out
 
 
 class Model:
@@ -477,7 +458,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": wl.description, "tokens_per_step": T, "layers": nl,
-                   "input_groups": "q,k,v and gate,up share their input" if not args.no_group else "none",
+                   "input_groups": ("q,k,v and gate,up share their input (gate,up only when their width is a "
+                                    "multiple of 8)") if not args.no_group else "none",
                    "fwd_mode": args.fwd_mode, "projection": args.proj, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -140,6 +140,33 @@ class _SeedOverride(Linear):
         return self.seed_value
 
 
+# Projections that read the same input in the model (Table 7: q, k, v read
+# the normed block input, gate and up the normed attention output).
+GROUPABLE = (("q", "k", "v"), ("gate", "up"))
+
+
+def input_groups(wl, grouped=True):
+    """Lists of layer indices that read the same input and run as one group:
+    q, k, v and gate, up of one block (when grouped and the group's column
+    slices start on 16-byte boundaries: every width and rank but the last a
+    multiple of 8), every other layer on its own."""
+    out, i, L = [], 0, wl.layers
+    while i < len(L):
+        g = [i]
+        if grouped:
+            for names in GROUPABLE:
+                k = len(names)
+                cand = L[i:i + k]
+                if (tuple(x.name for x in cand) == names and
+                        all(x.block == L[i].block and x.n == L[i].n for x in cand) and
+                        all(x.m % 8 == 0 and x.r % 8 == 0 for x in cand[:-1])):
+                    g = list(range(i, i + k))
+                    break
+        out.append(g)
+        i += len(g)
+    return out
+
+
 WORKLOAD_NAMES = ("single-f32", "llama-60m", "roberta-base", "llama-350m",
                   "llama-1b-r4", "llama-1b-r8")
 

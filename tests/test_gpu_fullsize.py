@@ -1,13 +1,17 @@
-"""Parity at the benchmark's full sizes: LLaMA-350M shapes and 65536 tokens, in
-the launch configuration the benchmark times.  q|k|v and gate|up run as input
+"""Parity at the benchmark's full sizes (LLaMA-350M shapes and 65536 tokens, and
+the other workloads' shapes at their token counts), in the launch configuration
+the benchmark times.  q|k|v and gate|up run as input
 groups (compact_fwd_group with its workspace: one staged operand, one
 persistent GEMM); o and down run alone; the backward of each group is one
 compact_bwd_group call (dL/dx over the concatenated weight, every G^_j of the
 group in one split-K launch); Alg. 3 runs for all 168 layers in one
 compact_step_batched call on column slices of the group weights.
 
-The oracle computes sampled outputs directly from the same seeded inputs (it
-never sees a GPU value): rows of y, z and dL/dx for sampled tokens (the last
+Every distinct input group of every bf16 workload is covered the same way
+(LLaMA-60M, RoBERTa-Base, LLaMA-1B at r = n/4 and n/8 too, each at its full
+token count; LLaMA-1B's gate and up run apart, their width 5461 not being a
+multiple of 8).  The oracle computes sampled outputs directly from the same
+seeded inputs (it never sees a GPU value): rows of y, z and dL/dx for sampled tokens (the last
 token always among them), columns of G^ as sums over all 65536 tokens, and
 columns of the updated W, M and V (the last column always among them).
 """
@@ -26,15 +30,31 @@ torch = pytest.importorskip("torch")
 cp = pytest.importorskip("paper_2410_15352_amd")
 
 TOL = 2e-2
-T = 65536
 
-# the four input groups of a LLaMA-350M block: n, widths m, ranks r
-KINDS = {
-    "qkv": (1024, (1024, 1024, 1024), (128, 128, 128)),
-    "o": (1024, (1024,), (128,)),
-    "gate_up": (1024, (2736, 2736), (128, 128)),
-    "down": (2736, (1024,), (342,)),
-}
+
+def _distinct_groups():
+    """(workload, tokens, n, widths, ranks, seeds) of every distinct input group
+    of the bf16 workloads, as the benchmark forms them (synthetic.input_groups)."""
+    from synthetic import input_groups
+    cases = []
+    for name in ("llama-60m", "roberta-base", "llama-350m", "llama-1b-r4", "llama-1b-r8"):
+        wl = workload(name)
+        seen = set()
+        for g in input_groups(wl):
+            Ls = [wl.layers[i] for i in g]
+            key = (Ls[0].n, tuple(L.m for L in Ls), tuple(L.r for L in Ls))
+            if key in seen:
+                continue
+            seen.add(key)
+            cases.append((name, wl.tokens, key[0], key[1], key[2], tuple(L.seed for L in Ls)))
+    return cases
+
+
+CASES = _distinct_groups()
+
+
+def _case_id(c):
+    return "{}-n{}-m{}-r{}".format(c[0], c[2], "+".join(map(str, c[3])), "+".join(map(str, c[4])))
 
 
 def _rows(t, idx):
@@ -47,11 +67,10 @@ def _sample(rng, size, k):
     return s
 
 
-@pytest.mark.parametrize("kind", list(KINDS))
-def test_full_size_forward_backward(kind):
-    n, ms, rs = KINDS[kind]
+@pytest.mark.parametrize("case", CASES, ids=_case_id)
+def test_full_size_forward_backward(case):
+    _, T, n, ms, rs, seeds = case
     M, R = sum(ms), sum(rs)
-    seeds = [((k + 1) << 32) | 5 for k in range(len(ms))]
     x = normal_bf16_blocked(T, n, seed=1000 + n)
     Ws = [normal_bf16_blocked(n, m, seed=2000 + 10 * k + n, scale=0.02) for k, m in enumerate(ms)]
     dy = normal_bf16_blocked(T, M, seed=3000 + M, scale=0.01)
