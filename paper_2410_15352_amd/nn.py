@@ -17,7 +17,7 @@ from __future__ import annotations
 
 import torch
 
-from . import (bwd_workspace_bytes, compact_bwd, compact_fwd, compact_fwd_group, compact_next_seed,
+from . import (bwd_group_workspace_bytes, compact_bwd_group, compact_fwd, compact_fwd_group, compact_next_seed,
                compact_step_batched, fwd_group_workspace_bytes, fwd_workspace_bytes, prepare_layers,
                step_batched_workspace_bytes)
 
@@ -91,17 +91,14 @@ class _GroupFn(torch.autograd.Function):
         dx = None
         if ctx.needs_input_grad[0]:
             dx = _empty2d(T, mod.n, torch.bfloat16, dy.device)
-            compact_bwd(dy, mod.weight, None, dx, None)  # sum over the group's projections
-        ws = WorkspacePool.get(dy.device, "bwd", max(bwd_workspace_bytes(T, mod.n, m, r)
-                                                     for m, r in zip(mod.ms, mod.rs)))
-        mo = ro = 0
-        for j, (m, r) in enumerate(zip(mod.ms, mod.rs)):
-            target = mod.ghat[j] if not mod.grad_ready else torch.empty_like(mod.ghat[j])
-            compact_bwd(dy[:, mo:mo + m], None, z[:, ro:ro + r], None, target, ws=ws)
-            if mod.grad_ready:
-                mod.ghat[j].add_(target)  # gradient accumulation: G^ is linear in dL/do
-            mo += m
-            ro += r
+        # Alg. 2 for the whole group in one call: dL/dx summed over the
+        # projections (one GEMM over the concatenated weight) and every G^_j
+        targets = [g if not mod.grad_ready else torch.empty_like(g) for g in mod.ghat]
+        ws = WorkspacePool.get(dy.device, "bwd", bwd_group_workspace_bytes(T, mod.n, mod.ms, mod.rs))
+        compact_bwd_group(dy, mod.weight if dx is not None else None, z, dx, targets, mod.ms, mod.rs, ws=ws)
+        if mod.grad_ready:
+            for g, t in zip(mod.ghat, targets):
+                g.add_(t)  # gradient accumulation: G^ is linear in dL/do
         mod.grad_ready = True
         return dx, None, None
 

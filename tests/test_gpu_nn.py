@@ -1,7 +1,7 @@
 """GPU checks of the PyTorch modules over the ABI (paper_2410_15352_amd.nn).
 
 * CompActLinear / CompActGroup: the forward is bitwise the ABI's compact_fwd /
-  compact_fwd_group; the backward's dL/dx and G^ are bitwise compact_bwd's;
+  compact_fwd_group; the backward's dL/dx and G^ are bitwise compact_bwd_group's;
   the only tensor autograd keeps for a layer is z (T x sum r, Alg. 1); a
   second backward before zero_grad accumulates G^; G^ is formed also when the
   input needs no gradient (a first layer).
@@ -87,20 +87,15 @@ def test_module_equals_abi(shape):
         cp.compact_fwd_group(x0, W, y1, z1, ms, rs, seeds,
                              ws=cnn.WorkspacePool.get(dev(), "t", cp.fwd_group_workspace_bytes(n, ms, rs)))
     dx1 = torch.empty(T, n, dtype=torch.bfloat16, device=dev())
-    cp.compact_bwd(dy, W, None, dx1, None)
+    Gs = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dy, W, z1, dx1, Gs, ms, rs,
+                         ws=cnn.WorkspacePool.get(dev(), "t", cp.bwd_group_workspace_bytes(T, n, ms, rs)))
     torch.cuda.synchronize()
     assert torch.equal(_bits(y), _bits(y1))
     assert torch.equal(_bits(saved[0]), _bits(z1))
     assert torch.equal(_bits(x.grad), _bits(dx1))
-    mo = ro = 0
-    for j, (m, r) in enumerate(zip(ms, rs)):
-        G = torch.empty(r, m, dtype=torch.float32, device=dev())
-        cp.compact_bwd(dy[:, mo:mo + m], None, z1[:, ro:ro + r], None, G,
-                       ws=cnn.WorkspacePool.get(dev(), "t", cp.bwd_workspace_bytes(T, n, m, r)))
-        torch.cuda.synchronize()
-        assert torch.equal(mod.ghat[j], G)
-        mo += m
-        ro += r
+    for j in range(len(ms)):
+        assert torch.equal(mod.ghat[j], Gs[j])
 
 
 def test_gradient_accumulation_and_zero_grad():
