@@ -6,9 +6,11 @@
 // W loads in flight, not to run the MFMA pipes hard.
 //
 // Each workgroup computes one 128 x 128 tile of W.  The read-modify-write of W
-// is done on the accumulators in registers (no LDS): one DPP swap between
-// adjacent lanes turns the MFMA output layout into bf16 pairs of two columns,
-// and each access instruction covers four 64-byte row segments.
+// is done on the accumulators in registers (no LDS).  bf16 W: an 8 x 8
+// transpose across lanes (DPP) turns the MFMA output layout into rows, so that
+// each lane reads and writes 8 consecutive columns (one 16-byte access; 8 loads
+// and 8 stores per lane and tile instead of 32 + 32).  fp32 W: one DPP swap
+// between adjacent lanes gives pairs of two columns.
 //
 // Workgroup: 4 waves, each 64 (columns of W) x 64 (rows of W) = 2 x 2 MFMA
 // 32x32x16 fragments.  Both operands are K-row major (N [r][m], P^T [r][n]); they
@@ -67,6 +69,40 @@ __device__ __forceinline__ void dec_wait_frags(u32x4 (&fa)[2], u32x4 (&fb)[2]) {
   asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(fa[0]), "+v"(fa[1]), "+v"(fb[0]), "+v"(fb[1]));
 }
 
+// 8 x 8 transpose of fp32 values across the 8 lanes of each lane group: on
+// exit lane t of a group holds in x[u] what lane u held in x[t] on entry.
+// Three exchanges of a lane bit with an element bit: xor 1 and xor 2 lanes by
+// quad permutes, xor 4 by row shifts of 4 with bank masks (4-lane banks).
+// one exchange of lane bit log2(D) with element bit log2(D) (D = 1, 2) by a
+// quad permute (QP: quad_perm 1,0,3,2 or 2,3,0,1)
+template <int D, int QP>
+__device__ __forceinline__ void dec_xchg(float (&x)[8], int lane) {
+  const bool hi = (lane & D) != 0;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    if (p & D) continue;
+    const float snd = hi ? x[p] : x[p | D];
+    const float rcv = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(snd), QP, 0xF, 0xF, false));
+    x[p] = hi ? rcv : x[p];
+    x[p | D] = hi ? x[p | D] : rcv;
+  }
+}
+
+__device__ __forceinline__ void dec_transpose8(float (&x)[8], int lane) {
+  dec_xchg<1, 0xB1>(x, lane);
+  dec_xchg<2, 0x4E>(x, lane);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const float keep = x[p];
+    // lanes 4-7 of each 8 take the partner's x[p + 4] into x[p] (row_shr:4),
+    // lanes 0-3 the partner's x[p] into x[p + 4] (row_shl:4)
+    x[p] = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x[p]), __float_as_int(x[p + 4]), 0x114, 0xF, 0xA,
+                                                      false));
+    x[p + 4] = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x[p + 4]), __float_as_int(keep), 0x104, 0xF,
+                                                          0x5, false));
+  }
+}
+
 template <bool WF32>
 __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
   typedef typename std::conditional<WF32, u32x2, uint32_t>::type WVec;
@@ -113,21 +149,37 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
                                             view_bytes(p.n, p.m, p.ldw, i0, c0, kEsz));
   const int odd = lane & 1;
   const int row_l = wi * 64 + 4 * (lane >> 5) + 2 * odd, col_l = wc * 64 + (lane & 30);
+  // bf16 W in rows: lane (l / 32, c = (l % 32) / 8, t = l % 8) holds, for block
+  // (b, a) and half s, row wi 64 + 32 b + 16 s + 8 (t / 4) + 4 (l / 32) + t % 4
+  // and the 8 columns wc 64 + 32 a + 8 c .. + 7 (one 16-byte access); the
+  // accumulators reach that layout through an 8 x 8 transpose across lanes
+  const int tr = lane & 7, row_r = wi * 64 + 8 * (tr >> 2) + 4 * (lane >> 5) + (tr & 3);
+  const int col_r = wc * 64 + 8 * ((lane & 31) >> 3);
   WVec wv[2][2][4][2];
+  u32x4 wr[2][2][2];
+  if constexpr (WF32) {
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int off = ((row_l + b * 32 + 8 * g + q) * p.ldw + col_l + a * 32) * kEsz;
-          if constexpr (WF32)
+          for (int q = 0; q < 2; ++q) {
+            const int off = ((row_l + b * 32 + 8 * g + q) * p.ldw + col_l + a * 32) * kEsz;
             wv[b][a][g][q] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rw, off, 0, 0));
-          else
-            wv[b][a][g][q] = __builtin_amdgcn_raw_buffer_load_b32(rw, off, 0, 0);
+          }
+  } else {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int sh = 0; sh < 2; ++sh) {
+          const int off = ((row_r + b * 32 + 16 * sh) * p.ldw + col_r + a * 32) * 2;
+          wr[b][a][sh] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rw, off, 0, 0));
         }
+  }
 
   f32x16 acc[2][2];  // [b][a]
   const f32x16 zero = {};
@@ -137,11 +189,12 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
     for (int a = 0; a < 2; ++a) acc[b][a] = zero;
   for (int t = 0; t < kt; ++t) {
     // this wave's copies of K step t have landed (later VMEM operations: the
-    // copies of the next 4 K steps and, before step 5, the 32 W loads); the
+    // copies of the next 4 K steps and, before step 5, the W loads: 32 for fp32
+    // W, 8 for bf16); the
     // barrier makes the whole stage visible and ends every wave's reads of
     // stage (t + 5) % 6 = (t - 1) % 6, which the next copies overwrite
     if (t < kDecAhead)
-      dec_wait_barrier<2 * (kDecAhead - 1) + 32>();
+      dec_wait_barrier<2 * (kDecAhead - 1) + (WF32 ? 32 : 8)>();
     else
       dec_wait_barrier<2 * (kDecAhead - 1)>();
     copy(t + kDecAhead);
@@ -162,6 +215,39 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
   // W <- W - coef acc, one rounding (RNE for bf16); columns past m not stored
   const float coef = p.coef;
   const int m_left = p.m - c0;
+  if constexpr (!WF32) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int sh = 0; sh < 2; ++sh) {
+          float x[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = coef * acc[b][a][8 * sh + e];
+          dec_transpose8(x, lane);  // x[u] = column col_r + 32 a + u of this lane's row
+          const u32x4 w = wr[b][a][sh];
+          u32x4 o;
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            o[k] = pack_bf16x2(__uint_as_float(w[k] << 16) - x[2 * k], __uint_as_float(w[k] & 0xFFFF0000u) - x[2 * k + 1]);
+          const int col = col_r + a * 32;
+          const int off = ((row_r + b * 32 + 16 * sh) * p.ldw + col) * 2;
+          if (col + 8 <= m_left) {
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(f32x4, o), rw, off, 0, 0);
+          } else if (col < m_left) {
+            // the tile's last columns: whole pairs, then a last single column
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+              if (col + 2 * k + 2 <= m_left)
+                __builtin_amdgcn_raw_buffer_store_b32(o[k], rw, off + 4 * k, 0, 0);
+              else if (col + 2 * k < m_left)
+                __builtin_amdgcn_raw_buffer_store_b16(static_cast<unsigned short>(o[k]), rw, off + 4 * k, 0, 0);
+            }
+          }
+        }
+    return;
+  }
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
