@@ -160,9 +160,12 @@ size_t compact_fwd_group_workspace_bytes(int64_t n, int32_t count, const int64_t
  *   G  [r x m] fp32, dense (ld = m): compressed weight gradient; may be NULL
  *                               to skip it (not both NULL)
  *   ws, ws_bytes  workspace of at least
- *         compact_bwd_workspace_bytes(tokens, n, m, r, dtype) bytes for the
- *         split-K partial sums of G^ (bf16 path; the sum over tokens is split
- *         and reduced in a fixed order, so G^ is deterministic).
+ *         compact_bwd_workspace_bytes(tokens, n, m, r, dtype) bytes (bf16
+ *         path), required when G is computed: it holds the split-K partial
+ *         sums of G^ (the sum over tokens is split and reduced in a fixed
+ *         order, so G^ is deterministic) and, before them, a K-tiled copy of W
+ *         that the dx GEMM reads (with NULL or a smaller workspace dx reads W
+ *         itself; dx is bitwise the same either way).
  */
 int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
                 int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
