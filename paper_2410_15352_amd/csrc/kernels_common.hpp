@@ -17,8 +17,10 @@ namespace compact {
 // stages, for each layer that needs it, the P^T panel of the decompression:
 // pt[j * ldpt + i] = bf16 of the unscaled stream element (i, j) (G, or S for
 // the sparse projection; zero for i >= n).  The two
-// jobs are independent; their workgroups alternate in the grid, so the
-// HBM-bound moment update and the VALU-bound P stream run side by side.
+// jobs are independent; the Adam workgroups are spread evenly over the whole
+// grid among the P^T workgroups (in proportion to their counts), so the
+// HBM-bound moment update and the VALU-bound P stream run side by side from
+// the first workgroup to the last.
 
 // Values shared by every layer of a step.
 struct AdamConsts {
@@ -196,17 +198,13 @@ __host__ __device__ inline int pt_blocks(int kind, int64_t r, int64_t ldpt) {
 
 __global__ void k_adam_pt_batched(StepBatch s) {
   const int na = s.adam_begin[s.count], np = s.pt_begin[s.count];
-  const int k = na < np ? na : np;
-  const int b = static_cast<int>(blockIdx.x);
-  bool adam;
-  int idx;
-  if (b < 2 * k) {
-    adam = (b & 1) == 0;
-    idx = b >> 1;
-  } else {
-    adam = na > np;
-    idx = b - k;
-  }
+  const int64_t total = static_cast<int64_t>(na) + np;
+  const int64_t b = blockIdx.x;
+  // Adam workgroups before grid position b: floor(b na / total); position b is
+  // an Adam workgroup where that count steps up
+  const int before = static_cast<int>(b * na / total);
+  const bool adam = static_cast<int>((b + 1) * na / total) > before;
+  const int idx = adam ? before : static_cast<int>(b) - before;
   if (adam) {
     const int l = batch_layer_of(s.adam_begin, s.count, idx);
     const int nb = s.adam_begin[l + 1] - s.adam_begin[l];

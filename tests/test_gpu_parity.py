@@ -243,8 +243,9 @@ def test_three_step_chain(name):
 
 
 def test_step_batched_equals_per_layer():
-    # the batched launch computes exactly what compact_step computes per layer
-    shapes = [(512, 512, 128), (512, 1376, 128), (1376, 512, 344), (300, 200, 40), (5461, 64, 1365)] * 4
+    # the batched launches compute exactly what compact_step computes per layer;
+    # 45 layers make two launch groups, so the two-stream schedule runs
+    shapes = [(512, 512, 128), (512, 1376, 128), (1376, 512, 344), (300, 200, 40), (5461, 64, 1365)] * 9
     layers_a, layers_b, states = [], [], []
     for i, (n, m, r) in enumerate(shapes):
         W, G, M, V = step_inputs(n, m, r, "bf16", t=2, data_seed=50 + i)
@@ -266,3 +267,49 @@ def test_step_batched_equals_per_layer():
     for La, Lb in zip(layers_a, layers_b):
         assert torch.equal(La["M"], Lb["M"]) and torch.equal(La["V"], Lb["V"])
         assert torch.equal(La["W"].view(torch.int16), Lb["W"].view(torch.int16))
+
+
+def test_step_batched_stream_order():
+    # on a caller's stream: work enqueued before the call (G, M, V, W set) is
+    # seen by every launch group, and work enqueued after it (clones) sees the
+    # finished step, with no host synchronisation in between
+    shapes = [(512, 512, 128), (512, 1376, 128), (1376, 512, 344)] * 30  # three launch groups
+    rng = np.random.default_rng(77)
+    s = torch.cuda.Stream()
+    layers, ref = [], []
+    for i, (n, m, r) in enumerate(shapes):
+        W, G, M, V = step_inputs(n, m, r, "bf16", t=3, data_seed=300 + i)
+        host = [torch.from_numpy(a.copy()).pin_memory() for a in (G, M, V)]
+        wh = to_dev(W, "bf16", ld_for(m, "bf16")).cpu().pin_memory()
+        layers.append(dict(W=torch.zeros(n, ld_for(m, "bf16"), dtype=torch.bfloat16, device=dev())[:, :m],
+                           G=torch.zeros(r, m, device=dev()), M=torch.zeros(r, m, device=dev()),
+                           V=torch.zeros(r, m, device=dev()), seed=((i + 3) << 32) | 1, alpha=0.5, host=host, wh=wh))
+        wr = to_dev(W, "bf16", ld_for(m, "bf16"))
+        gr, mr, vr = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+        ref.append(dict(W=wr, G=gr, M=mr, V=vr, seed=layers[-1]["seed"], alpha=0.5))
+    for L in ref:
+        n, m = L["W"].shape
+        ws1 = workspace(cp.step_workspace_bytes(n, m, L["G"].shape[0]))
+        cp.compact_step(L["W"], L["G"], L["M"], L["V"], L["seed"], 3, 1e-3, alpha=L["alpha"], ws=ws1)
+    torch.cuda.synchronize()
+    batch = [dict(W=L["W"], G=L["G"], M=L["M"], V=L["V"], seed=L["seed"], alpha=L["alpha"]) for L in layers]
+    ws = workspace(cp.step_batched_workspace_bytes(batch))
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        # a slow kernel first, so that a launch group not ordered after it would
+        # run before the copies below land
+        big = torch.empty(1 << 28, dtype=torch.uint8, device=dev())
+        for _ in range(4):
+            big.fill_(int(rng.integers(1, 255)))
+        for L in layers:
+            for d, h in zip((L["G"], L["M"], L["V"]), L["host"]):
+                d.copy_(h, non_blocking=True)
+            L["W"].copy_(L["wh"][:, :L["W"].shape[1]], non_blocking=True)
+        cp.compact_step_batched(batch, 3, 1e-3, ws=ws, stream=s.cuda_stream)
+        outs = [(L["W"].clone(), L["M"].clone(), L["V"].clone()) for L in layers]
+        for L in layers:  # overwritten right after the clones were taken
+            L["M"].fill_(0.0)
+    torch.cuda.synchronize()
+    for (w, m_, v), R in zip(outs, ref):
+        assert torch.equal(m_, R["M"]) and torch.equal(v, R["V"])
+        assert torch.equal(w.view(torch.int16), R["W"].view(torch.int16))
