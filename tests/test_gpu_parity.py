@@ -41,12 +41,13 @@ def _ids(s):
     return "T{}-n{}-m{}-r{}-{}".format(*s)
 
 
-@pytest.mark.parametrize("shape", SHAPES, ids=_ids)
-@pytest.mark.parametrize("use_ws", [True, False])
+# (shape, workspace): the fp32 path has no workspace mode
+FWD_CASES = [(s, ws) for s in SHAPES for ws in (True, False) if not (s[4] == "f32" and ws)]
+
+
+@pytest.mark.parametrize("shape,use_ws", FWD_CASES, ids=[f"{ws}-{_ids(s)}" for s, ws in FWD_CASES])
 def test_forward_parity(shape, use_ws):
     T, n, m, r, dt = shape
-    if dt == "f32" and use_ws:
-        pytest.skip("no workspace mode on the fp32 path")
     seed = (11 << 32) | 3
     x, W = fwd_inputs(T, n, m, dt, data_seed=T + n)
     xd, Wd = to_dev(x, dt, ld_for(n, dt)), to_dev(W, dt, ld_for(m, dt))
