@@ -314,3 +314,76 @@ def test_step_batched_stream_order():
     for (w, m_, v), R in zip(outs, ref):
         assert torch.equal(m_, R["M"]) and torch.equal(v, R["V"])
         assert torch.equal(w.view(torch.int16), R["W"].view(torch.int16))
+
+
+# degenerate sizes: rank 1, a single column, a single token, r = n, a wide n
+# with a narrow m; every path (forward, backward, step) on both dtypes
+TINY = [(1, 1, 1, 1), (3, 5, 2, 1), (7, 16, 1, 16), (40, 8, 3, 8), (2, 2048, 2, 1), (65, 33, 9, 7)]
+TINY_CASES = [(s + (dt,)) for s in TINY for dt in ("f32", "bf16")]
+
+
+@pytest.mark.parametrize("shape", TINY_CASES, ids=_ids)
+def test_degenerate_shapes(shape):
+    T, n, m, r, dt = shape
+    seed = (21 << 32) | 9
+    x, W = fwd_inputs(T, n, m, dt, data_seed=7 * T + n)
+    xd, Wd = to_dev(x, dt, ld_for(n, dt)), to_dev(W, dt, ld_for(m, dt))
+    y, z = empty(T, m, dt, ld_for(m, dt)), empty(T, r, dt, ld_for(r, dt))
+    fws = cp.fwd_workspace_bytes(n, m, r, CODE[dt])
+    cp.compact_fwd(xd, Wd, y, z, seed, ws=workspace(fws) if fws else None)
+    dy, _, _ = bwd_inputs(T, n, m, r, dt, data_seed=7 * T + m)
+    dyd = to_dev(dy, dt, ld_for(m, dt))
+    dx = empty(T, n, dt, ld_for(n, dt))
+    G = torch.empty(r, m, dtype=torch.float32, device=dev())
+    cp.compact_bwd(dyd, Wd, z, dx, G, ws=workspace(cp.bwd_workspace_bytes(T, n, m, r, CODE[dt])))
+    torch.cuda.synchronize()
+    y_ref, z_ref = oc.ref_fwd(x, W, seed, r)
+    assert oc.rel_fro(to_np(y), y_ref) <= TOL[dt]
+    assert oc.rel_fro(to_np(z), z_ref) <= TOL[dt]
+    dx_ref, G_ref = oc.ref_bwd(dy, to_np(z), W)
+    assert oc.rel_fro(to_np(dx), dx_ref) <= TOL[dt]
+    assert oc.rel_fro(G.cpu().numpy(), G_ref) <= TOL[dt]
+    # step (t = 3: smooth moments), fp32 master weights
+    t, lr, b1, b2, eps, alpha = 3, 1e-3, 0.9, 0.999, 1e-8, 0.5
+    W0, Gs, M, V = step_inputs(n, m, r, dt, t=t, data_seed=n + 3 * r)
+    Wm = to_dev(W0, "f32", ld_for(m, "f32"))
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (Gs, M, V))
+    cp.compact_step(Wm, Gd, Md, Vd, seed, t, lr, b1, b2, eps, alpha, dtype=dt,
+                    ws=workspace(cp.step_workspace_bytes(n, m, r, CODE[dt])))
+    torch.cuda.synchronize()
+    _, M_ref, V_ref, dW_ref = oc.ref_step(W0, Gs, M, V, seed, r, t, lr, b1, b2, eps, alpha)
+    assert oc.rel_fro(Md.cpu().numpy(), M_ref) <= TOL[dt]
+    assert oc.rel_fro(Vd.cpu().numpy(), V_ref) <= TOL[dt]
+    dW = to_np_f32(Wm).astype(np.float64) - W0.astype(np.float64)
+    assert oc.rel_fro(dW, dW_ref) <= (TOL[dt] if dt == "bf16" else 2e-4)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_zero_tokens(dt):
+    # an empty batch through the raw ABI (an empty torch view has no data
+    # pointer): the forward writes nothing, G^ (a sum over no tokens) is zero
+    n, m, r = 64, 48, 16
+    lib = cp.library()
+    stream = torch.cuda.current_stream().cuda_stream
+    x = empty(4, n, dt, ld_for(n, dt), fill=1.0)
+    _, W = fwd_inputs(4, n, m, dt, data_seed=3)
+    Wd = to_dev(W, dt, ld_for(m, dt))
+    y = empty(4, m, dt, ld_for(m, dt), fill=5.0)
+    z = empty(4, r, dt, ld_for(r, dt), fill=6.0)
+    fws = cp.fwd_workspace_bytes(n, m, r, CODE[dt])
+    wsf = workspace(fws)
+    st = lib.compact_fwd(x.data_ptr(), x.stride(0), Wd.data_ptr(), Wd.stride(0), y.data_ptr(), y.stride(0),
+                         z.data_ptr(), z.stride(0), 0, n, m, r, 7, 0, CODE[dt], wsf.data_ptr() if fws else None,
+                         fws, stream)
+    assert st == 0
+    G = torch.full((r, m), 3.0, dtype=torch.float32, device=dev())
+    dx = empty(4, n, dt, ld_for(n, dt), fill=8.0)
+    bws = cp.bwd_workspace_bytes(0, n, m, r, CODE[dt])
+    wsb = workspace(bws)
+    st = lib.compact_bwd(y.data_ptr(), y.stride(0), Wd.data_ptr(), Wd.stride(0), z.data_ptr(), z.stride(0),
+                         dx.data_ptr(), dx.stride(0), G.data_ptr(), 0, n, m, r, CODE[dt],
+                         wsb.data_ptr() if bws else None, bws, stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    assert float(G.abs().max()) == 0.0
+    assert bool((y.float() == 5.0).all()) and bool((z.float() == 6.0).all()) and bool((dx.float() == 8.0).all())
