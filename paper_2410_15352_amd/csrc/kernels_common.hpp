@@ -69,9 +69,11 @@ __device__ __forceinline__ void adam_range(const AdamLayer& p, const AdamConsts&
   if (p.m % 4 == 0) {
     for (int64_t q = first; q * 4 < total; q += stride) {
       const int64_t e = q * 4;
-      const f32x4 g = *reinterpret_cast<const f32x4*>(p.G + e);
-      const f32x4 mo = *reinterpret_cast<const f32x4*>(p.M + e);
-      const f32x4 vo = *reinterpret_cast<const f32x4*>(p.V + e);
+      // G, M and V are streamed once per step: non-temporal loads and stores (N,
+      // which the decompression reads next, is stored normally)
+      const f32x4 g = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p.G + e));
+      const f32x4 mo = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p.M + e));
+      const f32x4 vo = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p.V + e));
       f32x4 m1, v1, nv;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -81,8 +83,8 @@ __device__ __forceinline__ void adam_range(const AdamLayer& p, const AdamConsts&
         v1[i] = b;
         nv[i] = c;
       }
-      *reinterpret_cast<f32x4*>(p.M + e) = m1;
-      *reinterpret_cast<f32x4*>(p.V + e) = v1;
+      __builtin_nontemporal_store(m1, reinterpret_cast<f32x4*>(p.M + e));
+      __builtin_nontemporal_store(v1, reinterpret_cast<f32x4*>(p.V + e));
       const int64_t j = e / p.m, c = e - j * p.m;
       if (k.n_f32) {
         *reinterpret_cast<f32x4*>(static_cast<float*>(p.N) + j * p.ldn + c) = nv;
