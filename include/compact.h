@@ -54,7 +54,7 @@ typedef enum {
   COMPACT_OK = 0,
   COMPACT_EINVAL = -1,        /* bad size, pointer, rank or hyper-parameter */
   COMPACT_EALIGN = -2,        /* pointer or leading dimension misaligned    */
-  COMPACT_EUNSUPPORTED = -3,  /* valid request this build does not support  */
+  COMPACT_EUNSUPPORTED = -3,  /* valid request the library does not support */
   COMPACT_EWORKSPACE = -4,    /* workspace missing or too small             */
   COMPACT_EHIP = -5           /* a HIP runtime call or launch failed        */
 } compact_status;
