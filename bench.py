@@ -376,8 +376,9 @@ def model_sweep(args):
 def main():
     args = parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print(json.dumps({"error": "single-GPU build: this benchmark runs on exactly one GPU "
-                                   "(no collectives); rerun with --gpus 1"}), flush=True)
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU (the library has no "
+                                   "collectives; multi-GPU sharding is a design note only); rerun with --gpus 1"}),
+              flush=True)
         sys.exit(2)
     if args.model_sweep:
         return model_sweep(args)
