@@ -42,7 +42,7 @@ struct AdamLayer {
 };
 
 constexpr int kStepBatch = 40;  // layers per launch (kernel argument size)
-constexpr int kAdamVec = 1;     // float4 groups per thread
+constexpr int kAdamVec = 4;     // float4 groups per thread
 
 struct StepBatch {
   AdamConsts c;
