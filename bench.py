@@ -101,25 +101,51 @@ class Model:
         def rng(seed):
             return np.random.Generator(np.random.PCG64(seed))
 
-        # one activation / gradient / output buffer per distinct width (values
-        # do not affect timing); everything per layer is separate
-        # one activation / gradient / output buffer per distinct width (values
-        # do not affect timing); weights, z, G^ and Adam moments are per layer.
+        # Every input group has its own activation, output and gradient
+        # buffers (x, y, dL/do, dL/dx), as the layers of a model do, so no
+        # launch finds its operands left in the caches by another group's.
+        # When the workload's buffers would not fit in 85% of the device
+        # memory, blocks share `act_sets` sets of them round-robin (reported).
+        # Their values (x ~ N(0,1), dL/do ~ N(0, 1e-4)) come from a seeded
+        # device generator; weights, z, G^ and the Adam moments are per layer.
         # A group's weights are column slices of one [n x sum m] tensor, its z
         # column slices of one [T x sum r] tensor.
         self.groups = input_groups(wl, grouped)
-        self.x, self.dy, self.y, self.dx = {}, {}, {}, {}
-        self.W, self.z = [None] * len(wl.layers), [None] * len(wl.layers)
-        self.Wg, self.zg, self.msum = [], [], []
+        per_block = {}
         for g in self.groups:
             Ls = [wl.layers[i] for i in g]
+            n, M = Ls[0].n, sum(L.m for L in Ls)
+            per_block[Ls[0].block] = per_block.get(Ls[0].block, 0) + 2 * T * 2 * (ld8(n) + ld8(M))
+        need = max(per_block.values()) * len(per_block)
+        budget = int(0.85 * torch.cuda.get_device_properties(dev).total_memory) - 16 * 2**30
+        self.act_sets = max(1, min(len(per_block), budget // max(1, max(per_block.values()))))
+        gen = torch.Generator(device=dev)
+        act = {}  # (set, position of the group in its block) -> buffers
+
+        def act_buffers(gi, n, M):
+            Ls = [wl.layers[i] for i in self.groups[gi]]
+            key = (Ls[0].block % self.act_sets, Ls[0].k)
+            if key not in act:
+                gen.manual_seed(1234 + 97 * key[0] + key[1])
+                x = torch.empty(T, ld8(n), dtype=torch.bfloat16, device=dev)
+                x.normal_(0.0, 1.0, generator=gen)
+                dy = torch.empty(T, ld8(M), dtype=torch.bfloat16, device=dev)
+                dy.normal_(0.0, 0.01, generator=gen)
+                act[key] = (x[:, :n], torch.empty(T, ld8(M), dtype=torch.bfloat16, device=dev)[:, :M],
+                            dy[:, :M], torch.empty(T, ld8(n), dtype=torch.bfloat16, device=dev)[:, :n])
+            return act[key]
+
+        self.x, self.y, self.dy, self.dx = [], [], [], []
+        self.W, self.z = [None] * len(wl.layers), [None] * len(wl.layers)
+        self.Wg, self.zg, self.msum = [], [], []
+        for gi, g in enumerate(self.groups):
+            Ls = [wl.layers[i] for i in g]
             n, M, R = Ls[0].n, sum(L.m for L in Ls), sum(L.r for L in Ls)
-            if n not in self.x:
-                self.x[n] = dev_bf16(bf16_round(rng(1234 + n).standard_normal((T, n), np.float32)), ld8(n))
-                self.dx[n] = torch.empty(T, ld8(n), dtype=torch.bfloat16, device=dev)[:, :n]
-            if M not in self.dy:
-                self.dy[M] = dev_bf16(bf16_round(0.01 * rng(4321 + M).standard_normal((T, M), np.float32)), ld8(M))
-                self.y[M] = torch.empty(T, ld8(M), dtype=torch.bfloat16, device=dev)[:, :M]
+            xb, yb, dyb, dxb = act_buffers(gi, n, M)
+            self.x.append(xb)
+            self.y.append(yb)
+            self.dy.append(dyb)
+            self.dx.append(dxb)
             Wall = np.concatenate([bf16_round(0.02 * rng(1234 + L.layer_id).standard_normal((L.n, L.m), np.float32))
                                    for L in Ls], axis=1)
             Wg = dev_bf16(Wall, ld8(M))
@@ -133,6 +159,7 @@ class Model:
             self.Wg.append(Wg)
             self.zg.append(zg)
             self.msum.append(M)
+        self.act_bytes = need if self.act_sets == len(per_block) else None
         self.G, self.M, self.V = [], [], []
         for L in wl.layers:
             self.G.append(torch.empty(L.r, L.m, dtype=torch.float32, device=dev))
@@ -158,7 +185,7 @@ class Model:
     def fwd(self, gi):
         g = self.groups[gi]
         Ls = [self.wl.layers[i] for i in g]
-        x, y = self.x[Ls[0].n], self.y[self.msum[gi]]
+        x, y = self.x[gi], self.y[gi]
         if len(g) == 1:
             self.cp.compact_fwd(x, self.Wg[gi], y, self.zg[gi], self.seeds[g[0]], proj=self.proj, ws=self.ws_f)
         else:
@@ -168,13 +195,13 @@ class Model:
     def _bwd(self, gi, dx, ghat):
         g = self.groups[gi]
         Ls = [self.wl.layers[i] for i in g]
-        dy = self.dy[self.msum[gi]]
+        dy = self.dy[gi]
         if len(g) == 1:
             self.cp.compact_bwd(dy, self.Wg[gi] if dx else None, self.zg[gi] if ghat else None,
-                                self.dx[Ls[0].n] if dx else None, self.G[g[0]] if ghat else None, ws=self.ws_b)
+                                self.dx[gi] if dx else None, self.G[g[0]] if ghat else None, ws=self.ws_b)
         else:
             self.cp.compact_bwd_group(dy, self.Wg[gi] if dx else None, self.zg[gi] if ghat else None,
-                                      self.dx[Ls[0].n] if dx else None, [self.G[i] for i in g] if ghat else None,
+                                      self.dx[gi] if dx else None, [self.G[i] for i in g] if ghat else None,
                                       [L.m for L in Ls], [L.r for L in Ls], ws=self.ws_b)
 
     def bwd_dx(self, gi):
@@ -262,6 +289,20 @@ def time_phases(model, torch, reps=2, step_reps=10):
     return out
 
 
+def host_info():
+    """The CPU model and the cores this process may use (for the CPU baseline)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(wl, t_slice, min_secs=10.0, sparse_s=0):
     """The oracle (numpy fp64) timed on this host's cores on a bounded sample:
     fwd + bwd + step of each distinct layer shape on t_slice tokens (the full
@@ -270,11 +311,18 @@ def cpu_baseline(wl, t_slice, min_secs=10.0, sparse_s=0):
     the step is token-free)."""
     from oracle import compact as oc
     from synthetic import bwd_inputs, fwd_inputs
+    cores = len(os.sched_getaffinity(0))
+    host = host_info()
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threadpool_limits(cores)  # the BLAS uses every core this process may run on
+        blas = [d for d in threadpool_info() if d.get("user_api") == "blas"]
+        threads = max([d.get("num_threads", 1) for d in blas] or [1])
+        host["blas"] = ", ".join(f"{d.get('internal_api')} {d.get('version')} ({d.get('architecture')})" for d in blas)
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        threads = cores
+        host["blas"] = "unknown"
+    host["blas_threads"] = int(threads)
     counts = {}
     for L in wl.layers:
         counts[(L.n, L.m, L.r)] = counts.get((L.n, L.m, L.r), 0) + 1
@@ -307,6 +355,7 @@ def cpu_baseline(wl, t_slice, min_secs=10.0, sparse_s=0):
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
+        "host": host,
         "sample": (f"numpy fp64 oracle: fwd+bwd+step of each of the {len(counts)} distinct layer "
                    f"shapes at {Ts} tokens, {reps} repetition(s) ({spent:.1f} s){scaled}, "
                    f"weighted by the layer count of each shape ({len(wl.layers)} layers)"),
@@ -461,7 +510,9 @@ def main():
         "config": {"workload": wl.description, "tokens_per_step": T, "layers": nl,
                    "input_groups": ("q,k,v and gate,up share their input (gate,up only when their width is a "
                                     "multiple of 8)") if not args.no_group else "none",
-                   "fwd_mode": args.fwd_mode, "projection": args.proj, "parallelism": "single GPU"},
+                   "fwd_mode": args.fwd_mode, "projection": args.proj, "parallelism": "single GPU",
+                   "activation_buffers": ("one x, y, dL/do, dL/dx per input group" if model.act_bytes else
+                                          f"{model.act_sets} sets shared round-robin by the blocks")},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "phases_ms": {k: round(v, 4) for k, v in phases.items()},

@@ -36,15 +36,7 @@ def proj_code(proj):
     return PROJ[proj]
 
 
-def proj_scale(proj, r):
-    """P = proj_scale x the unscaled stream (compact_projection's output)."""
-    code = proj_code(proj)
-    kind, s_ = code & 0xFF, code >> 8
-    if kind == PROJ["identity"]:
-        return 1.0
-    return 1.0 / float(s_ or SPARSE_JL_DEFAULT_S if kind == PROJ["sparse-jl"] else r) ** 0.5
-
-__all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "proj_scale", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
+__all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
            "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
            "LayerBatch", "prepare_layers",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",

@@ -158,3 +158,73 @@ def test_full_size_step_batched():
         assert np.all(np.abs(to_np(d["W"][:, ci]) - exact) <= ulp + op_err)
         # and the update is not lost in the rounding: most elements moved
         assert np.mean(to_np(d["W"][:, ci]) != W0[:, cs]) > 0.5
+
+
+# One input group per workload at its full token count, every element:
+# the group with the most output tiles that the benchmark forms.
+EVERY = [
+    ("llama-60m", 512, (512, 512, 512), (128, 128, 128)),
+    ("roberta-base", 768, (768, 768, 768), (384, 384, 384)),
+    ("llama-350m", 1024, (2736, 2736), (128, 128)),
+    ("llama-1b-r4", 2048, (2048, 2048, 2048), (512, 512, 512)),
+    ("llama-1b-r8", 2048, (2048, 2048, 2048), (256, 256, 256)),
+]
+CHUNK = 8192
+
+
+@pytest.mark.parametrize("case", EVERY, ids=lambda c: c[0])
+def test_full_size_every_element(case):
+    from gpu_util import BF16_U, assert_elementwise
+    name, n, ms, rs = case
+    wl = workload(name)
+    T = wl.tokens
+    M, R = sum(ms), sum(rs)
+    seeds = tuple(((3 + k) << 32) | 1 for k in range(len(ms)))
+    x = normal_bf16_blocked(T, n, seed=4000 + n)
+    W = normal_bf16_blocked(n, M, seed=4100 + M, scale=0.02)
+    dy = normal_bf16_blocked(T, M, seed=4200 + M, scale=0.01)
+    zs = normal_bf16_blocked(T, R, seed=4300 + R, scale=float(np.sqrt(n / rs[0])))
+    xd = to_dev(x, "bf16", ld_for(n, "bf16"))
+    Wd = to_dev(W, "bf16", ld_for(M, "bf16"))
+    dyd = to_dev(dy, "bf16", ld_for(M, "bf16"))
+    zsd = to_dev(zs, "bf16", ld_for(R, "bf16"))
+    y = empty(T, M, "bf16", ld_for(M, "bf16"), fill=float("nan"))
+    z = empty(T, R, "bf16", ld_for(R, "bf16"), fill=float("nan"))
+    dx = empty(T, n, "bf16", ld_for(n, "bf16"), fill=float("nan"))
+    ws_f = workspace(cp.fwd_group_workspace_bytes(n, ms, rs))
+    ws_b = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs))
+    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, ws=ws_f)
+    Gs = [torch.full((r, m), float("nan"), dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dyd, Wd, z, dx, Gs, ms, rs, ws=ws_b)      # as the benchmark chains them
+    Gz = [torch.full((r, m), float("nan"), dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dyd, None, zsd, None, Gz, ms, rs, ws=ws_b)  # on a synthetic z
+    torch.cuda.synchronize()
+    Ps = [projection(s, n, r) for s, r in zip(seeds, rs)]
+    W64 = W.astype(np.float64)
+    aW = np.abs(W64)
+    G_ref = [np.zeros((r, m)) for m, r in zip(ms, rs)]
+    Gz_ref = [np.zeros((r, m)) for m, r in zip(ms, rs)]
+    Gz_abs = [np.zeros((r, m)) for m, r in zip(ms, rs)]
+    for r0 in range(0, T, CHUNK):
+        r1 = min(T, r0 + CHUNK)
+        xc, dyc, zsc = x[r0:r1].astype(np.float64), dy[r0:r1].astype(np.float64), zs[r0:r1].astype(np.float64)
+        ax = np.abs(xc)
+        yc, zc, dxc = to_np(y[r0:r1]), to_np(z[r0:r1]), to_np(dx[r0:r1])
+        assert_elementwise(yc, xc @ W64, ax @ aW, n, what=f"y rows {r0}..{r1}")
+        assert_elementwise(dxc, dyc @ W64.T, np.abs(dyc) @ aW.T, M, what=f"dx rows {r0}..{r1}")
+        mo = ro = 0
+        for k, (m, r) in enumerate(zip(ms, rs)):
+            z_ref = xc @ Ps[k]
+            assert_elementwise(zc[:, ro:ro + r], z_ref, ax @ np.abs(Ps[k]), n, operand_rel=BF16_U * 1.001,
+                               what=f"z[{k}] rows {r0}..{r1}")
+            G_ref[k] += z_ref.T @ dyc[:, mo:mo + m]
+            Gz_ref[k] += zsc[:, ro:ro + r].T @ dyc[:, mo:mo + m]
+            Gz_abs[k] += np.abs(zsc[:, ro:ro + r]).T @ np.abs(dyc[:, mo:mo + m])
+            mo += m
+            ro += r
+    for k in range(len(ms)):
+        # chained: the GPU's G^ sums its own (bf16) z, the oracle its exact z
+        assert oc.rel_fro(Gs[k].cpu().numpy(), G_ref[k]) <= TOL
+        got = Gz[k].cpu().numpy().astype(np.float64)
+        assert_elementwise(got, Gz_ref[k], Gz_abs[k], T + 256, bf16_out=False, what=f"G^[{k}] (synthetic z)")
+        assert oc.rel_fro(got, Gz_ref[k]) <= TOL
