@@ -18,7 +18,8 @@
  *  - All tensor pointers are DEVICE pointers owned by the caller; the library
  *    allocates nothing and frees nothing.  Scratch memory comes from a
  *    caller-provided workspace whose size is given by the matching
- *    *_workspace_bytes function.
+ *    *_workspace_bytes function (compact_bwd_noalloc alone uses a scratch
+ *    array of the library's device code instead, see there).
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *    Every call is asynchronous and ordered on that stream; the call returns
  *    after the launches are enqueued.
@@ -204,6 +205,31 @@ int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, 
 
 size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t count, const int64_t* m,
                                          const int64_t* r, int dtype);
+
+/*
+ * compact_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Arguments, results and errors as compact_bwd; the
+ * G^ split-K partial sums (and the K-tiled copy of W for dx, when it fits)
+ * live in a library-owned scratch array of COMPACT_NOALLOC_SCRATCH_BYTES per
+ * GPU, part of the library's device code: the runtime reserves it on every
+ * GPU the library runs on when the library is first used there, and it stays
+ * reserved until the process ends.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library call).  Results are bitwise those of
+ * compact_bwd with a workspace of that size.
+ * Every call on one GPU shares that GPU's scratch and leaves its contents
+ * behind: calls that may overlap on one GPU (different streams, or threads
+ * without ordering between them) race and must be serialised by the caller.
+ * Errors: as compact_bwd, and COMPACT_EUNSUPPORTED when G is requested and
+ * compact_bwd_workspace_bytes(tokens, n, m, r, dtype) exceeds the scratch
+ * (then nothing is launched).  This covers every layer of the LLaMA-60M,
+ * RoBERTa-Base, LLaMA-350M and LLaMA-1B shapes.
+ */
+#define COMPACT_NOALLOC_SCRATCH_BYTES (48u << 20)
+
+int compact_bwd_noalloc(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
+                        void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n, int64_t m, int64_t r,
+                        int dtype, void* stream);
 
 /*
  * Optimizer step, Alg. 3 (Adam on the compressed gradient, then decompression):

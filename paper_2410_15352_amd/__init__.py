@@ -36,7 +36,7 @@ def proj_code(proj):
     return PROJ[proj]
 
 
-__all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "fwd_group_workspace_bytes", "compact_bwd", "compact_step", "compact_pstream", "compact_next_seed",
+__all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "fwd_group_workspace_bytes", "compact_bwd", "compact_bwd_noalloc", "compact_step", "compact_pstream", "compact_next_seed",
            "compact_pstream_boxmuller", "compact_step_batched", "step_batched_workspace_bytes",
            "LayerBatch", "prepare_layers",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "step_workspace_bytes",
@@ -165,6 +165,23 @@ def compact_bwd(dy, W, z, dx, G, ws=None, stream=None):
     st = lib.compact_bwd(_ptr(dy), _ld(dy), _ptr(W), _ld(W), _ptr(z), _ld(z), _ptr(dx), _ld(dx),
                          _ptr(G), T, n, m, r, _dtype_code(dy), wp, wb, _stream(stream, dy))
     _check("compact_bwd", st)
+
+
+NOALLOC_SCRATCH_BYTES = 48 << 20
+
+
+def compact_bwd_noalloc(dy, W, z, dx, G, stream=None):
+    """compact_bwd without a workspace: the library's own per-GPU scratch
+    (calls that overlap on one GPU race)."""
+    lib = _lib.load()
+    T, m = dy.shape
+    r = z.shape[1] if z is not None else (G.shape[0] if G is not None else 1)
+    n = W.shape[0] if W is not None else (dx.shape[1] if dx is not None else r)
+    if G is not None and (not G.is_contiguous() or tuple(G.shape) != (r, m)):
+        raise ValueError("G must be a contiguous (r, m) fp32 tensor")
+    st = lib.compact_bwd_noalloc(_ptr(dy), _ld(dy), _ptr(W), _ld(W), _ptr(z), _ld(z), _ptr(dx), _ld(dx),
+                                 _ptr(G), T, n, m, r, _dtype_code(dy), _stream(stream, dy))
+    _check("compact_bwd_noalloc", st)
 
 
 def bwd_group_workspace_bytes(tokens, n, ms, rs, dtype=BF16):

@@ -22,6 +22,8 @@ SIGNATURES = {
     "compact_bwd": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
                             c_i64, c_i64, c_i64, c_int, c_vp, c_size, c_vp]),
     "compact_bwd_workspace_bytes": (c_size, [c_i64, c_i64, c_i64, c_i64, c_int]),
+    "compact_bwd_noalloc": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
+                                    c_i64, c_i64, c_i64, c_int, c_vp]),
     "compact_bwd_group": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
                                   ctypes.POINTER(c_vp), c_i64, c_i64, ctypes.c_int32, ctypes.POINTER(c_i64),
                                   ctypes.POINTER(c_i64), c_int, c_vp, c_size, c_vp]),

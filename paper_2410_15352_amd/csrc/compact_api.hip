@@ -8,6 +8,7 @@
 #include <string>
 #include <vector>
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/compact.h"
 #include "gemm_w4_launch.hpp"
@@ -78,6 +79,7 @@ int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
 }
 
 constexpr size_t kWsAlign = 256;
+constexpr int kMaxScratchDevices = 64;
 
 void* align_ws(void* ws) {
   const uintptr_t a = (reinterpret_cast<uintptr_t>(ws) + kWsAlign - 1) & ~uintptr_t(kWsAlign - 1);
@@ -936,6 +938,57 @@ int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, 
   }
   if ((st = launch_step_groups(plans, adam_consts(t, beta1, beta2, eps, proj, dtype), dtype, w_dtype, s))) return st;
   return ok();
+}
+
+// Scratch of compact_bwd_noalloc: one array per GPU, part of the library's
+// code object (allocated by the runtime when the module is loaded on a device,
+// held until the process ends).  Host code never passes `scratch` itself to a
+// kernel: its name is a host-side stand-in; the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[COMPACT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];
+
+// The device address of this device's `scratch` (the current device), looked
+// up on the first call on the device.
+int scratch_ptr(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(COMPACT_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices) return fail(COMPACT_EUNSUPPORTED, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(COMPACT_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return COMPACT_OK;
+}
+
+}  // namespace
+
+int compact_bwd_noalloc(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
+                        void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n, int64_t m, int64_t r,
+                        int dtype, void* stream) {
+  int st;
+  if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
+  if ((st = check_shape(tokens, n, m, r, COMPACT_PROJ_GAUSSIAN))) return st;
+  const size_t need = G != nullptr ? compact_bwd_workspace_bytes(tokens, n, m, r, dtype) : 0;
+  if (need > COMPACT_NOALLOC_SCRATCH_BYTES)
+    return fail(COMPACT_EUNSUPPORTED, "backward needs %zu B of scratch; compact_bwd_noalloc has %zu B (use compact_bwd)",
+                need, static_cast<size_t>(COMPACT_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if ((st = scratch_ptr(&ws))) return st;
+  // with a whole scratch (not only `need` bytes) compact_bwd also stages W
+  // for dx whenever that fits, as it does with a caller workspace this large
+  return compact_bwd(dy, lddy, W, ldw, z, ldz, dx, lddx, G, tokens, n, m, r, dtype, ws,
+                     COMPACT_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int compact_pstream(uint64_t seed, int64_t n, int64_t r, float* out, int64_t ld, void* stream) {
