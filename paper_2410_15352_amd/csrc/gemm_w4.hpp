@@ -176,12 +176,21 @@ constexpr int w4_vm_allow() {
   return (w4_drip(T - 2) ? 1 : 0) + 8 + (w4_drip(T - 1) ? 16 : 0) + 4 + (w4_drip(T) ? 8 : 0);
 }
 
+// The lane id, computed where it is used (volatile: not merged with another
+// computation of it, so no register holds it across the tile loop).
+__device__ __forceinline__ int w4_lane_id() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // ------------------------------ per-lane state ------------------------------
 struct W4Lane {
   int lane, wave, wm, wn;
   uint32_t a0, a1, b0, b1;  // fragment byte addresses, stage 0, steps 0 and 1
   uint32_t lds;             // dynamic LDS base
-  int va[4], vb[4];         // A and B copy offsets (k = 0) of blocks 4 wave + q
+  int va, vb;               // A and B copy offsets (k = 0) of block 4 wave (q = 0)
+  int qa, qb;               // what the offsets add per block q (16 rows; wave-uniform)
   int kchunk;               // 8 * logical chunk this lane copies
   int ksb;                  // bytes the B offsets advance per element of k0
 };
@@ -214,12 +223,13 @@ __device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
   L.a1 = L.lds + w4_frag_off(L.wm * 128, L.lane, 1);
   L.b0 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 0);
   L.b1 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 1);
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int j = L.wave * 4 + q;
-    L.va[q] = w4_copy_off(g.lda, L.lane, j, L.kchunk);
-    L.vb[q] = w4_copy_off(g.b_tiled ? 32 : g.ldb, L.lane, j, L.kchunk);
-  }
+  // block q = 0 of this wave; block q adds 16 q rows (a wave-uniform step),
+  // so only one offset per operand stays in a vector register
+  const int ldb_rows = g.b_tiled ? 32 : g.ldb;
+  L.va = w4_copy_off(g.lda, L.lane, L.wave * 4, L.kchunk);
+  L.vb = w4_copy_off(ldb_rows, L.lane, L.wave * 4, L.kchunk);
+  L.qa = 32 * g.lda;
+  L.qb = 32 * ldb_rows;
   L.ksb = g.b_tiled ? 2 * g.rows_b : 2;
   return L;
 }
@@ -300,14 +310,14 @@ __device__ __forceinline__ void w4_copy(const W4Gemm& g, const W4Lane& L, const 
   const uint32_t oob = ~static_cast<uint32_t>(k0 + L.kchunk - g.K) & kW4Oob;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t vo = static_cast<uint32_t>(L.va[q] + 2 * k0) | oob;
+    const uint32_t vo = static_cast<uint32_t>(L.va + q * L.qa + 2 * k0) | oob;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         d.ra, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(sa + (L.wave * 4 + q) * 1024u)), 16,
         static_cast<int>(vo), 0, 0, 0);
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t vo = static_cast<uint32_t>(L.vb[q] + L.ksb * k0) | oob;
+    const uint32_t vo = static_cast<uint32_t>(L.vb + q * L.qb + L.ksb * k0) | oob;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         d.rb, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(sb + (L.wave * 4 + q) * 1024u)), 16,
         static_cast<int>(vo), 0, 0, 0);
@@ -351,13 +361,16 @@ __device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, c
   const int64_t wcol0 = static_cast<int64_t>(seg ? c.ct - g.seg[0].tiles : c.ct) * kW4Tile + L.wn * 128;
   o.rc = w4_rsrc(C + wrow0 * ldc + wcol0, live ? ((g.M - wrow0) * ldc - wcol0) * 2 : 0);
   o.rstride = static_cast<uint32_t>(ldc * 2);
-  const int lr = L.lane & 31, lh = L.lane >> 5, odd = L.lane & 1;
+  // 32-bit lane arithmetic (every size fits; the host checks), from a lane
+  // id recomputed here: lane values kept alive across the tile loop would be
+  // spilled, and each reload waits for every copy in flight
+  const int lane = w4_lane_id();
+  const int lr = lane & 31, lh = lane >> 5, odd = lane & 1;
   const uint32_t rl = static_cast<uint32_t>(4 * lh + 2 * odd) * o.rstride;
+  const int room = static_cast<int>(cols) - static_cast<int>(wcol0) - 1 - (lr & ~1);  // cl + 1 < cols - wcol0
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int cl = j * 32 + (lr & ~1);
-    o.vj[j] = wcol0 + cl + 1 < cols ? rl + 2u * static_cast<uint32_t>(cl) : kW4Oob;
-  }
+  for (int j = 0; j < 4; ++j)
+    o.vj[j] = j * 32 < room ? rl + 2u * static_cast<uint32_t>(j * 32 + (lr & ~1)) : kW4Oob;
   return o;
 }
 
@@ -417,7 +430,7 @@ __device__ __forceinline__ void w4_copy_one(const W4Lane& L, const W4CopyCursor&
                                             int k3, uint32_t s3) {
   const int q = c & 3;
   const bool is_a = c < 4;
-  const uint32_t vo = static_cast<uint32_t>(is_a ? L.va[q] + 2 * k3 : L.vb[q] + L.ksb * k3) | oob;
+  const uint32_t vo = static_cast<uint32_t>(is_a ? L.va + q * L.qa + 2 * k3 : L.vb + q * L.qb + L.ksb * k3) | oob;
   const uint32_t dst = L.lds + (is_a ? 0u : static_cast<uint32_t>(kW4BBase)) + s3 + (L.wave * 4 + q) * 1024u;
   __builtin_amdgcn_raw_ptr_buffer_load_lds(is_a ? cc.d.ra : cc.d.rb,
                                            reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
