@@ -374,41 +374,45 @@ __device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, c
   return o;
 }
 
-__device__ __forceinline__ void w4_pack(const f32x16 (&acc)[4][4], int lane, uint32_t (&out)[128]) {
-  const bool odd = (lane & 1) != 0;
+// Accumulator block b (row group gr: rows 8 gr + 4 (lane / 32) + 0 .. 3 of
+// column lane % 32) converted to bf16 pairs: raw[(b * 4 + gr) * 2] holds rows
+// + 0, + 1 and raw[... + 1] rows + 2, + 3.
+__device__ __forceinline__ void w4_convert_block(const f32x16& a, int b, uint32_t (&raw)[128]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int gr = 0; gr < 4; ++gr) {
-        const uint32_t p01 = pack_bf16x2(acc[i][j][4 * gr + 0], acc[i][j][4 * gr + 1]);
-        const uint32_t p23 = pack_bf16x2(acc[i][j][4 * gr + 2], acc[i][j][4 * gr + 3]);
-        const uint32_t snd = odd ? p01 : p23;
-        const uint32_t rcv = static_cast<uint32_t>(
-            __builtin_amdgcn_mov_dpp(static_cast<int>(snd), 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
-        const int e = ((i * 4 + j) * 4 + gr) * 2;
-        // even lane: rows R, R+1 of columns C (own), C+1 (partner);
-        // odd lane: rows R+2, R+3 of columns C-1 (partner), C (own)
-        out[e] = odd ? __builtin_amdgcn_perm(p23, rcv, 0x05040100u) : __builtin_amdgcn_perm(rcv, p01, 0x05040100u);
-        out[e + 1] = odd ? __builtin_amdgcn_perm(p23, rcv, 0x07060302u) : __builtin_amdgcn_perm(rcv, p01, 0x07060302u);
-      }
+  for (int gr = 0; gr < 4; ++gr) {
+    raw[(b * 4 + gr) * 2] = pack_bf16x2(a[4 * gr + 0], a[4 * gr + 1]);
+    raw[(b * 4 + gr) * 2 + 1] = pack_bf16x2(a[4 * gr + 2], a[4 * gr + 3]);
+  }
 }
 
-// Stores of accumulator blocks (i, j) = (B / 4, B % 4) for B in [B0, B0 + NB).
-template <int B0, int NB>
-__device__ __forceinline__ void w4_store(const W4Out& o, const uint32_t (&out)[128]) {
+// The two stores of (block, row group) from its raw pair p01, p23, one DPP
+// swap between the lanes of a column pair: the even lane gets rows R, R + 1 of
+// columns C, C + 1 (o0, o1), the odd lane rows R + 2, R + 3 of C - 1, C.
+__device__ __forceinline__ void w4_shuffle(uint32_t p01, uint32_t p23, bool odd, uint32_t& o0, uint32_t& o1) {
+  const uint32_t snd = odd ? p01 : p23;
+  const uint32_t rcv =
+      static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(snd), 0xB1, 0xF, 0xF, false));  // 1,0,3,2
+  const uint32_t hi = odd ? p23 : rcv, lo = odd ? rcv : p01;
+  o0 = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+  o1 = __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+}
+
+__device__ __forceinline__ uint32_t w4_store_off(const W4Out& od, int b, int gr, int w) {
+  return od.vj[b & 3] + static_cast<uint32_t>((b >> 2) * 32 + gr * 8 + w) * od.rstride;
+}
+
+// Every store of a converted tile at once (the last tile of the workgroup).
+__device__ __forceinline__ void w4_flush(const W4Out& od, const uint32_t (&raw)[128]) {
+  const bool odd = (w4_lane_id() & 1) != 0;
 #pragma unroll
-  for (int b = B0; b < B0 + NB; ++b) {
-    const int i = b >> 2, j = b & 3;
+  for (int b = 0; b < 16; ++b)
 #pragma unroll
-    for (int gr = 0; gr < 4; ++gr)
-#pragma unroll
-      for (int w = 0; w < 2; ++w) {
-        const uint32_t vo = o.vj[j] + static_cast<uint32_t>(i * 32 + gr * 8 + w) * o.rstride;
-        __builtin_amdgcn_raw_buffer_store_b32(out[(b * 4 + gr) * 2 + w], o.rc, static_cast<int>(vo), 0, 0);
-      }
-  }
+    for (int gr = 0; gr < 4; ++gr) {
+      uint32_t o0, o1;
+      w4_shuffle(raw[(b * 4 + gr) * 2], raw[(b * 4 + gr) * 2 + 1], odd, o0, o1);
+      __builtin_amdgcn_raw_buffer_store_b32(o0, od.rc, static_cast<int>(w4_store_off(od, b, gr, 0)), 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(o1, od.rc, static_cast<int>(w4_store_off(od, b, gr, 1)), 0, 0);
+    }
 }
 
 // ------------------------------ MFMA steps ---------------------------------
@@ -438,18 +442,27 @@ __device__ __forceinline__ void w4_copy_one(const W4Lane& L, const W4CopyCursor&
 }
 
 // Store n (0 .. 15) of K tile T: block 2 T + n / 8, row group (n / 2) % 4, row n % 2.
+// An even n shuffles the pair of its (block, row group) and keeps the second
+// value in `hold` for store n + 1.
 template <int T>
-__device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&out)[128], int n) {
+__device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&raw)[128], bool odd, uint32_t& hold,
+                                             int n) {
   const int b = 2 * T + (n >> 3), gr = (n >> 1) & 3, w = n & 1;
-  const int bi = b >> 2, bj = b & 3;
-  const uint32_t vo = od.vj[bj] + static_cast<uint32_t>(bi * 32 + gr * 8 + w) * od.rstride;
-  __builtin_amdgcn_raw_buffer_store_b32(out[(b * 4 + gr) * 2 + w], od.rc, static_cast<int>(vo), 0, 0);
+  uint32_t v;
+  if (w == 0) {
+    w4_shuffle(raw[(b * 4 + gr) * 2], raw[(b * 4 + gr) * 2 + 1], odd, v, hold);
+  } else {
+    v = hold;
+  }
+  __builtin_amdgcn_raw_buffer_store_b32(v, od.rc, static_cast<int>(w4_store_off(od, b, gr, w)), 0, 0);
 }
 
 template <int T>
 __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc, int kt,
                                          int n_my, const W4Walk& wk, const W4Out& od,
-                                         const uint32_t (&out)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4]) {
+                                         uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4]) {
+  const bool odd = w4_drip(T) ? (w4_lane_id() & 1) != 0 : false;
+  uint32_t hold = 0;
   const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
   const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
   const uint32_t s3 = static_cast<uint32_t>((h + 3) & 3) * kW4StageBytes;
@@ -468,7 +481,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
     }
     if (i % 4 == 0) w4_copy_one<T>(L, cc, i / 4, oob, k3, s3);
     if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, out, i / 2);
+      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, i / 2);
     }
   }
   w4_pin_acc(acc);
@@ -486,7 +499,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
     }
     if (i % 4 == 2) w4_copy_one<T>(L, cc, 4 + i / 4, oob, k3, s3);
     if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, out, 8 + i / 2);
+      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, 8 + i / 2);
     }
   }
   w4_pin(f[0]);
@@ -516,9 +529,9 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   }
   W4Frags f[2];
   f32x16 acc[4][4];
-  uint32_t out[128];
+  uint32_t raw[128];
 #pragma unroll
-  for (int e = 0; e < 128; ++e) out[e] = 0u;
+  for (int e = 0; e < 128; ++e) raw[e] = 0u;  // stored against an empty range by the first tile
   W4Cursor oc{0, 0, 0};
   w4_tile_at(g, wk, oc);
   W4Out od = w4_out_desc(g, L, oc, false);  // nothing to store before the first tile
@@ -527,23 +540,26 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   w4_read(L.a0, L.b0, f[0]);
   int h = 0;
   for (int q = 0; q < n_my; ++q) {
-    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, wk, od, out, f, acc);
-    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, wk, od, out, f, acc);
-    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, wk, od, out, f, acc);
+    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc);
+    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc);
+    // bf16 pairs only here (the stores of the next tile's first K tiles do
+    // the lane shuffles, in the shadow of its MFMAs)
+#pragma unroll
+    for (int b = 0; b < 16; ++b) w4_convert_block(acc[b >> 2][b & 3], b, raw);
     h += kt;
     od = w4_out_desc(g, L, oc, true);
-    w4_pack(acc, L.lane, out);
     w4_next_tile(g, wk, oc);
   }
-  w4_store<0, 16>(od, out);
+  w4_flush(od, raw);
   w4_wait_vm<0>();  // no copy may still be writing LDS when the workgroup ends
 }
 
