@@ -386,7 +386,7 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
   int st;
   const int64_t ldb = pt_ld(n);
   const int64_t rows_b = stacked_rows(G.msum, G.rsum);
-  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, rows_b, ldy, G.msum, ldz, G.rsum) &&
+  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, rows_b, ldy, G.msum, ldz, G.rsum, true) &&
           tiled_fits(rows_b, n);
   if (!taken) return COMPACT_OK;
   uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
@@ -614,17 +614,19 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
     return ok();
   }
 
-  if (dx != nullptr && gemm_w4_eligible(tokens, m, lddy, ldw, n, lddx, n, 0, 0)) {
+  const int64_t npad = round_up(n, kW4Tile);
+  const bool stage_w = ws != nullptr && ws_bytes >= dx_stage_bytes(n, m) + kWsAlign && tiled_fits(npad, m);
+  if (dx != nullptr && gemm_w4_eligible(tokens, m, lddy, ldw, n, lddx, n, 0, 0, stage_w)) {
     // persistent GEMM: dx = dL/do W^T with W [n][m] as the K-contiguous B,
     // copied into the K-tiled layout first when the workspace holds it
+    // (always when m % 8 != 0: the copy is zero past m)
     W4Gemm g{};
     g.A = static_cast<const uint16_t*>(dy); g.lda = static_cast<int>(lddy);
     g.M = static_cast<int>(tokens); g.K = static_cast<int>(m);
     g.B = static_cast<const uint16_t*>(W); g.ldb = static_cast<int>(ldw); g.rows_b = static_cast<int>(n);
-    const int64_t npad = round_up(n, kW4Tile);
-    if (ws != nullptr && ws_bytes >= dx_stage_bytes(n, m) + kWsAlign && tiled_fits(npad, m)) {
+    if (stage_w) {
       uint16_t* wt = static_cast<uint16_t*>(align_ws(ws));
-      const int64_t units = n * (m / 8);
+      const int64_t units = n * ceil_div(m, 8);
       hipLaunchKernelGGL(k_stage_rows_bf16, dim3(static_cast<uint32_t>(ceil_div(units, 256))), dim3(256), 0, s,
                          static_cast<const uint16_t*>(W), ldw, n, m, PanelOut{wt, 0, npad});
       if ((st = check_launch("W K-tile staging (bf16)"))) return st;

@@ -50,11 +50,14 @@
 //
 // Edges: operand rows past the matrix and chunks at k >= K read as zero (buffer
 // range check), so the K sum is exact; stores past the last row are dropped by
-// the same check, column pairs past the last column are steered out of range.
-// Requirements (checked by the host): K % 8 == 0, K >= 320, every output
-// column count even, 256 * ld * 2 + 2 K < 2^31 for every matrix, lda and
-// ldb multiples of 8 (16-byte chunks); for a K-tiled B (below) the whole
-// operand below 2^31 bytes.
+// the same check, column pairs past the last column are steered out of range
+// (an odd width writes its last column alone, w4_store_tail).  With K % 8 != 0
+// the chunk that holds element K - 1 is read whole and its elements past K are
+// cleared in registers (w4_mask_k); B must then be K-tiled (staged by this
+// library, zero past K).  Requirements (checked by the host): K >= 320,
+// 256 * ld * 2 + 2 K < 2^31 for every matrix, lda and ldb multiples of 8
+// (16-byte chunks); for a K-tiled B (below) the whole operand below 2^31
+// bytes.
 #pragma once
 #include "common.hpp"
 
@@ -349,6 +352,7 @@ struct W4Out {
   __amdgpu_buffer_rsrc_t rc;  // base at the wave tile's first element
   uint32_t vj[4];             // lane byte offset for column block j, or out of range
   uint32_t rstride;           // ldc * 2
+  int room;                   // columns of the wave tile inside the matrix (cols - first column)
 };
 
 __device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, const W4Cursor& c, bool live) {
@@ -367,7 +371,8 @@ __device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, c
   const int lane = w4_lane_id();
   const int lr = lane & 31, lh = lane >> 5, odd = lane & 1;
   const uint32_t rl = static_cast<uint32_t>(4 * lh + 2 * odd) * o.rstride;
-  const int room = static_cast<int>(cols) - static_cast<int>(wcol0) - 1 - (lr & ~1);  // cl + 1 < cols - wcol0
+  o.room = static_cast<int>(cols) - static_cast<int>(wcol0);
+  const int room = o.room - 1 - (lr & ~1);  // cl + 1 < cols - wcol0
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     o.vj[j] = j * 32 < room ? rl + 2u * static_cast<uint32_t>(j * 32 + (lr & ~1)) : kW4Oob;
@@ -401,7 +406,35 @@ __device__ __forceinline__ uint32_t w4_store_off(const W4Out& od, int b, int gr,
   return od.vj[b & 3] + static_cast<uint32_t>((b >> 2) * 32 + gr * 8 + w) * od.rstride;
 }
 
+// An odd output width: the column pair that straddles the last column is
+// steered out of range by w4_store_off; its first column (the low halves)
+// goes out here with 2-byte stores, all 32 of a wave tile at once, right
+// after the tile is converted (only wave tiles that hold the last column).
+__device__ __forceinline__ void w4_store_tails(const W4Out& od, const uint32_t (&raw)[128]) {
+  if ((od.room & 1) == 0 || od.room <= 0 || od.room >= 128) return;  // wave-uniform
+  const int lane = w4_lane_id();
+  const int lr = lane & 31, lh = lane >> 5, odd = lane & 1;
+  const int j = (od.room - 1) >> 5;  // column block of the last column
+  const int cl = j * 32 + (lr & ~1);
+  const uint32_t base = cl + 1 == od.room ? static_cast<uint32_t>(4 * lh + 2 * odd) * od.rstride +
+                                                2u * static_cast<uint32_t>(cl)
+                                          : kW4Oob;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int gr = 0; gr < 4; ++gr) {
+      const int b = i * 4 + j;
+      uint32_t o0, o1;
+      w4_shuffle(raw[(b * 4 + gr) * 2], raw[(b * 4 + gr) * 2 + 1], odd != 0, o0, o1);
+      const uint32_t r = static_cast<uint32_t>(i * 32 + gr * 8) * od.rstride;
+      __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(o0), od.rc, static_cast<int>(base + r), 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(o1), od.rc,
+                                            static_cast<int>(base + r + od.rstride), 0, 0);
+    }
+}
+
 // Every store of a converted tile at once (the last tile of the workgroup).
+template <bool ODD>
 __device__ __forceinline__ void w4_flush(const W4Out& od, const uint32_t (&raw)[128]) {
   const bool odd = (w4_lane_id() & 1) != 0;
 #pragma unroll
@@ -413,6 +446,7 @@ __device__ __forceinline__ void w4_flush(const W4Out& od, const uint32_t (&raw)[
       __builtin_amdgcn_raw_buffer_store_b32(o0, od.rc, static_cast<int>(w4_store_off(od, b, gr, 0)), 0, 0);
       __builtin_amdgcn_raw_buffer_store_b32(o1, od.rc, static_cast<int>(w4_store_off(od, b, gr, 1)), 0, 0);
     }
+  if constexpr (ODD) w4_store_tails(od, raw);
 }
 
 // ------------------------------ MFMA steps ---------------------------------
@@ -457,10 +491,36 @@ __device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&r
   __builtin_amdgcn_raw_buffer_store_b32(v, od.rc, static_cast<int>(w4_store_off(od, b, gr, w)), 0, 0);
 }
 
-template <int T>
+// K % 8 != 0: the last 16-byte chunk of every A row holds K % 8 elements of
+// the row and then whatever the caller's row padding holds (possibly NaN);
+// the copies bring it into LDS whole.  In the tile's last K tile the A
+// fragments that hold that chunk (k step kk, the lanes of half h) have the
+// elements past K cleared before their MFMAs.  (B past K is zero: this
+// library stages it.)
+__device__ __forceinline__ void w4_mask_k(const W4Gemm& g, W4Frags& f, int kk, bool last) {
+  const int c = ((g.K - 1) & 31) >> 3;  // chunk of element K - 1 in its K tile
+  if ((c >> 1) != kk) return;           // (wave-uniform, fixed for the launch)
+  // per dword of the chunk (two elements): the bits kept in the last K tile
+  // (wave-uniform values, so only the lane-half test is per lane)
+  const bool hit = (w4_lane_id() >> 5) == (c & 1);  // this lane's fragments hold the chunk
+  const int keep = g.K & 7;
+  uint32_t pm[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t part = 2 * d + 1 < keep ? 0xFFFFFFFFu : (2 * d < keep ? 0x0000FFFFu : 0u);
+    pm[d] = last ? part : 0xFFFFFFFFu;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int d = 0; d < 4; ++d) f.a[i][d] = hit ? (f.a[i][d] & pm[d]) : f.a[i][d];
+}
+
+template <int T, bool KMASK, bool ODD>
 __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc, int kt,
                                          int n_my, const W4Walk& wk, const W4Out& od,
-                                         uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4]) {
+                                         uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4],
+                                         bool last = false) {
   const bool odd = w4_drip(T) ? (w4_lane_id() & 1) != 0 : false;
   uint32_t hold = 0;
   const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
@@ -469,6 +529,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
   const f32x16 zero = {};
   const int k3 = cc.k * kW4K;
   const uint32_t oob = ~static_cast<uint32_t>(k3 + L.kchunk - g.K) & kW4Oob;
+  if constexpr (KMASK) w4_mask_k(g, f[0], 0, last);
   // step 0: MFMAs on f[0]; reads of f[1]; copies 0 .. 3 of step h + 3
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -488,6 +549,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
   // step 1: MFMAs on f[1]; reads of f[0] for step h + 1; copies 4 .. 7
   w4_wait_vm<w4_vm_allow<T>()>();
   w4_lds_barrier(f[1]);
+  if constexpr (KMASK) w4_mask_k(g, f[1], 1, last);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int fa = i >> 2, fb = i & 3;
@@ -508,6 +570,8 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
 
 // The whole persistent GEMM for this workgroup.  Launch with kW4Threads
 // threads, kW4Lds bytes of dynamic LDS and at most one workgroup per CU.
+// KMASK: K % 8 != 0 (B K-tiled); ODD: an output width is odd.
+template <bool KMASK, bool ODD>
 __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   const int G = static_cast<int>(gridDim.x);
   const int p = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
@@ -540,26 +604,30 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   w4_read(L.a0, L.b0, f[0]);
   int h = 0;
   for (int q = 0; q < n_my; ++q) {
-    w4_ktile<0>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<1>(g, L, h + 1, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<2>(g, L, h + 2, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<3>(g, L, h + 3, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<4>(g, L, h + 4, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<5>(g, L, h + 5, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<6>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<7>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<8>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<9>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc);
-    for (int t = 10; t < kt; ++t) w4_ktile<10>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<0, KMASK, ODD>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<1, KMASK, ODD>(g, L, h + 1, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<2, KMASK, ODD>(g, L, h + 2, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<3, KMASK, ODD>(g, L, h + 3, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<4, KMASK, ODD>(g, L, h + 4, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<5, KMASK, ODD>(g, L, h + 5, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<6, KMASK, ODD>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<7, KMASK, ODD>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<8, KMASK, ODD>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
+    w4_ktile<9, KMASK, ODD>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc, kt == 10);
+    for (int t = 10; t < kt; ++t)
+      w4_ktile<10, KMASK, ODD>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc, t == kt - 1);
     // bf16 pairs only here (the stores of the next tile's first K tiles do
     // the lane shuffles, in the shadow of its MFMAs)
 #pragma unroll
     for (int b = 0; b < 16; ++b) w4_convert_block(acc[b >> 2][b & 3], b, raw);
     h += kt;
     od = w4_out_desc(g, L, oc, true);
+    if constexpr (ODD) {
+      if (q + 1 < n_my) w4_store_tails(od, raw);  // the last tile's go out with w4_flush
+    }
     w4_next_tile(g, wk, oc);
   }
-  w4_flush(od, raw);
+  w4_flush<ODD>(od, raw);
   w4_wait_vm<0>();  // no copy may still be writing LDS when the workgroup ends
 }
 

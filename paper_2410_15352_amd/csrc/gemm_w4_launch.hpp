@@ -12,9 +12,10 @@
 namespace compact {
 
 // True when the persistent kernel handles this problem (see the requirements
-// in gemm_w4.hpp); `ldc_cols` lists each segment's (ldc, cols).
+// in gemm_w4.hpp): each output segment's (ldc, cols); b_tiled: B is the
+// K-tiled operand this library stages (needed when K % 8 != 0).
 bool gemm_w4_eligible(int64_t M, int64_t K, int64_t lda, int64_t ldb, int64_t rows_b, int64_t ldc0,
-                      int64_t cols0, int64_t ldc1, int64_t cols1);
+                      int64_t cols0, int64_t ldc1, int64_t cols1, bool b_tiled);
 
 // Which pass a launch serves (each has its own kernel instantiation).
 enum class W4Use { kForward, kDx };

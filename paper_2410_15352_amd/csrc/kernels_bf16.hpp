@@ -112,14 +112,11 @@ __device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t 
   for (int p = 0; p < 2; ++p) {
     const int id = t + 256 * p, c = id >> 3, ii = (id & 7) * 8;
     const int64_t gc = c0 + c, gi = r0 + ii;
-    if (gc >= cols) continue;
-    const u32x4 w = *reinterpret_cast<const u32x4*>(&tile[c][ii]);
-    if (gi + 8 <= rows) {
-      *reinterpret_cast<u32x4*>(panel_at(out, gc, gi)) = w;
-    } else {
-      for (int e = 0; e < 8 && gi + e < rows; ++e)
-        *panel_at(out, gc, gi + e) = static_cast<uint16_t>(w[e >> 1] >> (16 * (e & 1)));
-    }
+    if (gc >= cols || gi >= rows) continue;
+    // the tile holds zeros past `rows`: a chunk that straddles the end is
+    // written whole, so that the operand is zero up to the next multiple of 8
+    // (the panel's K extent is a multiple of 32)
+    *reinterpret_cast<u32x4*>(panel_at(out, gc, gi)) = *reinterpret_cast<const u32x4*>(&tile[c][ii]);
   }
 }
 
@@ -162,15 +159,26 @@ __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
 
 // The dx GEMM's B operand, W [n x m] (row R = input feature, K = m), copied
 // into the K-tiled layout: element (R, k) of `out` = W[R * ldw + k] for R < n,
-// k < m.  One thread per 8 consecutive k of one row (m % 8 == 0): a 16-byte
-// load and a 16-byte store.
+// k < m, and zero for m <= k < round_up(m, 8).  One thread per 8 consecutive
+// k of one row: a 16-byte load and a 16-byte store (the last chunk of a row
+// element by element when m % 8 != 0: the row's padding is not read).
 __global__ __launch_bounds__(256) void k_stage_rows_bf16(const uint16_t* W, int64_t ldw, int64_t n, int64_t m,
                                                          PanelOut out) {
-  const int64_t kq = m / 8;
+  const int64_t kq = ceil_div(m, 8);
   const int64_t u = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (u >= n * kq) return;
   const int64_t row = u / kq, k = (u - row * kq) * 8;
-  *reinterpret_cast<u32x4*>(panel_at(out, row, k)) = *reinterpret_cast<const u32x4*>(W + row * ldw + k);
+  u32x4 v;
+  if (k + 8 <= m) {
+    v = *reinterpret_cast<const u32x4*>(W + row * ldw + k);
+  } else {
+    uint16_t e[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) e[i] = k + i < m ? W[row * ldw + k + i] : uint16_t(0);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) v[d] = static_cast<uint32_t>(e[2 * d]) | (static_cast<uint32_t>(e[2 * d + 1]) << 16);
+  }
+  *reinterpret_cast<u32x4*>(panel_at(out, row, k)) = v;
 }
 
 // Unscaled fp32 stream of any projection (n x r, leading dimension ld), one

@@ -10,10 +10,11 @@
 namespace compact {
 
 // One instantiation per use, so that profiles report the forward and the dx
-// GEMM separately.
-template <int USE>
+// GEMM separately; KMASK: K % 8 != 0, ODD: an odd output width (the LLaMA-1B
+// widths of 5461).
+template <int USE, bool KMASK = false, bool ODD = false>
 __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
-  gemm_w4_persistent(g);
+  gemm_w4_persistent<KMASK, ODD>(g);
 }
 
 __global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) { ghat_w4(p); }
@@ -30,7 +31,7 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
-std::atomic<bool> g_lds_set[kMaxDevices][3];  // dynamic LDS limit raised: k_gemm_w4<0>, <1>, k_ghat_w4
+std::atomic<bool> g_lds_set[kMaxDevices][9];  // dynamic LDS limit raised: k_ghat_w4, the 8 k_gemm_w4
 
 bool fits_offsets(int64_t ld, int64_t K) {
   // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
@@ -46,12 +47,13 @@ bool fits_offsets(int64_t ld, int64_t K) {
 int w4_band_rows(int tiles_m) { return tiles_m < 4 ? (tiles_m > 0 ? tiles_m : 1) : 4; }
 
 bool gemm_w4_eligible(int64_t M, int64_t K, int64_t lda, int64_t ldb, int64_t rows_b, int64_t ldc0,
-                      int64_t cols0, int64_t ldc1, int64_t cols1) {
-  if (M < 1 || K % 8 != 0 || K < int64_t(kW4MinKTiles) * kW4K) return false;
+                      int64_t cols0, int64_t ldc1, int64_t cols1, bool b_tiled) {
+  if (M < 1 || K < int64_t(kW4MinKTiles) * kW4K) return false;
+  if (K % 8 != 0 && !b_tiled) return false;  // B's padding past K must be zero (staged here)
   if (lda % 8 != 0 || ldb % 8 != 0 || lda < K || ldb < K) return false;
   if (!fits_offsets(lda, K) || !fits_offsets(ldb, K) || !fits_offsets(ldc0, 0)) return false;
-  if (cols0 < 1 || cols0 % 2 != 0) return false;
-  if (cols1 != 0 && (cols1 % 2 != 0 || !fits_offsets(ldc1, 0))) return false;
+  if (cols0 < 1) return false;
+  if (cols1 != 0 && !fits_offsets(ldc1, 0)) return false;
   const int64_t limit = int64_t(1) << 30;
   if (M > limit || rows_b > limit || ldc0 > limit || ldc1 > limit) return false;
   return true;
@@ -69,21 +71,32 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
     cus = cus > 0 ? cus : 1;
     g_cus[dev].store(cus, std::memory_order_relaxed);
   }
-  const int u = use == W4Use::kForward ? 0 : 1;
-  const void* fn = u == 0 ? reinterpret_cast<const void*>(k_gemm_w4<0>) : reinterpret_cast<const void*>(k_gemm_w4<1>);
-  if (!g_lds_set[dev][u].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kW4Lds));
+  const bool kmask = g.K % 8 != 0;
+  const bool odd = g.seg[0].cols % 2 != 0 || (g.seg[1].tiles > 0 && g.seg[1].cols % 2 != 0);
+  const int u = (use == W4Use::kForward ? 0 : 4) + (kmask ? 2 : 0) + (odd ? 1 : 0);
+  static const void* const fns[8] = {
+      reinterpret_cast<const void*>(k_gemm_w4<0, false, false>), reinterpret_cast<const void*>(k_gemm_w4<0, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, true, false>), reinterpret_cast<const void*>(k_gemm_w4<0, true, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, false, false>), reinterpret_cast<const void*>(k_gemm_w4<1, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, true, false>), reinterpret_cast<const void*>(k_gemm_w4<1, true, true>)};
+  if (!g_lds_set[dev][1 + u].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(fns[u], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kW4Lds));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][u].store(true, std::memory_order_release);
+    g_lds_set[dev][1 + u].store(true, std::memory_order_release);
   }
   if (g.tiles <= 0) return hipSuccess;
-  const int grid = g.tiles < cus ? g.tiles : cus;
+  const dim3 grid(static_cast<uint32_t>(g.tiles < cus ? g.tiles : cus));
   W4Gemm gg = g;
   gg.band_rows = w4_band_rows(g.tiles / g.tiles_n);
-  if (u == 0) {
-    hipLaunchKernelGGL(k_gemm_w4<0>, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, gg);
-  } else {
-    hipLaunchKernelGGL(k_gemm_w4<1>, dim3(static_cast<uint32_t>(grid)), dim3(kW4Threads), kW4Lds, stream, gg);
+  switch (u) {
+    case 0: hipLaunchKernelGGL((k_gemm_w4<0, false, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 1: hipLaunchKernelGGL((k_gemm_w4<0, false, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 2: hipLaunchKernelGGL((k_gemm_w4<0, true, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 3: hipLaunchKernelGGL((k_gemm_w4<0, true, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 4: hipLaunchKernelGGL((k_gemm_w4<1, false, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 5: hipLaunchKernelGGL((k_gemm_w4<1, false, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    case 6: hipLaunchKernelGGL((k_gemm_w4<1, true, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
+    default: hipLaunchKernelGGL((k_gemm_w4<1, true, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
   }
   return hipGetLastError();
 }
@@ -113,11 +126,11 @@ hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  if (!g_lds_set[dev][2].load(std::memory_order_acquire)) {
+  if (!g_lds_set[dev][0].load(std::memory_order_acquire)) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_ghat_w4), hipFuncAttributeMaxDynamicSharedMemorySize,
                             static_cast<int>(kGhLds));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][2].store(true, std::memory_order_release);
+    g_lds_set[dev][0].store(true, std::memory_order_release);
   }
   const int64_t blocks = int64_t(p.tile_begin[p.count]) * p.splits;
   if (blocks <= 0) return hipSuccess;

@@ -168,11 +168,14 @@ EVERY = [
     ("llama-350m", 1024, (2736, 2736), (128, 128)),
     ("llama-1b-r4", 2048, (2048, 2048, 2048), (512, 512, 512)),
     ("llama-1b-r8", 2048, (2048, 2048, 2048), (256, 256, 256)),
+    # the widths of 5461: down (K = 5461, z of 1365 columns) and gate (5461 outputs)
+    ("llama-1b-r4", 5461, (2048,), (1365,)),
+    ("llama-1b-r8", 2048, (5461,), (256,)),
 ]
 CHUNK = 8192
 
 
-@pytest.mark.parametrize("case", EVERY, ids=lambda c: c[0])
+@pytest.mark.parametrize("case", EVERY, ids=lambda c: "{}-n{}-m{}".format(c[0], c[1], "+".join(map(str, c[2]))))
 def test_full_size_every_element(case):
     from gpu_util import BF16_U, assert_elementwise
     name, n, ms, rs = case
@@ -193,7 +196,10 @@ def test_full_size_every_element(case):
     dx = empty(T, n, "bf16", ld_for(n, "bf16"), fill=float("nan"))
     ws_f = workspace(cp.fwd_group_workspace_bytes(n, ms, rs))
     ws_b = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs))
-    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, ws=ws_f)
+    if len(ms) > 1:
+        cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, ws=ws_f)
+    else:
+        cp.compact_fwd(xd, Wd, y, z, seeds[0], ws=ws_f)
     Gs = [torch.full((r, m), float("nan"), dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
     cp.compact_bwd_group(dyd, Wd, z, dx, Gs, ms, rs, ws=ws_b)      # as the benchmark chains them
     Gz = [torch.full((r, m), float("nan"), dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]

@@ -7,7 +7,10 @@ tile's K loop, the operand copies run ahead across tile boundaries, and the
 walk covers several bands per XCD.  The token counts are not multiples of the
 tile (a ragged last row of tiles), and the widths leave ragged last column
 tiles (384 z columns, 5472 or 2736 output columns).  The shapes are those of
-the LLaMA-350M layers (q|k|v and gate|up input groups, down alone).
+the LLaMA-350M layers (q|k|v and gate|up input groups, down alone) and the
+LLaMA-1B layers of width 5461 (a K that is not a multiple of 8, whose last
+16-byte chunk the kernel clears past K; odd output widths, whose last column
+goes out alone).
 
 Each element is held to a bound, beside the relative Frobenius error: the
 output rounding plus a probabilistic accumulation bound (gpu_util); a wrong
@@ -34,12 +37,17 @@ FWD = [
     (16384 + 77, 1024, (1024, 1024, 1024), (128, 128, 128)),
     (16384 + 77, 1024, (2736, 2736), (128, 128)),
     (32768 + 77, 2736, (1024,), (342,)),
+    # LLaMA-1B widths of 5461: K % 8 != 0 (down), odd output widths (gate, z of down)
+    (16384 + 77, 5461, (2048,), (1365,)),
+    (8192 + 77, 2048, (5461,), (512,)),
 ]
 # dx = dL/do W^T has n output columns: more tokens for three tiles per CU
 DX = [
     (49152 + 77, 1024, (1024, 1024, 1024), (128, 128, 128)),
     (32768 + 77, 2736, (1024,), (342,)),
     (49152 + 77, 1024, (2736, 2736), (128, 128)),
+    (12288 + 77, 5461, (2048,), (1365,)),     # odd output width (dL/dx of down)
+    (24576 + 77, 2048, (5461,), (512,)),      # K % 8 != 0 (dL/dx of gate)
 ]
 
 
