@@ -1,14 +1,15 @@
 """Oracle for the CompAct linear layer in fp64 — test infrastructure only.
 
-Each function follows one passage of the paper (CompAct, §3.2 and §3.3):
+Each function states one part of the method (CompAct, §3.2 and §3.3):
 
-* ``ref_fwd``   Alg. 1: o = x W and the saved activation z = x P.
-* ``ref_bwd``   Alg. 2: G^ = z^T dL/do (r x m) and dL/dx = dL/do W^T.
-* ``ref_adam``  Alg. 3, first block: Adam moments on the r x m compressed
-                gradient, bias correction, N = M^ / (sqrt(V^) + eps).
-* ``ref_step``  Alg. 3: ref_adam, then W <- W - lr * alpha * P N with P
-                re-sampled from the layer seed.
-* ``next_seed`` Alg. 3, end: t <- t + 1 and the seed advances every T steps.
+* ``ref_fwd``   forward (Alg. 1): the output x W and the kept activation x P.
+* ``ref_bwd``   backward (Alg. 2): the input gradient and the compressed
+                weight gradient z^T dL/do (r x m).
+* ``ref_adam``  Adam on the compressed gradient (Alg. 3): moments and the
+                bias-corrected, normalised direction.
+* ``ref_step``  the update (Alg. 3): the direction mapped back through the
+                re-drawn P, scaled by alpha and the learning rate.
+* ``next_seed`` the re-sampling schedule (end of Alg. 3).
 * ``memory_elements`` Table 1, CompAct column.
 
 Readings where the paper is silent or inconsistent:
@@ -40,62 +41,68 @@ def _f64(a):
 
 
 def ref_fwd(x, W, seed: int, r: int, identity: bool = False, sparse_s: int = 0):
-    """Alg. 1.  x: (T, n), W: (n, m) -> (o (T, m), z (T, r)).  sparse_s > 0
-    takes the sparse JL projection with that many draws per row (§5)."""
+    """Forward of the compressed layer (§3.2, Alg. 1): the layer output x W and
+    the activation kept for the backward pass, x P, with P drawn from the layer
+    seed (§3.3).  x: (T, n), W: (n, m) -> ((T, m), (T, r)).  sparse_s > 0 takes
+    the sparse JL projection with that many draws per row (§5)."""
     x, W = _f64(x), _f64(W)
-    n = x.shape[1]
-    P = projection(seed, n, r, identity, sparse_s)
-    o = x @ W
-    z = x @ P
-    return o, z
+    proj = projection(seed, x.shape[1], r, identity, sparse_s)
+    return x @ W, x @ proj
 
 
 def ref_bwd(dy, z, W):
-    """Alg. 2.  dy: (T, m), z: (T, r), W: (n, m) -> (dx (T, n), Ghat (r, m))."""
+    """Backward of the compressed layer (§3.2, Alg. 2): the input gradient
+    dL/do W^T (exact, P does not enter it) and the weight gradient in the
+    projected space, z^T dL/do.  dy: (T, m), z: (T, r), W: (n, m) ->
+    ((T, n), (r, m))."""
     dy, z, W = _f64(dy), _f64(z), _f64(W)
-    Ghat = z.T @ dy
-    dx = dy @ W.T
-    return dx, Ghat
+    return dy @ W.T, z.T @ dy
 
 
 def ref_adam(Ghat, M, V, t: int, beta1: float, beta2: float, eps: float):
-    """Alg. 3 moments.  Returns (M_t, V_t, N_t) with M_t, V_t uncorrected."""
+    """Adam on the r x m compressed gradient (§3.2; the bias-corrected form of
+    Alg. 3): exponential averages of the gradient and of its square, and the
+    normalised step direction built from their bias-corrected values.
+    Returns (first moment, second moment, direction); the stored moments are
+    the uncorrected averages.  t is the 1-based step index."""
     if t < 1:
         raise ValueError("step index t is 1-based")
-    G, M, V = _f64(Ghat), _f64(M), _f64(V)
+    g, mean, sq = _f64(Ghat), _f64(M), _f64(V)
     b1, b2 = F64(beta1), F64(beta2)
-    M_t = b1 * M + (F64(1) - b1) * G
-    V_t = b2 * V + (F64(1) - b2) * G * G
-    M_hat = M_t / (F64(1) - b1 ** t)
-    V_hat = V_t / (F64(1) - b2 ** t)
-    N_t = M_hat / (np.sqrt(V_hat) + F64(eps))
-    return M_t, V_t, N_t
+    mean = b1 * mean + (F64(1) - b1) * g
+    sq = b2 * sq + (F64(1) - b2) * g * g
+    mean_unbiased = mean / (F64(1) - b1 ** t)
+    sq_unbiased = sq / (F64(1) - b2 ** t)
+    return mean, sq, mean_unbiased / (np.sqrt(sq_unbiased) + F64(eps))
 
 
 def ref_step(W, Ghat, M, V, seed: int, r: int, t: int, lr: float, beta1: float,
              beta2: float, eps: float, alpha: float, identity: bool = False,
              rho: str = "adam", sparse_s: int = 0):
-    """Alg. 3.  Returns (W_{t+1}, M_t, V_t, dW) with dW = W_{t+1} - W_t.
+    """One optimizer step of the compressed layer (§3.2, Alg. 3): the Adam
+    direction in the projected space is mapped back to the weight space by
+    the same P as the forward (re-drawn from the seed, §3.3), scaled by alpha
+    and the learning rate, and subtracted from W.
+    Returns (new W, first moment, second moment, the change of W).
 
-    ``rho="sgd"`` replaces the Adam normalisation by the identity (N = G^);
-    it exists only to test the unbiasedness of the decompression."""
+    ``rho="sgd"`` uses the compressed gradient itself as the direction; it
+    exists only to test that the decompressed update is unbiased."""
     W = _f64(W)
-    n = W.shape[0]
     if rho == "adam":
-        M_t, V_t, N_t = ref_adam(Ghat, M, V, t, beta1, beta2, eps)
+        mean, sq, direction = ref_adam(Ghat, M, V, t, beta1, beta2, eps)
     elif rho == "sgd":
-        M_t, V_t, N_t = _f64(M), _f64(V), _f64(Ghat)
+        mean, sq, direction = _f64(M), _f64(V), _f64(Ghat)
     else:
         raise ValueError(rho)
-    P = projection(seed, n, r, identity, sparse_s)
-    G_tilde = F64(alpha) * (P @ N_t)
-    dW = -F64(lr) * G_tilde
-    return W + dW, M_t, V_t, dW
+    proj = projection(seed, W.shape[0], r, identity, sparse_s)
+    change = -F64(lr) * (F64(alpha) * (proj @ direction))
+    return W + change, mean, sq, change
 
 
 def next_seed(seed: int, t: int, T: int):
-    """Alg. 3 schedule.  ``t`` is the 1-based index of the step just taken with
-    ``seed``; returns the seed for step t + 1.  T <= 0 means never re-seed."""
+    """The re-sampling schedule (§3.3, end of Alg. 3): after the step with
+    1-based index ``t``, the layer moves to the next seed (a new P) when t is
+    a multiple of the period T; T <= 0 keeps one P for the whole run."""
     if t < 1:
         raise ValueError("step index t is 1-based")
     seed = int(seed)
