@@ -191,17 +191,22 @@ size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t
  *      r[j] but the last a multiple of 8), count 1 .. 8
  *   ws, ws_bytes  workspace of at least
  *      compact_bwd_group_workspace_bytes(tokens, n, count, m, r, dtype) bytes
+ *   accumulate  0: G[j] = G^_j;  1: G[j] = G[j] + G^_j (gradient accumulation
+ *      over several backward passes before one optimizer step: the sum over
+ *      the splits is formed first and added to G[j] in one fp32 addition, so
+ *      the result is bitwise G[j] + (the G^_j of accumulate = 0))
  * bf16: one dx GEMM, then one split-K launch for every G^_j (one grid of about
  * one workgroup per CU over all projections) and one reduction launch; the
  * splits are summed in a fixed order, so each G^_j is deterministic (it may
  * differ in the last bits from compact_bwd on the slices, whose token splits
  * differ).  dx is bitwise compact_bwd's.  fp32: compact_bwd per slice.
- * Errors: COMPACT_EINVAL, COMPACT_EALIGN, COMPACT_EWORKSPACE, COMPACT_EHIP;
- * nothing is launched on a validation error.
+ * Errors: COMPACT_EINVAL (also accumulate not 0 or 1), COMPACT_EALIGN,
+ * COMPACT_EWORKSPACE, COMPACT_EHIP; nothing is launched on a validation error.
  */
 int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
                       void* dx, int64_t lddx, float* const* G, int64_t tokens, int64_t n, int32_t count,
-                      const int64_t* m, const int64_t* r, int dtype, void* ws, size_t ws_bytes, void* stream);
+                      const int64_t* m, const int64_t* r, int dtype, int accumulate, void* ws, size_t ws_bytes,
+                      void* stream);
 
 size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t count, const int64_t* m,
                                          const int64_t* r, int dtype);

@@ -189,12 +189,13 @@ def bwd_group_workspace_bytes(tokens, n, ms, rs, dtype=BF16):
     return int(_lib.load().compact_bwd_group_workspace_bytes(int(tokens), int(n), count, m_arr, r_arr, dtype))
 
 
-def compact_bwd_group(dy, W, z, dx, Gs, ms, rs, ws=None, stream=None):
+def compact_bwd_group(dy, W, z, dx, Gs, ms, rs, ws=None, stream=None, accumulate=False):
     """Alg. 2 for the projections of an input group: dx = dy W^T over the
     concatenated weight W = [W_0 | W_1 | ...] (the sum over the projections)
     and G^_j = z_j^T dy_j for column slices dy_j (sum(ms[:j]) ..) and z_j
     (sum(rs[:j]) ..), one split-K launch for all of them.  dx or Gs may be
-    None; Gs is a list of contiguous (r_j, m_j) fp32 tensors."""
+    None; Gs is a list of contiguous (r_j, m_j) fp32 tensors, overwritten, or
+    with accumulate=True increased by G^_j (gradient accumulation)."""
     import ctypes
     lib = _lib.load()
     T = dy.shape[0]
@@ -210,7 +211,8 @@ def compact_bwd_group(dy, W, z, dx, Gs, ms, rs, ws=None, stream=None):
         g_arr = (ctypes.c_void_p * count)(*[G.data_ptr() for G in Gs])
     wp, wb = _ws(ws)
     st = lib.compact_bwd_group(_ptr(dy), _ld(dy), _ptr(W), _ld(W), _ptr(z), _ld(z), _ptr(dx), _ld(dx), g_arr, T,
-                               n, count, m_arr, r_arr, _dtype_code(dy), wp, wb, _stream(stream, dy))
+                               n, count, m_arr, r_arr, _dtype_code(dy), 1 if accumulate else 0, wp, wb,
+                               _stream(stream, dy))
     _check("compact_bwd_group", st)
 
 

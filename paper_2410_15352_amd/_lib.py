@@ -26,7 +26,7 @@ SIGNATURES = {
                                     c_i64, c_i64, c_i64, c_int, c_vp]),
     "compact_bwd_group": (c_int, [c_vp, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp, c_i64,
                                   ctypes.POINTER(c_vp), c_i64, c_i64, ctypes.c_int32, ctypes.POINTER(c_i64),
-                                  ctypes.POINTER(c_i64), c_int, c_vp, c_size, c_vp]),
+                                  ctypes.POINTER(c_i64), c_int, c_int, c_vp, c_size, c_vp]),
     "compact_bwd_group_workspace_bytes": (c_size, [c_i64, c_i64, ctypes.c_int32, ctypes.POINTER(c_i64),
                                                    ctypes.POINTER(c_i64), c_int]),
     "compact_step": (c_int, [c_vp, c_i64, c_vp, c_vp, c_vp, c_i64, c_i64, c_i64, c_u64, c_i64,

@@ -175,13 +175,13 @@ int64_t pt_ld(int64_t n) { return round_up(n, kBK); }
 
 // G[j][c] = sum over splits, in order, of part[s][j][c].
 int launch_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t plane, int64_t r, int64_t m, float* G,
-                         hipStream_t s) {
+                         int accumulate, hipStream_t s) {
   if (m % 4 == 0 && aligned16(G)) {
     hipLaunchKernelGGL(k_splitk_reduce4, dim3(static_cast<uint32_t>(ceil_div(r * (m / 4), 256))), dim3(256), 0, s,
-                       part, splits, ldp, plane, r, m, G);
+                       part, splits, ldp, plane, r, m, G, accumulate);
   } else {
     hipLaunchKernelGGL(k_splitk_reduce, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s, part,
-                       splits, ldp, plane, r, m, G);
+                       splits, ldp, plane, r, m, G, accumulate);
   }
   return check_launch("G^ reduce");
 }
@@ -190,9 +190,10 @@ int launch_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t pla
 // the layer table and one reduction launch.  z[j], dy[j] may be column slices.
 int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const* z, const int64_t* ldz,
                       const void* const* dy, const int64_t* lddy, float* const* G, const int64_t* r,
-                      const int64_t* m, void* ws, hipStream_t s) {
+                      const int64_t* m, int accumulate, void* ws, hipStream_t s) {
   GhatW4Params p{};
   ReduceBatch rb{};
+  rb.accumulate = accumulate;
   char* base = static_cast<char*>(align_ws(ws));
   p.count = rb.count = g.count;
   p.T = static_cast<int>(tokens);
@@ -566,9 +567,14 @@ int compact_fwd_group(const void* x, int64_t ldx, const void* W, int64_t ldw, vo
   return ok();
 }
 
-int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
-                int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
-                int64_t m, int64_t r, int dtype, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Alg. 2 for one projection; accumulate: G <- G + z^T dL/do.
+int bwd_impl(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz, void* dx,
+             int64_t lddx, float* G, int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype, int accumulate,
+             void* ws, size_t ws_bytes, void* stream) {
   int st;
   if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
   if ((st = check_shape(tokens, n, m, r, COMPACT_PROJ_GAUSSIAN))) return st;
@@ -587,7 +593,7 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (tokens == 0) {
-    if (G != nullptr) {
+    if (G != nullptr && !accumulate) {  // a sum over no tokens
       hipLaunchKernelGGL(k_fill_f32, dim3(static_cast<uint32_t>(ceil_div(r * m, 256))), dim3(256), 0, s, G, r * m, 0.0f);
       if ((st = check_launch("zero G"))) return st;
     }
@@ -607,7 +613,7 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
       GemmF32Params gp{};
       gp.A = mem_operand(static_cast<const float*>(z), 1, ldz, r, tokens);
       gp.B = mem_operand(static_cast<const float*>(dy), lddy, 1, tokens, m);
-      gp.M = r; gp.N = m; gp.K = tokens; gp.mode = 0;
+      gp.M = r; gp.N = m; gp.K = tokens; gp.mode = accumulate ? 2 : 0;
       gp.out = G; gp.ldo = m; gp.scale = 1.0f;
       if ((st = launch_gemm_f32(gp, s, "G^ (fp32)"))) return st;
     }
@@ -655,7 +661,7 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
   }
   const GhatGroupPlan gp = ghat_group_plan(tokens, 1, &r, &m);
   if (G != nullptr && ghat_w4_eligible(gp, tokens, ldz, lddy)) {
-    if ((st = launch_ghat_group(gp, tokens, &z, &ldz, &dy, &lddy, &G, &r, &m, ws, s))) return st;
+    if ((st = launch_ghat_group(gp, tokens, &z, &ldz, &dy, &lddy, &G, &r, &m, accumulate, ws, s))) return st;
   } else if (G != nullptr) {
     const SplitPlan sp = ghat_plan(tokens, r, m);
     GhatParams p{};
@@ -669,9 +675,19 @@ int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const 
                        dim3(kGThreads), kGhatLds, s, p);
     if ((st = check_launch("G^ split-K (bf16)"))) return st;
     const int64_t ldp = int64_t(sp.tiles_m) * kGBN, plane = int64_t(sp.tiles_r) * kGBM * ldp;
-    if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, s))) return st;
+    if ((st = launch_splitk_reduce(p.part, sp.splits, ldp, plane, r, m, G, accumulate, s))) return st;
   }
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
+                int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
+                int64_t m, int64_t r, int dtype, void* ws, size_t ws_bytes, void* stream) {
+  return bwd_impl(dy, lddy, W, ldw, z, ldz, dx, lddx, G, tokens, n, m, r, dtype, 0, ws, ws_bytes, stream);
 }
 
 size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t count, const int64_t* m,
@@ -693,8 +709,10 @@ size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t coun
 
 int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
                       void* dx, int64_t lddx, float* const* G, int64_t tokens, int64_t n, int32_t count,
-                      const int64_t* m, const int64_t* r, int dtype, void* ws, size_t ws_bytes, void* stream) {
+                      const int64_t* m, const int64_t* r, int dtype, int accumulate, void* ws, size_t ws_bytes,
+                      void* stream) {
   int st;
+  if (accumulate != 0 && accumulate != 1) return fail(COMPACT_EINVAL, "accumulate must be 0 or 1");
   if (!valid_dtype(dtype)) return fail(COMPACT_EINVAL, "unknown dtype %d", dtype);
   if (count < 1 || count > kGhMaxLayers) return fail(COMPACT_EINVAL, "group of %d projections (1 .. %d)", count, kGhMaxLayers);
   if (m == nullptr || r == nullptr) return fail(COMPACT_EINVAL, "m or r array is NULL");
@@ -742,14 +760,15 @@ int compact_bwd_group(const void* dy, int64_t lddy, const void* W, int64_t ldw, 
   }
   const GhatGroupPlan gp = ghat_group_plan(tokens, count, r, m);
   if (dtype == COMPACT_BF16 && tokens > 0 && ghat_w4_eligible(gp, tokens, ldz, lddy)) {
-    if ((st = launch_ghat_group(gp, tokens, zs, ldzs, dys, lddys, G, r, m, ws, static_cast<hipStream_t>(stream))))
+    if ((st = launch_ghat_group(gp, tokens, zs, ldzs, dys, lddys, G, r, m, accumulate, ws,
+                                static_cast<hipStream_t>(stream))))
       return st;
     return ok();
   }
   // otherwise G^ of each projection on its own
   for (int j = 0; j < count; ++j)
-    if ((st = compact_bwd(dys[j], lddy, nullptr, ldw, zs[j], ldz, nullptr, lddx, G[j], tokens, n, m[j], r[j], dtype,
-                          ws, ws_bytes, stream)))
+    if ((st = bwd_impl(dys[j], lddy, nullptr, ldw, zs[j], ldz, nullptr, lddx, G[j], tokens, n, m[j], r[j], dtype,
+                       accumulate, ws, ws_bytes, stream)))
       return st;
   return ok();
 }

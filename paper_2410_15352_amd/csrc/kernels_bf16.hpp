@@ -285,10 +285,11 @@ __global__ __launch_bounds__(WGM* WGN* kWave, occupancy_for(BM, BN, WGM, WGN)) v
   for_each_acc(acc, lane, [&](int row, int col, float v) { out[(r0 + row) * ldp + c0 + col] = v; });
 }
 
-// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c];
-// four consecutive columns per thread (m % 4 == 0), else one.
+// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c]
+// (accumulate: G[j][c] + that sum, one addition at the end); four consecutive
+// columns per thread (m % 4 == 0), else one.
 __global__ void k_splitk_reduce4(const float* part, int splits, int64_t ldp, int64_t plane,
-                                 int64_t r, int64_t m, float* G) {
+                                 int64_t r, int64_t m, float* G, int accumulate) {
   const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t mq = m / 4;
   if (q >= r * mq) return;
@@ -317,7 +318,15 @@ __global__ void k_splitk_reduce4(const float* part, int splits, int64_t ldp, int
     s.z = s.z + v.z;
     s.w = s.w + v.w;
   }
-  *reinterpret_cast<f32x4*>(G + j * m + c) = s;
+  f32x4* dst = reinterpret_cast<f32x4*>(G + j * m + c);
+  if (accumulate) {
+    const f32x4 g = *dst;
+    s.x = g.x + s.x;
+    s.y = g.y + s.y;
+    s.z = g.z + s.z;
+    s.w = g.w + s.w;
+  }
+  *dst = s;
 }
 
 // The reduction for several projections in one launch (one G^ split-K launch
@@ -334,6 +343,7 @@ struct ReduceLayer {
 
 struct ReduceBatch {
   int count, splits;
+  int accumulate;  // G + the sum instead of the sum
   int begin[9];  // first workgroup of each layer; begin[count] = grid
   ReduceLayer layer[8];
 };
@@ -368,25 +378,33 @@ __global__ void k_splitk_reduce_batched(ReduceBatch b) {
   }
   float* dst = p.G + j * p.m + c;
   if (p.vec) {
+    if (b.accumulate) {
+      const f32x4 g = *reinterpret_cast<const f32x4*>(dst);
+      s.x = g.x + s.x;
+      s.y = g.y + s.y;
+      s.z = g.z + s.z;
+      s.w = g.w + s.w;
+    }
     *reinterpret_cast<f32x4*>(dst) = s;
   } else {
     const float e[4] = {s.x, s.y, s.z, s.w};
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      if (c + u < p.m) dst[u] = e[u];
+      if (c + u < p.m) dst[u] = b.accumulate ? dst[u] + e[u] : e[u];
   }
 }
 
-// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c].
+// G[j][c] = sum over s = 0 .. splits-1 (in this order) of part[s][j][c]
+// (accumulate: G[j][c] + that sum).
 __global__ void k_splitk_reduce(const float* part, int splits, int64_t ldp, int64_t plane,
-                                int64_t r, int64_t m, float* G) {
+                                int64_t r, int64_t m, float* G, int accumulate) {
   const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (e >= r * m) return;
   const int64_t j = e / m, c = e % m;
   const float* src = part + j * ldp + c;
   float s = 0.0f;
   for (int k = 0; k < splits; ++k) s += src[k * plane];
-  G[e] = s;
+  G[e] = accumulate ? G[e] + s : s;
 }
 
 }  // namespace compact

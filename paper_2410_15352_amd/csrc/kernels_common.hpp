@@ -241,7 +241,7 @@ __device__ __forceinline__ float operand_elem(const OperandF32& o, int64_t u, in
 }
 
 // C (M x N) = A (M x K) B (K x N).  mode 0: out = scale * C;  mode 1 (update):
-// out = out - coef * C.
+// out = out - coef * C;  mode 2 (accumulate): out = out + C.
 struct GemmF32Params {
   OperandF32 A, B;
   int64_t M, N, K;
@@ -284,6 +284,8 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32Params p) {
       float* o = p.out + gr * p.ldo + gc;
       if (p.mode == 0) {
         *o = p.scale * acc[a][b];
+      } else if (p.mode == 2) {
+        *o = *o + acc[a][b];
       } else {
         const float d = p.coef * acc[a][b];
         *o = *o - d;

@@ -92,13 +92,12 @@ class _GroupFn(torch.autograd.Function):
         if ctx.needs_input_grad[0]:
             dx = _empty2d(T, mod.n, torch.bfloat16, dy.device)
         # Alg. 2 for the whole group in one call: dL/dx summed over the
-        # projections (one GEMM over the concatenated weight) and every G^_j
-        targets = [g if not mod.grad_ready else torch.empty_like(g) for g in mod.ghat]
+        # projections (one GEMM over the concatenated weight) and every G^_j,
+        # added to the G^ of earlier backward passes until zero_grad (the
+        # library's accumulate mode)
         ws = WorkspacePool.get(dy.device, "bwd", bwd_group_workspace_bytes(T, mod.n, mod.ms, mod.rs))
-        compact_bwd_group(dy, mod.weight if dx is not None else None, z, dx, targets, mod.ms, mod.rs, ws=ws)
-        if mod.grad_ready:
-            for g, t in zip(mod.ghat, targets):
-                g.add_(t)  # gradient accumulation: G^ is linear in dL/do
+        compact_bwd_group(dy, mod.weight if dx is not None else None, z, dx, mod.ghat, mod.ms, mod.rs, ws=ws,
+                          accumulate=mod.grad_ready)
         mod.grad_ready = True
         return dx, None, None
 

@@ -192,17 +192,18 @@ def test_bwd_group_workspace_size(lib):
     (dict(G=(FAKE, None, FAKE)), -1),
     (dict(G=(FAKE, FAKE + 4, FAKE)), -2),
     (dict(ws=None), -4), (dict(ws_bytes=64), -4),
+    (dict(accumulate=2), -1),
 ])
 def test_bwd_group_validation(lib, kw, status):
     a = dict(dy=FAKE, lddy=3072, W=FAKE, ldw=3072, z=FAKE, ldz=384, dx=FAKE, lddx=1024, G=(FAKE, FAKE, FAKE),
-             tokens=4096, n=1024, count=3, m=(1024, 1024, 1024), r=(128, 128, 128), dtype=1, ws=FAKE,
+             tokens=4096, n=1024, count=3, m=(1024, 1024, 1024), r=(128, 128, 128), dtype=1, accumulate=0, ws=FAKE,
              ws_bytes=1 << 40, stream=None)
     a.update(kw)
     arr = lambda v, t: None if v is None else (t * len(v))(*v)
     st = lib.compact_bwd_group(a["dy"], a["lddy"], a["W"], a["ldw"], a["z"], a["ldz"], a["dx"], a["lddx"],
                                arr(a["G"], ctypes.c_void_p), a["tokens"], a["n"], a["count"],
-                               arr(a["m"], ctypes.c_int64), arr(a["r"], ctypes.c_int64), a["dtype"], a["ws"],
-                               a["ws_bytes"], a["stream"])
+                               arr(a["m"], ctypes.c_int64), arr(a["r"], ctypes.c_int64), a["dtype"],
+                               a["accumulate"], a["ws"], a["ws_bytes"], a["stream"])
     assert st == status
     assert lib.compact_last_error()
 

@@ -161,14 +161,13 @@ def test_ghat_and_step_on_overhanging_column_slices():
     assert torch.equal(W_all[:, :m].contiguous().view(torch.int16), to_dev(W_a, "bf16").view(torch.int16))
 
 
-def _bwd_group_inputs(T, n, ms, rs, data_seed):
-    parts = [bwd_inputs(T, n, m, r, "bf16", data_seed=data_seed + j) for j, (m, r) in enumerate(zip(ms, rs))]
+def _bwd_group_inputs(T, n, ms, rs, data_seed, dt="bf16"):
+    parts = [bwd_inputs(T, n, m, r, dt, data_seed=data_seed + j) for j, (m, r) in enumerate(zip(ms, rs))]
     M, R = sum(ms), sum(rs)
     dy_all = np.concatenate([p[0] for p in parts], axis=1)
     z_all = np.concatenate([p[1] for p in parts], axis=1)
     W_all = np.concatenate([p[2] for p in parts], axis=1)
-    dev_t = (to_dev(dy_all, "bf16", ld_for(M, "bf16")), to_dev(z_all, "bf16", ld_for(R, "bf16")),
-             to_dev(W_all, "bf16", ld_for(M, "bf16")))
+    dev_t = (to_dev(dy_all, dt, ld_for(M, dt)), to_dev(z_all, dt, ld_for(R, dt)), to_dev(W_all, dt, ld_for(M, dt)))
     return parts, dev_t
 
 
@@ -237,11 +236,46 @@ def test_bwd_group_parts_and_empty():
     lib = cp.library()
     st = lib.compact_bwd_group(dyd.data_ptr(), dyd.stride(0), None, 0, zd.data_ptr(), zd.stride(0), None, 0,
                                (ctypes.c_void_p * 3)(*[G.data_ptr() for G in G0]), 0, n, 3,
-                               (ctypes.c_int64 * 3)(*ms), (ctypes.c_int64 * 3)(*rs), 1, ws.data_ptr(), ws.numel(),
+                               (ctypes.c_int64 * 3)(*ms), (ctypes.c_int64 * 3)(*rs), 1, 0, ws.data_ptr(), ws.numel(),
+                               torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    # zero tokens with accumulate: G^ + (a sum over no tokens) leaves G^ as it is
+    G1 = [torch.full((r, m), 3.0, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    st = lib.compact_bwd_group(dyd.data_ptr(), dyd.stride(0), None, 0, zd.data_ptr(), zd.stride(0), None, 0,
+                               (ctypes.c_void_p * 3)(*[G.data_ptr() for G in G1]), 0, n, 3,
+                               (ctypes.c_int64 * 3)(*ms), (ctypes.c_int64 * 3)(*rs), 1, 1, ws.data_ptr(), ws.numel(),
                                torch.cuda.current_stream().cuda_stream)
     assert st == 0
     torch.cuda.synchronize()
+    assert all(bool((G == 3.0).all()) for G in G1)
     assert oc.rel_fro(to_np(dx), sum(oc.ref_bwd(p[0], p[1], p[2])[0] for p in parts)) <= TOL
     for G, p in zip(Gs, parts):
         assert oc.rel_fro(G.cpu().numpy(), oc.ref_bwd(p[0], p[1], p[2])[1]) <= TOL
     assert all(float(G.abs().max()) == 0.0 for G in G0)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("T", [513, 16384 + 77])
+def test_bwd_group_accumulate(T, dt):
+    # gradient accumulation in the library: G^ <- G^ + z^T dL/do is bitwise
+    # G^ + (the G^ of a fresh call), one fp32 addition per element, on the
+    # bf16 path (one split-K launch; T = 16461 takes several splits) and the
+    # fp32 one; against the oracle for two backward passes in a row
+    n, ms, rs = 512, (512, 512, 512), (128, 128, 128)
+    parts1, (dy1, z1, Wd) = _bwd_group_inputs(T, n, ms, rs, data_seed=11, dt=dt)
+    parts2, (dy2, z2, _) = _bwd_group_inputs(T, n, ms, rs, data_seed=12, dt=dt)
+    code = cp.BF16 if dt == "bf16" else cp.F32
+    ws = workspace(cp.bwd_group_workspace_bytes(T, n, ms, rs, code)) if dt == "bf16" else None
+    fresh = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    acc = [torch.empty(r, m, dtype=torch.float32, device=dev()) for m, r in zip(ms, rs)]
+    cp.compact_bwd_group(dy1, None, z1, None, acc, ms, rs, ws=ws)                    # first pass
+    prev = [g.clone() for g in acc]
+    cp.compact_bwd_group(dy2, None, z2, None, acc, ms, rs, ws=ws, accumulate=True)   # second pass, added
+    cp.compact_bwd_group(dy2, None, z2, None, fresh, ms, rs, ws=ws)
+    torch.cuda.synchronize()
+    for a, p, f in zip(acc, prev, fresh):
+        assert torch.equal(a, p + f)
+    tol = TOL if dt == "bf16" else 1e-5
+    for a, q1, q2 in zip(acc, parts1, parts2):
+        ref = oc.ref_bwd(q1[0], q1[1], q1[2])[1] + oc.ref_bwd(q2[0], q2[1], q2[2])[1]
+        assert oc.rel_fro(a.cpu().numpy(), ref) <= tol
