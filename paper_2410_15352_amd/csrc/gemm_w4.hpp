@@ -383,10 +383,24 @@ __device__ __forceinline__ W4Out w4_out_desc(const W4Gemm& g, const W4Lane& L, c
 // column lane % 32) converted to bf16 pairs: raw[(b * 4 + gr) * 2] holds rows
 // + 0, + 1 and raw[... + 1] rows + 2, + 3.
 __device__ __forceinline__ void w4_convert_block(const f32x16& a, int b, uint32_t (&raw)[128]) {
+  // The accumulators are read out one block at a time, each block after the
+  // previous one is converted (the first read takes that block's last value
+  // as an input).  Left to itself the compiler reads 13 of the 16 blocks out
+  // of the accumulator registers before converting any: 208 VGPRs at once,
+  // the peak that made the K % 8 != 0 variants spill.
+  float v[16];
+  const uint32_t dep = b > 0 ? raw[b * 8 - 1] : 0u;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    if (e == 0)
+      asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(a[e]), "v"(dep));
+    else
+      asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(a[e]));
+  }
 #pragma unroll
   for (int gr = 0; gr < 4; ++gr) {
-    raw[(b * 4 + gr) * 2] = pack_bf16x2(a[4 * gr + 0], a[4 * gr + 1]);
-    raw[(b * 4 + gr) * 2 + 1] = pack_bf16x2(a[4 * gr + 2], a[4 * gr + 3]);
+    raw[(b * 4 + gr) * 2] = pack_bf16x2(v[4 * gr + 0], v[4 * gr + 1]);
+    raw[(b * 4 + gr) * 2 + 1] = pack_bf16x2(v[4 * gr + 2], v[4 * gr + 3]);
   }
 }
 
