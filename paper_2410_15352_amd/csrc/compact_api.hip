@@ -117,25 +117,37 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
 }
 
 // Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp) for one or
-// more projections of the same tokens (one launch): 128 x 256 tiles, one split
-// count for all of them, at most one workgroup per CU (256 on MI355X), splits
-// of whole 32-token K tiles.  Projection j's partial sums take
-// splits x (tiles_r 128) x (tiles_m 256) fp32 at byte offset part_off[j].
+// more projections of the same tokens (one launch): tm x tn tiles (128 x 256,
+// or 384 x 128 when every projection of the launch has 256 < r and 384-row
+// tiles pad r no further than 128-row ones), one split count for all of them,
+// at most one workgroup per CU (256 on MI355X), splits of whole 32-token K
+// tiles.  Projection j's partial sums take splits x (tiles_r tm) x
+// (tiles_m tn) fp32 at byte offset part_off[j].
 struct GhatGroupPlan {
   int count;
+  int tall, tm, tn;
   int tiles_r[kGhMaxLayers], tiles_m[kGhMaxLayers];
   int tiles, splits;
   int64_t split_len;
   size_t part_off[kGhMaxLayers], bytes;
 };
 
+bool ghat_tall_fits(int64_t r) {
+  return r > 256 && round_up(r, kGhTallTm) <= round_up(r, kGhTm);
+}
+
 GhatGroupPlan ghat_group_plan(int64_t tokens, int count, const int64_t* r, const int64_t* m) {
   GhatGroupPlan g{};
   g.count = count;
+  g.tall = count > 0 ? 1 : 0;
+  for (int j = 0; j < count; ++j)
+    if (!ghat_tall_fits(r[j])) g.tall = 0;
+  g.tm = g.tall ? kGhTallTm : kGhTm;
+  g.tn = g.tall ? kGhTallTn : kGhTn;
   int64_t tiles = 0;
   for (int j = 0; j < count; ++j) {
-    g.tiles_r[j] = static_cast<int>(ceil_div(r[j], kGhTm));
-    g.tiles_m[j] = static_cast<int>(ceil_div(m[j], kGhTn));
+    g.tiles_r[j] = static_cast<int>(ceil_div(r[j], g.tm));
+    g.tiles_m[j] = static_cast<int>(ceil_div(m[j], g.tn));
     tiles += int64_t(g.tiles_r[j]) * g.tiles_m[j];
   }
   g.tiles = static_cast<int>(tiles);
@@ -148,7 +160,7 @@ GhatGroupPlan ghat_group_plan(int64_t tokens, int count, const int64_t* r, const
   size_t off = 0;
   for (int j = 0; j < count; ++j) {
     g.part_off[j] = off;
-    const size_t b = size_t(g.splits) * size_t(g.tiles_r[j]) * kGhTm * size_t(g.tiles_m[j]) * kGhTn * sizeof(float);
+    const size_t b = size_t(g.splits) * size_t(g.tiles_r[j]) * g.tm * size_t(g.tiles_m[j]) * g.tn * sizeof(float);
     off += size_t(round_up(static_cast<int64_t>(b), kWsAlign));
   }
   g.bytes = off;
@@ -199,6 +211,7 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
   p.T = static_cast<int>(tokens);
   p.splits = rb.splits = g.splits;
   p.split_len = static_cast<int>(g.split_len);
+  p.tall = g.tall;
   int tb = 0, rbk = 0;
   for (int j = 0; j < g.count; ++j) {
     GhatW4Layer& L = p.layer[j];
@@ -212,8 +225,8 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
     ReduceLayer& R = rb.layer[j];
     R.part = L.part;
     R.G = G[j];
-    R.ldp = int64_t(g.tiles_m[j]) * kGhTn;
-    R.plane = int64_t(g.tiles_r[j]) * kGhTm * R.ldp;
+    R.ldp = int64_t(g.tiles_m[j]) * g.tn;
+    R.plane = int64_t(g.tiles_r[j]) * g.tm * R.ldp;
     R.r = L.r; R.m = L.m;
     R.mq = static_cast<int>(ceil_div(m[j], 4));
     R.vec = (m[j] % 4 == 0 && aligned16(G[j])) ? 1 : 0;

@@ -4,29 +4,37 @@
 // K rows and read back as MFMA fragments with the transposing LDS read
 // ds_read_b64_tr_b16.
 //
-// Workgroup: 4 waves, output tile 128 (rows of G^) x 256 (columns), each
-// wave 64 x 128 (2 x 4 MFMA 32x32x16 fragments), over one range of tokens
-// (a split); the fp32 partial tile goes to part[split] and a separate kernel
-// sums the splits in a fixed order (deterministic G^).  One launch covers up
-// to 8 projections of the same tokens (a layer table): the projections of an
-// input group then share one grid of about one workgroup per CU, with fewer
-// and longer splits than a launch per projection would have.
+// Workgroup: 4 waves over one range of tokens (a split), two tile shapes:
+//   128 x 256 (rows of G^ x columns): waves 2 x 2, each 64 x 128 (2 x 4 MFMA
+//     32x32x16 fragments), 6 fragment reads per 8 MFMAs;
+//   384 x 128 ("tall", for 256 < r <= 384 and other r that 384-row tiles
+//     cover without more padding than 128-row ones, e.g. the down projection
+//     at r = 342): waves stacked along the rows, each 96 x 128 (3 x 4
+//     fragments), 7 fragment reads per 12 MFMAs; every column of dL/do is
+//     then copied and read by one tile instead of by each of three.
+// The fp32 partial tile goes to part[split] and a separate kernel sums the
+// splits in a fixed order (deterministic G^).  One launch covers up to 8
+// projections of the same tokens (a layer table): the projections of an input
+// group then share one grid of about one workgroup per CU, with fewer and
+// longer splits than a launch per projection would have.
 //
 // Pipeline as in gemm_w4.hpp: 32-token K tiles, four LDS stages, copies by
 // buffer_load_dwordx4 ... lds issued 3 K tiles ahead (six stages, 5 ahead, time
 // the same) and spread over the MFMAs, one barrier per K tile:
-//   step 0: read fragments (t, 1); copies 0 .. 2 of this wave for K tile
-//           t + 3; 8 MFMAs on fragments (t, 0)
-//   step 1: wait for this wave's copies of K tile t + 1 (9 later copies may
-//           still be in flight); barrier; read fragments (t + 1, 0); copies
-//           3 .. 5; 8 MFMAs on fragments (t, 1)
+//   step 0: read fragments (t, 1); the first half of this wave's copies for
+//           K tile t + 3; the MFMAs on fragments (t, 0)
+//   step 1: wait for this wave's copies of K tile t + 1 (the copies of K tile
+//           t + 2 and the first half of t + 3 may still be in flight);
+//           barrier; read fragments (t + 1, 0); the second half of the
+//           copies; the MFMAs on fragments (t, 1)
 //
-// LDS (bytes from the dynamic base): stage s of z^T at 8192 s ([32][128]
-// bf16, 256-byte K rows), stage s of dL/do at 32768 + 16384 s ([32][256] bf16,
-// 512-byte K rows).  16-byte chunk c of K row k sits at c ^ (4 (k mod 4)).
-// The transposing 64-bit read is served 32 lanes at a time; those lanes touch
-// 4 K rows x 64 bytes (4 aligned chunks per row), which this swizzle puts on
-// the 64 distinct banks.
+// LDS (bytes from the dynamic base): stage s of z^T at s * TM * 64 ([32][TM]
+// bf16), stage s of dL/do at 4 * TM * 64 + s * TN * 64 ([32][TN] bf16).
+// 16-byte chunk c of K row k sits at c ^ (4 (k mod 4)) (the XOR stays inside
+// the aligned group of 16 chunks, so rows of 48 chunks work too).  The
+// transposing 64-bit read is served 32 lanes at a time; those lanes touch 4 K
+// rows x 64 bytes (4 aligned chunks per row), which this swizzle puts on the
+// 64 distinct banks (every row length here is a multiple of 256 bytes).
 //
 // Edges: tokens past T read as zero (buffer range check); splits are whole K
 // tiles, so a split never reads another split's tokens.  Rows of G^ past r and
@@ -39,15 +47,27 @@
 
 namespace compact {
 
-constexpr int kGhTm = 128, kGhTn = 256;  // tile: rows of G^ (r), columns (m)
 constexpr int kGhK = 32;                 // K tile (tokens)
 constexpr int kGhStages = 4;
 constexpr int kGhAhead = kGhStages - 1;  // K tiles copied ahead
-constexpr int kGhCopies = 6;             // copies per wave per K tile (2 of z^T, 4 of dL/do)
-constexpr int kGhAStage = kGhK * kGhTm * 2;  // 8 KB
-constexpr int kGhBStage = kGhK * kGhTn * 2;  // 16 KB
-constexpr int kGhBBase = kGhStages * kGhAStage;
-constexpr size_t kGhLds = size_t(kGhStages) * (kGhAStage + kGhBStage);  // 96 KB
+
+// Tile geometry: TALL = false: 128 x 256, TALL = true: 384 x 128.
+template <bool TALL>
+struct GhShape {
+  static constexpr int kTm = TALL ? 384 : 128;  // rows of G^ (r)
+  static constexpr int kTn = TALL ? 128 : 256;  // columns (m)
+  static constexpr int kFm = TALL ? 3 : 2;      // MFMA fragments per wave: rows
+  static constexpr int kFn = 4;                 //   and columns
+  static constexpr int kACopies = kTm * kGhK * 2 / 1024 / 4;  // 1 KB copies per wave per K tile: z^T
+  static constexpr int kBCopies = kTn * kGhK * 2 / 1024 / 4;  //   dL/do
+  static constexpr int kCopies = kACopies + kBCopies;         // 6 or 8
+  static constexpr int kAStage = kGhK * kTm * 2;              // 8 or 24 KB
+  static constexpr int kBStage = kGhK * kTn * 2;              // 16 or 8 KB
+  static constexpr int kBBase = kGhStages * kAStage;
+  static constexpr size_t kLds = size_t(kGhStages) * (kAStage + kBStage);  // 96 or 128 KB
+};
+constexpr int kGhTm = GhShape<false>::kTm, kGhTn = GhShape<false>::kTn;
+constexpr int kGhTallTm = GhShape<true>::kTm, kGhTallTn = GhShape<true>::kTn;
 
 // One projection of a launch: G^_j = z_j^T dL/do_j.  The projections of one
 // launch share the token count and the split plan; in an input group (q, k, v
@@ -69,39 +89,56 @@ struct GhatW4Params {
   int count;
   int T, splits;
   int split_len;  // tokens per split, a multiple of kGhK
+  int tall;       // 384 x 128 tiles (k_ghat_w4<true>) instead of 128 x 256
 };
 
-// Per-lane copy offsets.  z^T copy block q (1 KB = 4 K rows of 256 bytes):
-// lane L lands at K row 4 q + L / 16, physical chunk L % 16; dL/do block q
-// (2 K rows of 512 bytes): K row 2 q + L / 32, physical chunk L % 32.  Each
+// Per-lane copy offsets.  A stage of an operand with ROWS columns per K row
+// holds ROWS / 8 16-byte chunks per K row; copy block q (1 KB) fills chunks
+// 64 q .. 64 q + 63 of the stage in order, so lane L lands at linear chunk
+// 64 q + L: K row (64 q + L) / (ROWS / 8), physical chunk the remainder.  Each
 // lane fetches the logical chunk phys ^ (4 (k mod 4)).  Offsets are bytes from
 // the operand's first token of the split and first column of the tile.
 __device__ __forceinline__ int gh_off(int ld, int krow, int chunk) {
   return krow * ld * 2 + ((chunk ^ (4 * (krow & 3))) * 16);
 }
 
-// s_waitcnt vmcnt(N), lgkmcnt(0), then s_barrier; fragments pass through so
-// that the MFMAs after it stay after it
-template <int N>
-__device__ __forceinline__ void gh_wait_barrier(u32x4 (&fa)[2][2], u32x4 (&fb)[2][4]) {
-  static_assert(N >= 0 && N < 64, "vmcnt immediate");
-  asm volatile("s_waitcnt vmcnt(%6) lgkmcnt(0)\n\ts_barrier"
-               : "+v"(fa[1][0]), "+v"(fa[1][1]), "+v"(fb[1][0]), "+v"(fb[1][1]), "+v"(fb[1][2]), "+v"(fb[1][3])
-               : "n"(N)
-               : "memory");
+template <int ROWS>
+__device__ __forceinline__ int gh_block_off(int ld, int q, int lane) {
+  constexpr int cpr = ROWS / 8;
+  const int idx = 64 * q + lane;
+  return gh_off(ld, idx / cpr, idx % cpr);
 }
 
-__device__ __forceinline__ void gh_pin_acc(f32x16 (&acc)[2][4]) {
-  asm volatile(""
-               : "+a"(acc[0][0]), "+a"(acc[0][1]), "+a"(acc[0][2]), "+a"(acc[0][3]), "+a"(acc[1][0]),
-                 "+a"(acc[1][1]), "+a"(acc[1][2]), "+a"(acc[1][3]));
+// Passes a fragment set through an empty statement, so that whatever uses the
+// fragments stays after the statement before it.
+template <int FM>
+__device__ __forceinline__ void gh_tie(u32x4 (&fa)[FM], u32x4 (&fb)[4]) {
+#pragma unroll
+  for (int i = 0; i < FM; ++i) asm volatile("" : "+v"(fa[i]));
+  asm volatile("" : "+v"(fb[0]), "+v"(fb[1]), "+v"(fb[2]), "+v"(fb[3]));
+}
+
+// s_waitcnt vmcnt(N), lgkmcnt(0), then s_barrier; fragments pass through so
+// that the MFMAs after it stay after it
+template <int N, int FM>
+__device__ __forceinline__ void gh_wait_barrier(u32x4 (&fa)[2][FM], u32x4 (&fb)[2][4]) {
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+  gh_tie<FM>(fa[1], fb[1]);
+}
+
+template <int FM>
+__device__ __forceinline__ void gh_pin_acc(f32x16 (&acc)[FM][4]) {
+#pragma unroll
+  for (int i = 0; i < FM; ++i) asm volatile("" : "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]));
 }
 
 // Waits for this wave's LDS reads (the fragments of the next MFMAs) and ties
 // the fragments to that point, so the MFMAs that use them stay after it.
-__device__ __forceinline__ void gh_wait_frags(u32x4 (&fa)[2][2], u32x4 (&fb)[2][4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(fa[0][0]), "+v"(fa[0][1]), "+v"(fb[0][0]), "+v"(fb[0][1]), "+v"(fb[0][2]), "+v"(fb[0][3]));
+template <int FM>
+__device__ __forceinline__ void gh_wait_frags(u32x4 (&fa)[2][FM], u32x4 (&fb)[2][4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : : : "memory");
+  gh_tie<FM>(fa[0], fb[0]);
 }
 
 // ds_read_b64_tr_b16 as inline assembly.  The compiler cannot tell these LDS
@@ -140,20 +177,27 @@ __device__ __forceinline__ u32x4 gh_frag(uint32_t stage, int n0, int kk, int lan
   return out;
 }
 
-// Fragments of 16-deep step kk of the stage at LDS byte offsets (sa, sb).
-__device__ __forceinline__ void gh_read(uint32_t lbase, uint32_t sa, uint32_t sb, int wm, int wn, int lane, int kk,
-                                        u32x4 (&fa)[2], u32x4 (&fb)[4]) {
+// Fragments of 16-deep step kk of the stage at LDS byte offsets (sa, sb):
+// rows r0 .. r0 + 32 FM - 1 of z^T, columns c0 .. c0 + 127 of dL/do.
+template <bool TALL>
+__device__ __forceinline__ void gh_read(uint32_t lbase, uint32_t sa, uint32_t sb, int r0, int c0, int lane, int kk,
+                                        u32x4 (&fa)[GhShape<TALL>::kFm], u32x4 (&fb)[4]) {
+  using S = GhShape<TALL>;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) fa[i] = gh_frag<kGhTm>(lbase + sa, wm * 64 + i * 32, kk, lane);
+  for (int i = 0; i < S::kFm; ++i) fa[i] = gh_frag<S::kTm>(lbase + sa, r0 + i * 32, kk, lane);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) fb[j] = gh_frag<kGhTn>(lbase + sb, wn * 128 + j * 32, kk, lane);
+  for (int j = 0; j < 4; ++j) fb[j] = gh_frag<S::kTn>(lbase + sb, c0 + j * 32, kk, lane);
 }
 
 // The G^ partial tile of workgroup (split, layer, column tile, row tile).
+template <bool TALL>
 __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
+  using S = GhShape<TALL>;
+  constexpr int FM = S::kFm, NM = S::kFm * S::kFn;  // fragments (rows), MFMAs per step
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  // this wave's rows and columns inside the tile
+  const int wr0 = TALL ? wave * 96 : (wave >> 1) * 64, wc0 = TALL ? 0 : (wave & 1) * 128;
   const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
   // order (split, layer, column tile, row tile): the row tiles that share dL/do
   // columns, and the column tiles of one layer that share z, are adjacent,
@@ -164,7 +208,7 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
   const GhatW4Layer& p = prm.layer[li];
   const int tile = tile_all - prm.tile_begin[li];
   const int ct = tile / p.tiles_r, rt = tile % p.tiles_r;
-  const int row0 = rt * kGhTm, col0 = ct * kGhTn;
+  const int row0 = rt * S::kTm, col0 = ct * S::kTn;
   const int t_begin = split * prm.split_len;
   const int t_end = min(t_begin + prm.split_len, prm.T);
   const int kt = (t_end - t_begin + kGhK - 1) / kGhK;
@@ -175,85 +219,84 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
   const int64_t ybytes = view_bytes(prm.T, p.m, p.lddy, t_begin, col0, 2);
   const __amdgpu_buffer_rsrc_t rz = w4_rsrc(p.z + static_cast<int64_t>(t_begin) * p.ldz + row0, zbytes);
   const __amdgpu_buffer_rsrc_t ry = w4_rsrc(p.dy + static_cast<int64_t>(t_begin) * p.lddy + col0, ybytes);
-  // this wave's copy blocks: z^T blocks 2 wave + {0, 1}, dL/do blocks 4 wave + {0 .. 3}
-  int voz[2], voy[4];
+  // this wave's copy blocks: z^T blocks kACopies wave + q, dL/do blocks
+  // kBCopies wave + q
+  int voz[S::kACopies], voy[S::kBCopies];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int b = wave * 2 + q;
-    voz[q] = gh_off(p.ldz, 4 * b + (lane >> 4), lane & 15);
-  }
+  for (int q = 0; q < S::kACopies; ++q) voz[q] = gh_block_off<S::kTm>(p.ldz, wave * S::kACopies + q, lane);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int b = wave * 4 + q;
-    voy[q] = gh_off(p.lddy, 2 * b + (lane >> 5), lane & 31);
-  }
+  for (int q = 0; q < S::kBCopies; ++q) voy[q] = gh_block_off<S::kTn>(p.lddy, wave * S::kBCopies + q, lane);
   const uint32_t lbase = __builtin_amdgcn_groupstaticsize();
-  // copy c (0 .. 5) of this wave for K tile u into stage u % 4; tokens past
-  // this split's K tiles or past T land out of range (the last split is the only
-  // one whose K tiles run past T)
+  // copy c (0 .. kCopies - 1) of this wave for K tile u into stage u % 4;
+  // tokens past this split's K tiles or past T land out of range (the last
+  // split is the only one whose K tiles run past T)
   auto copy = [&](int u, int c) {
     const int st = u % kGhStages;
     const uint32_t krow_bytes_z = static_cast<uint32_t>(u) * kGhK * p.ldz * 2;
     const uint32_t krow_bytes_y = static_cast<uint32_t>(u) * kGhK * p.lddy * 2;
     const uint32_t oob = u < kt ? 0u : kW4Oob;
-    if (c < 2) {
-      const uint32_t dst = lbase + st * kGhAStage + static_cast<uint32_t>(wave * 2 + c) * 1024u;
+    if (c < S::kACopies) {
+      const uint32_t dst = lbase + st * S::kAStage + static_cast<uint32_t>(wave * S::kACopies + c) * 1024u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rz, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
                                                static_cast<int>((voz[c] + krow_bytes_z) | oob), 0, 0, 0);
     } else {
-      const int q = c - 2;
-      const uint32_t dst = lbase + kGhBBase + st * kGhBStage + static_cast<uint32_t>(wave * 4 + q) * 1024u;
+      const int q = c - S::kACopies;
+      const uint32_t dst = lbase + S::kBBase + st * S::kBStage + static_cast<uint32_t>(wave * S::kBCopies + q) * 1024u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
                                                static_cast<int>((voy[q] + krow_bytes_y) | oob), 0, 0, 0);
     }
   };
-  f32x16 acc[2][4];
+  f32x16 acc[FM][4];
   const f32x16 zero = {};
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero;
-  u32x4 fa[2][2], fb[2][4];  // [kk parity][fragment]
+  u32x4 fa[2][FM], fb[2][4];  // [kk parity][fragment]
+  // copies in step 0 (MFMAs 0, 3, 6, ...) and step 1 of a K tile
+  constexpr int kStep0 = (NM + 2) / 3;
+  static_assert(kStep0 * 2 == S::kCopies, "the copies split evenly over the two steps");
   if (kt > 0) {
 #pragma unroll
     for (int u = 0; u < kGhAhead; ++u)
 #pragma unroll
-      for (int c = 0; c < kGhCopies; ++c) copy(u, c);
+      for (int c = 0; c < S::kCopies; ++c) copy(u, c);
     w4_wait_vm<0>();
     asm volatile("s_barrier" ::: "memory");
-    gh_read(lbase, 0, kGhBBase, wm, wn, lane, 0, fa[0], fb[0]);
-    gh_wait_frags(fa, fb);
+    gh_read<TALL>(lbase, 0, S::kBBase, wr0, wc0, lane, 0, fa[0], fb[0]);
+    gh_wait_frags<FM>(fa, fb);
     for (int t = 0; t < kt; ++t) {
       const uint32_t st0 = static_cast<uint32_t>(t % kGhStages), st1 = static_cast<uint32_t>((t + 1) % kGhStages);
-      const uint32_t sa = st0 * kGhAStage, sb = kGhBBase + st0 * kGhBStage;
-      const uint32_t sa1 = st1 * kGhAStage, sb1 = kGhBBase + st1 * kGhBStage;
+      const uint32_t sa = st0 * S::kAStage, sb = S::kBBase + st0 * S::kBStage;
+      const uint32_t sa1 = st1 * S::kAStage, sb1 = S::kBBase + st1 * S::kBStage;
       // step 0
-      gh_read(lbase, sa, sb, wm, wn, lane, 1, fa[1], fb[1]);
+      gh_read<TALL>(lbase, sa, sb, wr0, wc0, lane, 1, fa[1], fb[1]);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < NM; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[0][fi], fb[0][fj], acc[fi][fj]);
         if (i % 3 == 0) copy(t + kGhAhead, i / 3);
       }
-      gh_pin_acc(acc);
+      gh_pin_acc<FM>(acc);
       // step 1: this wave's copies of K tile t + 1 have landed when at most the
-      // copies of the next kGhAhead - 2 K tiles and 3 of the one after are in flight
-      gh_wait_barrier<kGhCopies * (kGhAhead - 2) + 3>(fa, fb);
-      gh_read(lbase, sa1, sb1, wm, wn, lane, 0, fa[0], fb[0]);
+      // copies of the next kGhAhead - 2 K tiles and the step-0 copies of the
+      // one after are in flight
+      gh_wait_barrier<S::kCopies * (kGhAhead - 2) + kStep0, FM>(fa, fb);
+      gh_read<TALL>(lbase, sa1, sb1, wr0, wc0, lane, 0, fa[0], fb[0]);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < NM; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[1][fi], fb[1][fj], acc[fi][fj]);
-        if (i % 3 == 0) copy(t + kGhAhead, 3 + i / 3);
+        if (i % 3 == 0) copy(t + kGhAhead, kStep0 + i / 3);
       }
-      gh_wait_frags(fa, fb);
+      gh_wait_frags<FM>(fa, fb);
     }
     w4_wait_vm<0>();  // no copy may still be writing LDS when the workgroup ends
   }
   // fp32 partial tile: lane (l % 32) owns a column, 16 rows per fragment
-  const int64_t ldp = static_cast<int64_t>(p.tiles_m) * kGhTn;
-  float* out = p.part + static_cast<int64_t>(split) * (p.tiles_r * kGhTm) * ldp;
-  const int64_t r0 = row0 + wm * 64, c0 = col0 + wn * 128;
+  const int64_t ldp = static_cast<int64_t>(p.tiles_m) * S::kTn;
+  float* out = p.part + static_cast<int64_t>(split) * (p.tiles_r * S::kTm) * ldp;
+  const int64_t r0 = row0 + wr0, c0 = col0 + wc0;
   for_each_acc(acc, lane, [&](int row, int col, float v) { out[(r0 + row) * ldp + c0 + col] = v; });
 }
 

@@ -424,12 +424,11 @@ __device__ __forceinline__ uint32_t w4_store_off(const W4Out& od, int b, int gr,
 // steered out of range by w4_store_off; its first column (the low halves)
 // goes out here with 2-byte stores, all 32 of a wave tile at once, right
 // after the tile is converted (only wave tiles that hold the last column).
-__device__ __forceinline__ void w4_store_tails(const W4Out& od, const uint32_t (&raw)[128]) {
-  if ((od.room & 1) == 0 || od.room <= 0 || od.room >= 128) return;  // wave-uniform
+template <int J>
+__device__ __forceinline__ void w4_store_tails_j(const W4Out& od, const uint32_t (&raw)[128]) {
   const int lane = w4_lane_id();
   const int lr = lane & 31, lh = lane >> 5, odd = lane & 1;
-  const int j = (od.room - 1) >> 5;  // column block of the last column
-  const int cl = j * 32 + (lr & ~1);
+  const int cl = J * 32 + (lr & ~1);
   const uint32_t base = cl + 1 == od.room ? static_cast<uint32_t>(4 * lh + 2 * odd) * od.rstride +
                                                 2u * static_cast<uint32_t>(cl)
                                           : kW4Oob;
@@ -437,7 +436,7 @@ __device__ __forceinline__ void w4_store_tails(const W4Out& od, const uint32_t (
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int gr = 0; gr < 4; ++gr) {
-      const int b = i * 4 + j;
+      const int b = i * 4 + J;
       uint32_t o0, o1;
       w4_shuffle(raw[(b * 4 + gr) * 2], raw[(b * 4 + gr) * 2 + 1], odd != 0, o0, o1);
       const uint32_t r = static_cast<uint32_t>(i * 32 + gr * 8) * od.rstride;
@@ -445,6 +444,19 @@ __device__ __forceinline__ void w4_store_tails(const W4Out& od, const uint32_t (
       __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(o1), od.rc,
                                             static_cast<int>(base + r + od.rstride), 0, 0);
     }
+}
+
+// The column block of the last column is wave-uniform; a branch per block
+// keeps every index into raw a constant (an index computed at run time would
+// put raw in scratch memory).
+__device__ __forceinline__ void w4_store_tails(const W4Out& od, const uint32_t (&raw)[128]) {
+  if ((od.room & 1) == 0 || od.room <= 0 || od.room >= 128) return;  // wave-uniform
+  switch ((od.room - 1) >> 5) {  // column block of the last column
+    case 0: w4_store_tails_j<0>(od, raw); break;
+    case 1: w4_store_tails_j<1>(od, raw); break;
+    case 2: w4_store_tails_j<2>(od, raw); break;
+    default: w4_store_tails_j<3>(od, raw); break;
+  }
 }
 
 // Every store of a converted tile at once (the last tile of the workgroup).

@@ -17,7 +17,10 @@ __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
   gemm_w4_persistent<KMASK, ODD>(g);
 }
 
-__global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) { ghat_w4(p); }
+template <bool TALL>
+__global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) {
+  ghat_w4<TALL>(p);
+}
 
 // Three workgroups per CU for bf16 W (168 registers per lane), two for fp32 W.
 template <bool WF32>
@@ -31,7 +34,7 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
-std::atomic<bool> g_lds_set[kMaxDevices][9];  // dynamic LDS limit raised: k_ghat_w4, the 8 k_gemm_w4
+std::atomic<bool> g_lds_set[kMaxDevices][10];  // dynamic LDS limit raised: the 8 k_gemm_w4, the 2 k_ghat_w4
 
 bool fits_offsets(int64_t ld, int64_t K) {
   // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
@@ -79,10 +82,10 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
       reinterpret_cast<const void*>(k_gemm_w4<0, true, false>), reinterpret_cast<const void*>(k_gemm_w4<0, true, true>),
       reinterpret_cast<const void*>(k_gemm_w4<1, false, false>), reinterpret_cast<const void*>(k_gemm_w4<1, false, true>),
       reinterpret_cast<const void*>(k_gemm_w4<1, true, false>), reinterpret_cast<const void*>(k_gemm_w4<1, true, true>)};
-  if (!g_lds_set[dev][1 + u].load(std::memory_order_acquire)) {
+  if (!g_lds_set[dev][u].load(std::memory_order_acquire)) {
     e = hipFuncSetAttribute(fns[u], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kW4Lds));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][1 + u].store(true, std::memory_order_release);
+    g_lds_set[dev][u].store(true, std::memory_order_release);
   }
   if (g.tiles <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(g.tiles < cus ? g.tiles : cus));
@@ -126,15 +129,20 @@ hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  if (!g_lds_set[dev][0].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_ghat_w4), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            static_cast<int>(kGhLds));
+  const int v = p.tall ? 1 : 0;
+  const void* fn = p.tall ? reinterpret_cast<const void*>(k_ghat_w4<true>) : reinterpret_cast<const void*>(k_ghat_w4<false>);
+  const size_t lds = p.tall ? GhShape<true>::kLds : GhShape<false>::kLds;
+  if (!g_lds_set[dev][8 + v].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][0].store(true, std::memory_order_release);
+    g_lds_set[dev][8 + v].store(true, std::memory_order_release);
   }
   const int64_t blocks = int64_t(p.tile_begin[p.count]) * p.splits;
   if (blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_ghat_w4, dim3(static_cast<uint32_t>(blocks)), dim3(256), kGhLds, stream, p);
+  if (p.tall)
+    hipLaunchKernelGGL(k_ghat_w4<true>, dim3(static_cast<uint32_t>(blocks)), dim3(256), lds, stream, p);
+  else
+    hipLaunchKernelGGL(k_ghat_w4<false>, dim3(static_cast<uint32_t>(blocks)), dim3(256), lds, stream, p);
   return hipGetLastError();
 }
 

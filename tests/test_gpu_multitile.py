@@ -143,7 +143,16 @@ def test_multitile_dx_every_element(case):
     assert (num / den) ** 0.5 <= TOL
 
 
-@pytest.mark.parametrize("case", FWD, ids=_ids)
+# G^ cases: the forward groups, plus launches on the 384 x 128 tiles (every
+# projection of the launch with 256 < r and no more padding than 128-row
+# tiles): a group of two such projections, and r = n/8 of LLaMA-1B's down
+GHAT = FWD + [
+    (16384 + 77, 1024, (1024, 520), (344, 300)),
+    (8192 + 77, 5461, (2048,), (682,)),
+]
+
+
+@pytest.mark.parametrize("case", GHAT, ids=_ids)
 def test_multitile_ghat_every_element(case):
     # G^_j = z_j^T dL/do_j over all tokens (split-K, fp32 partials summed in a
     # fixed order): every element against the exact sum
