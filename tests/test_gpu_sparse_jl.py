@@ -9,7 +9,12 @@ sparse JL matrices, §5) against the fp64 oracle.
   the Gaussian call's y (the projection only touches z); an input group is
   bitwise its per-projection calls.
 * Alg. 3 with the sparse P: M, V and the update against the oracle, fp32 and
-  bf16 weights; the batched step is bitwise the per-layer step.
+  bf16 weights; the batched step is bitwise the per-layer step.  On the bf16
+  path the update is a row gather (row i of P N is a signed sum of s rows of
+  N): every element of the update on W = 0 against the oracle within the
+  rounding of N to bf16, of the s-term sum and of W, for ragged widths, rows
+  padded past m (a column slice), rows wider than one work unit and s = 64
+  with repeated columns.
 """
 import numpy as np
 import pytest
@@ -18,7 +23,7 @@ from oracle import compact as oc
 from oracle.pstream import sparse_jl_raw
 from synthetic import bf16_round, fwd_inputs, step_inputs
 
-from gpu_util import dev, empty, ld_for, to_dev, to_np, to_np_f32, workspace
+from gpu_util import BF16_U, assert_elementwise, dev, empty, ld_for, to_dev, to_np, to_np_f32, workspace
 
 pytestmark = pytest.mark.gpu
 
@@ -163,3 +168,41 @@ def test_step_batched_equals_per_layer():
     for La, Lb in zip(layers_a, layers_b):
         assert torch.equal(La["M"], Lb["M"]) and torch.equal(La["V"], Lb["V"])
         assert torch.equal(La["W"].view(torch.int16), Lb["W"].view(torch.int16))
+
+
+# (n, m, r, s, W dtype, ldw): ragged m (the last chunk of a row element by
+# element); rows padded past m; m = 2736 (two work units per row); s = 64 over
+# r = 5 (every row draws each column many times)
+GATHER = [
+    (300, 203, 40, 8, "f32", 204),
+    (300, 203, 40, 3, "bf16", 208),
+    (256, 1000, 128, 8, "bf16", 1032),
+    (1024, 2736, 128, 8, "f32", 2736),
+    (2736, 1024, 342, 8, "bf16", 1024),
+    (100, 37, 5, 64, "bf16", 40),
+]
+
+
+@pytest.mark.parametrize("case", GATHER, ids=lambda c: "n{}-m{}-r{}-s{}-{}-ld{}".format(*c))
+def test_step_gather_every_element(case):
+    n, m, r, s, wdt, ldw = case
+    seed, t, lr, b1, b2, eps, alpha = (11 << 32) | 3, 2, 1e-2, 0.9, 0.999, 1e-8, 0.5
+    _, G, M, V = step_inputs(n, m, r, "f32", t=t, data_seed=n + m + s)
+    W0 = np.zeros((n, m), np.float32)
+    Wd = to_dev(W0, wdt, ldw)
+    Gd, Md, Vd = (torch.from_numpy(a.copy()).to(dev()) for a in (G, M, V))
+    ws = workspace(cp.step_workspace_bytes(n, m, r, CODE["bf16"]))
+    cp.compact_step(Wd, Gd, Md, Vd, seed, t, lr, b1, b2, eps, alpha, proj=f"sparse-jl:{s}", dtype="bf16", ws=ws)
+    torch.cuda.synchronize()
+    _, _, direction = oc.ref_adam(G, M, V, t, b1, b2, eps)
+    _, _, _, change = oc.ref_step(W0, G, M, V, seed, r, t, lr, b1, b2, eps, alpha, sparse_s=s)
+    P = oc.projection(seed, n, r, sparse_s=s)
+    absprod = lr * alpha * (np.abs(P) @ np.abs(direction))
+    # N is rounded to bf16 once (2^-8 of each term); the s terms are summed in
+    # fp32; the update rounds once more when W is bf16
+    assert_elementwise(to_np(Wd), change, absprod, s, bf16_out=(wdt == "bf16"), operand_rel=BF16_U * 1.001,
+                       what=f"dW {case}")
+    # the columns past m of a padded row are untouched
+    if ldw > m:
+        full = Wd.as_strided((n, ldw), (Wd.stride(0), 1))
+        assert not torch.any(full[:, m:].float() != 0)
