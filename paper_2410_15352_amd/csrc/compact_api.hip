@@ -872,7 +872,7 @@ void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t
     q.coef = d.coef;
     q.groups = static_cast<int>(ceil_div(m, 512 * kSjltChunks));
     q.vec = aligned16(W) && (ldw * elem_size(w_dtype)) % 16 == 0;
-    P.sjlt_blocks = static_cast<int>(ceil_div(n * q.groups, 4));
+    P.sjlt_blocks = static_cast<int>(ceil_div(ceil_div(n, kSjltRows) * q.groups, 4));
     return;
   }
   uint16_t* pt = reinterpret_cast<uint16_t*>(
