@@ -14,7 +14,6 @@
 #include "gemm_w4_launch.hpp"
 #include "kernels_bf16.hpp"
 #include "kernels_common.hpp"
-#include "dec_sjlt.hpp"
 
 using namespace compact;
 
@@ -797,8 +796,6 @@ struct StepPlan {
   int adam_blocks, pt_blocks;
   DecW4Layer dl;
   int dec_tiles;
-  DecSjltLayer sl;  // the sparse projection's row-gather decompression (no P^T panel)
-  int sjlt_blocks;
 };
 
 int validate_step(const void* W, int64_t ldw, const float* G, const float* M, const float* V, int64_t n,
@@ -841,7 +838,7 @@ AdamConsts adam_consts(int64_t t, double beta1, double beta2, double eps, int pr
 
 // `ws` is this layer's scratch (step_layer_bytes, 256-byte aligned).
 void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n, int64_t m, int64_t r,
-               uint64_t seed, double lr, double alpha, int proj, int dtype, int w_dtype, void* ws, StepPlan& P) {
+               uint64_t seed, double lr, double alpha, int proj, int dtype, void* ws, StepPlan& P) {
   const int64_t ldn = n_ld(m), ldpt = pt_ld(n);
   char* base = static_cast<char*>(ws);
   AdamLayer& a = P.al;
@@ -855,26 +852,11 @@ void plan_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t
   P.adam_blocks = adam_blocks(r, m);
   P.pt_blocks = 0;
   P.dec_tiles = 0;
-  P.sjlt_blocks = 0;
   const double coef64 = lr * alpha * proj_scale64(proj, r);
   DecW4Layer& d = P.dl;
   d = DecW4Layer{};
   d.coef = static_cast<float>(coef64);
   if (dtype != COMPACT_BF16) return;
-  const ProjDesc pd = proj_desc(proj, r);
-  if (pd.kind == COMPACT_PROJ_SPARSE_JL) {
-    DecSjltLayer& q = P.sl;
-    q = DecSjltLayer{};
-    q.W = W; q.ldw = static_cast<int>(ldw);
-    q.N = static_cast<const uint16_t*>(a.N); q.ldn = static_cast<int>(ldn);
-    q.n = static_cast<int>(n); q.m = static_cast<int>(m); q.r = static_cast<int>(r); q.s = pd.s;
-    q.key = a.key;
-    q.coef = d.coef;
-    q.groups = static_cast<int>(ceil_div(m, 512 * kSjltChunks));
-    q.vec = aligned16(W) && (ldw * elem_size(w_dtype)) % 16 == 0;
-    P.sjlt_blocks = static_cast<int>(ceil_div(ceil_div(n, kSjltRows) * q.groups, 4));
-    return;
-  }
   uint16_t* pt = reinterpret_cast<uint16_t*>(
       base + round_up(static_cast<int64_t>(size_t(r) * size_t(ldn) * elem_size(dtype)), kWsAlign));
   a.pt = pt;
@@ -914,25 +896,6 @@ int launch_step_groups(const std::vector<StepPlan>& plans, const AdamConsts& c, 
   }
   if (dtype != COMPACT_BF16) return COMPACT_OK;
   static_assert(kDecBatch >= kStepBatch, "one decompression launch per Adam launch");
-  static_assert(kSjltBatch >= kStepBatch, "one decompression launch per Adam launch");
-  if (c.kind == COMPACT_PROJ_SPARSE_JL) {  // every layer of the call has the sparse projection
-    for (int i0 = 0; i0 < count; i0 += per) {
-      DecSjltBatch d{};
-      d.count = std::min(per, count - i0);
-      d.begin[0] = 0;
-      for (int j = 0; j < d.count; ++j) {
-        d.layer[j] = plans[i0 + j].sl;
-        d.begin[j + 1] = d.begin[j] + plans[i0 + j].sjlt_blocks;
-      }
-      if (d.begin[d.count] == 0) continue;
-      if (w_dtype == COMPACT_F32)
-        hipLaunchKernelGGL(k_dec_sjlt<true>, dim3(static_cast<uint32_t>(d.begin[d.count])), dim3(256), 0, s, d);
-      else
-        hipLaunchKernelGGL(k_dec_sjlt<false>, dim3(static_cast<uint32_t>(d.begin[d.count])), dim3(256), 0, s, d);
-      if ((st = check_launch("decompression (sparse projection)"))) return st;
-    }
-    return COMPACT_OK;
-  }
   for (int i0 = 0; i0 < count; i0 += per) {
     DecW4Batch d{};
     d.count = std::min(per, count - i0);
@@ -962,7 +925,7 @@ int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64
   if (ws == nullptr || ws_bytes < need) return fail(COMPACT_EWORKSPACE, "step workspace %zu B < %zu B", ws_bytes, need);
   hipStream_t s = static_cast<hipStream_t>(stream);
   std::vector<StepPlan> plans(1);
-  plan_step(W, ldw, G, M, V, n, m, r, seed, lr, alpha, proj, dtype, w_dtype, align_ws(ws), plans[0]);
+  plan_step(W, ldw, G, M, V, n, m, r, seed, lr, alpha, proj, dtype, align_ws(ws), plans[0]);
   if ((st = launch_step_groups(plans, adam_consts(t, beta1, beta2, eps, proj, dtype), dtype, w_dtype, s))) return st;
   if (dtype == COMPACT_F32) {
     GemmF32Params gp{};
@@ -1004,7 +967,7 @@ int compact_step_batched(const compact_layer* layers, int32_t count, int64_t t, 
   char* cursor = static_cast<char*>(align_ws(ws));
   for (int32_t i = 0; i < count; ++i) {
     const compact_layer& L = layers[i];
-    plan_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, L.seed, lr, L.alpha, proj, dtype, w_dtype, cursor, plans[i]);
+    plan_step(L.W, L.ldw, L.G, L.M, L.V, L.n, L.m, L.r, L.seed, lr, L.alpha, proj, dtype, cursor, plans[i]);
     cursor += step_layer_bytes(L.n, L.m, L.r, dtype);
   }
   if ((st = launch_step_groups(plans, adam_consts(t, beta1, beta2, eps, proj, dtype), dtype, w_dtype, s))) return st;

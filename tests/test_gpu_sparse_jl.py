@@ -9,12 +9,11 @@ sparse JL matrices, §5) against the fp64 oracle.
   the Gaussian call's y (the projection only touches z); an input group is
   bitwise its per-projection calls.
 * Alg. 3 with the sparse P: M, V and the update against the oracle, fp32 and
-  bf16 weights; the batched step is bitwise the per-layer step.  On the bf16
-  path the update is a row gather (row i of P N is a signed sum of s rows of
-  N): every element of the update on W = 0 against the oracle within the
-  rounding of N to bf16, of the s-term sum and of W, for ragged widths, rows
-  padded past m (a column slice), rows wider than one work unit and s = 64
-  with repeated columns.
+  bf16 weights; the batched step is bitwise the per-layer step.  Every
+  element of the update on W = 0 against the oracle within the rounding of N
+  to bf16, of the (at most s nonzero) terms' sum and of W, for ragged widths,
+  rows padded past m (a column slice), wide rows and s = 64 with repeated
+  columns.
 """
 import numpy as np
 import pytest
@@ -170,10 +169,9 @@ def test_step_batched_equals_per_layer():
         assert torch.equal(La["W"].view(torch.int16), Lb["W"].view(torch.int16))
 
 
-# (n, m, r, s, W dtype, ldw): ragged m (the last chunk of a row element by
-# element); rows padded past m; m = 2736 (two work units per row); s = 64 over
-# r = 5 (every row draws each column many times)
-GATHER = [
+# (n, m, r, s, W dtype, ldw): ragged m; rows padded past m; m = 2736; s = 64
+# over r = 5 (every row draws each column many times)
+UPDATE = [
     (300, 203, 40, 8, "f32", 204),
     (300, 203, 40, 3, "bf16", 208),
     (256, 1000, 128, 8, "bf16", 1032),
@@ -183,8 +181,8 @@ GATHER = [
 ]
 
 
-@pytest.mark.parametrize("case", GATHER, ids=lambda c: "n{}-m{}-r{}-s{}-{}-ld{}".format(*c))
-def test_step_gather_every_element(case):
+@pytest.mark.parametrize("case", UPDATE, ids=lambda c: "n{}-m{}-r{}-s{}-{}-ld{}".format(*c))
+def test_step_update_every_element(case):
     n, m, r, s, wdt, ldw = case
     seed, t, lr, b1, b2, eps, alpha = (11 << 32) | 3, 2, 1e-2, 0.9, 0.999, 1e-8, 0.5
     _, G, M, V = step_inputs(n, m, r, "f32", t=t, data_seed=n + m + s)
@@ -198,8 +196,8 @@ def test_step_gather_every_element(case):
     _, _, _, change = oc.ref_step(W0, G, M, V, seed, r, t, lr, b1, b2, eps, alpha, sparse_s=s)
     P = oc.projection(seed, n, r, sparse_s=s)
     absprod = lr * alpha * (np.abs(P) @ np.abs(direction))
-    # N is rounded to bf16 once (2^-8 of each term); the s terms are summed in
-    # fp32; the update rounds once more when W is bf16
+    # N is rounded to bf16 once (2^-8 of each term); at most s nonzero terms
+    # are summed in fp32; the update rounds once more when W is bf16
     assert_elementwise(to_np(Wd), change, absprod, s, bf16_out=(wdt == "bf16"), operand_rel=BF16_U * 1.001,
                        what=f"dW {case}")
     # the columns past m of a padded row are untouched
