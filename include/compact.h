@@ -40,6 +40,11 @@
  *  - Projection: the caller passes the same seed to compact_fwd and to
  *    compact_step of the same iteration (Alg. 1 and Alg. 3 re-sample P from
  *    the layer seed); compact_bwd needs no seed (Alg. 2 uses only z and W).
+ *  - Non-finite values are not checked for and never masked: a NaN or an
+ *    infinity in an input reaches exactly the outputs that depend on it under
+ *    IEEE arithmetic (a NaN in token t of x: row t of y and z; a NaN in
+ *    dL/do at (t, c): row t of dx, column c of G^, M, V and of W).  Other
+ *    elements are unaffected.
  */
 #ifndef COMPACT_H_
 #define COMPACT_H_
