@@ -117,15 +117,16 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
 }
 
 // Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp) for one or
-// more projections of the same tokens (one launch): tm x tn tiles (128 x 256,
-// or 384 x 128 when every projection of the launch has 256 < r and 384-row
-// tiles pad r no further than 128-row ones), one split count for all of them,
+// more projections of the same tokens (one launch): tm x tn tiles (256 x 256
+// when every projection of the launch has r >= 256 and 256-row tiles pad r no
+// further than 128-row ones; else 384 x 128 when 256 < r and 384-row tiles
+// pad no further; else 128 x 256), one split count for all of them,
 // at most one workgroup per CU (256 on MI355X), splits of whole 32-token K
 // tiles.  Projection j's partial sums take splits x (tiles_r tm) x
 // (tiles_m tn) fp32 at byte offset part_off[j].
 struct GhatGroupPlan {
   int count;
-  int tall, tm, tn;
+  int shape, tm, tn;
   int tiles_r[kGhMaxLayers], tiles_m[kGhMaxLayers];
   int tiles, splits;
   int64_t split_len;
@@ -136,14 +137,21 @@ bool ghat_tall_fits(int64_t r) {
   return r > 256 && round_up(r, kGhTallTm) <= round_up(r, kGhTm);
 }
 
+bool ghat_square_fits(int64_t r) {
+  return r >= 256 && round_up(r, kGhSqTm) <= round_up(r, kGhTm);
+}
+
 GhatGroupPlan ghat_group_plan(int64_t tokens, int count, const int64_t* r, const int64_t* m) {
   GhatGroupPlan g{};
   g.count = count;
-  g.tall = count > 0 ? 1 : 0;
-  for (int j = 0; j < count; ++j)
-    if (!ghat_tall_fits(r[j])) g.tall = 0;
-  g.tm = g.tall ? kGhTallTm : kGhTm;
-  g.tn = g.tall ? kGhTallTn : kGhTn;
+  bool square = count > 0, tall = count > 0;
+  for (int j = 0; j < count; ++j) {
+    square = square && ghat_square_fits(r[j]);
+    tall = tall && ghat_tall_fits(r[j]);
+  }
+  g.shape = square ? 2 : tall ? 1 : 0;
+  g.tm = square ? kGhSqTm : tall ? kGhTallTm : kGhTm;
+  g.tn = square ? kGhSqTn : tall ? kGhTallTn : kGhTn;
   int64_t tiles = 0;
   for (int j = 0; j < count; ++j) {
     g.tiles_r[j] = static_cast<int>(ceil_div(r[j], g.tm));
@@ -211,7 +219,7 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
   p.T = static_cast<int>(tokens);
   p.splits = rb.splits = g.splits;
   p.split_len = static_cast<int>(g.split_len);
-  p.tall = g.tall;
+  p.shape = g.shape;
   int tb = 0, rbk = 0;
   for (int j = 0; j < g.count; ++j) {
     GhatW4Layer& L = p.layer[j];

@@ -4,14 +4,21 @@
 // K rows and read back as MFMA fragments with the transposing LDS read
 // ds_read_b64_tr_b16.
 //
-// Workgroup: 4 waves over one range of tokens (a split), two tile shapes:
-//   128 x 256 (rows of G^ x columns): waves 2 x 2, each 64 x 128 (2 x 4 MFMA
-//     32x32x16 fragments), 6 fragment reads per 8 MFMAs;
-//   384 x 128 ("tall", for 256 < r <= 384 and other r that 384-row tiles
-//     cover without more padding than 128-row ones, e.g. the down projection
-//     at r = 342): waves stacked along the rows, each 96 x 128 (3 x 4
-//     fragments), 7 fragment reads per 12 MFMAs; every column of dL/do is
-//     then copied and read by one tile instead of by each of three.
+// Workgroup: 4 waves over one range of tokens (a split), three tile shapes
+// (rows of G^ x columns):
+//   0: 128 x 256: waves 2 x 2, each 64 x 128 (2 x 4 MFMA 32x32x16
+//      fragments), 6 fragment reads per 8 MFMAs;
+//   1: 384 x 128 ("tall", for 256 < r that 384-row tiles cover without more
+//      padding than 128-row ones, e.g. the down projection at r = 342): waves
+//      stacked along the rows, each 96 x 128 (3 x 4 fragments), 7 fragment
+//      reads per 12 MFMAs; every column of dL/do is copied and read by one
+//      tile instead of by each of three;
+//   2: 256 x 256 ("square", for r a multiple of 256 or padded no further than
+//      by 128-row tiles, e.g. r = 512 of LLaMA-1B): waves 2 x 2, each 128 x 128
+//      (4 x 4 fragments, 256 accumulation registers), 8 fragment reads per 16
+//      MFMAs.
+// The transposing fragment reads bound the kernel when r is large; shapes 1
+// and 2 read fewer bytes per MFMA.
 // The fp32 partial tile goes to part[split] and a separate kernel sums the
 // splits in a fixed order (deterministic G^).  One launch covers up to 8
 // projections of the same tokens (a layer table): the projections of an input
@@ -51,13 +58,16 @@ constexpr int kGhK = 32;                 // K tile (tokens)
 constexpr int kGhStages = 4;
 constexpr int kGhAhead = kGhStages - 1;  // K tiles copied ahead
 
-// Tile geometry: TALL = false: 128 x 256, TALL = true: 384 x 128.
-template <bool TALL>
+// Tile geometry per shape (above).
+template <int SHAPE>
 struct GhShape {
-  static constexpr int kTm = TALL ? 384 : 128;  // rows of G^ (r)
-  static constexpr int kTn = TALL ? 128 : 256;  // columns (m)
-  static constexpr int kFm = TALL ? 3 : 2;      // MFMA fragments per wave: rows
-  static constexpr int kFn = 4;                 //   and columns
+  static constexpr int kTm = SHAPE == 1 ? 384 : SHAPE == 2 ? 256 : 128;  // rows of G^ (r)
+  static constexpr int kTn = SHAPE == 1 ? 128 : 256;                     // columns (m)
+  static constexpr int kFm = SHAPE == 1 ? 3 : SHAPE == 2 ? 4 : 2;        // MFMA fragments per wave: rows
+  static constexpr int kFn = 4;                                          //   and columns
+  static constexpr int kWaveRows = kFm * 32;
+  static constexpr int kWaveRowGroups = kTm / kWaveRows;                 // waves along the rows
+  static constexpr int kEvery = SHAPE == 2 ? 4 : 3;                      // a copy at every kEvery-th MFMA
   static constexpr int kACopies = kTm * kGhK * 2 / 1024 / 4;  // 1 KB copies per wave per K tile: z^T
   static constexpr int kBCopies = kTn * kGhK * 2 / 1024 / 4;  //   dL/do
   static constexpr int kCopies = kACopies + kBCopies;         // 6 or 8
@@ -65,9 +75,11 @@ struct GhShape {
   static constexpr int kBStage = kGhK * kTn * 2;              // 16 or 8 KB
   static constexpr int kBBase = kGhStages * kAStage;
   static constexpr size_t kLds = size_t(kGhStages) * (kAStage + kBStage);  // 96 or 128 KB
+  static_assert(kWaveRowGroups * (kTn / 128) == 4, "four waves per tile");
 };
-constexpr int kGhTm = GhShape<false>::kTm, kGhTn = GhShape<false>::kTn;
-constexpr int kGhTallTm = GhShape<true>::kTm, kGhTallTn = GhShape<true>::kTn;
+constexpr int kGhTm = GhShape<0>::kTm, kGhTn = GhShape<0>::kTn;
+constexpr int kGhTallTm = GhShape<1>::kTm, kGhTallTn = GhShape<1>::kTn;
+constexpr int kGhSqTm = GhShape<2>::kTm, kGhSqTn = GhShape<2>::kTn;
 
 // One projection of a launch: G^_j = z_j^T dL/do_j.  The projections of one
 // launch share the token count and the split plan; in an input group (q, k, v
@@ -89,7 +101,7 @@ struct GhatW4Params {
   int count;
   int T, splits;
   int split_len;  // tokens per split, a multiple of kGhK
-  int tall;       // 384 x 128 tiles (k_ghat_w4<true>) instead of 128 x 256
+  int shape;      // tile shape (GhShape): 0 128 x 256, 1 384 x 128, 2 256 x 256
 };
 
 // Per-lane copy offsets.  A stage of an operand with ROWS columns per K row
@@ -179,10 +191,10 @@ __device__ __forceinline__ u32x4 gh_frag(uint32_t stage, int n0, int kk, int lan
 
 // Fragments of 16-deep step kk of the stage at LDS byte offsets (sa, sb):
 // rows r0 .. r0 + 32 FM - 1 of z^T, columns c0 .. c0 + 127 of dL/do.
-template <bool TALL>
+template <int SHAPE>
 __device__ __forceinline__ void gh_read(uint32_t lbase, uint32_t sa, uint32_t sb, int r0, int c0, int lane, int kk,
-                                        u32x4 (&fa)[GhShape<TALL>::kFm], u32x4 (&fb)[4]) {
-  using S = GhShape<TALL>;
+                                        u32x4 (&fa)[GhShape<SHAPE>::kFm], u32x4 (&fb)[4]) {
+  using S = GhShape<SHAPE>;
 #pragma unroll
   for (int i = 0; i < S::kFm; ++i) fa[i] = gh_frag<S::kTm>(lbase + sa, r0 + i * 32, kk, lane);
 #pragma unroll
@@ -190,14 +202,16 @@ __device__ __forceinline__ void gh_read(uint32_t lbase, uint32_t sa, uint32_t sb
 }
 
 // The G^ partial tile of workgroup (split, layer, column tile, row tile).
-template <bool TALL>
+template <int SHAPE>
 __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
-  using S = GhShape<TALL>;
+  using S = GhShape<SHAPE>;
   constexpr int FM = S::kFm, NM = S::kFm * S::kFn;  // fragments (rows), MFMAs per step
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // this wave's rows and columns inside the tile
-  const int wr0 = TALL ? wave * 96 : (wave >> 1) * 64, wc0 = TALL ? 0 : (wave & 1) * 128;
+  // this wave's rows and columns inside the tile: 2 x 2 waves for the
+  // 256-wide tiles, 4 x 1 for the tall one
+  const int wr0 = S::kTn == 256 ? (wave >> 1) * S::kWaveRows : wave * S::kWaveRows;
+  const int wc0 = S::kTn == 256 ? (wave & 1) * 128 : 0;
   const uint32_t logical = xcd_remap(blockIdx.x, gridDim.x);
   // order (split, layer, column tile, row tile): the row tiles that share dL/do
   // columns, and the column tiles of one layer that share z, are adjacent,
@@ -253,8 +267,8 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = zero;
   u32x4 fa[2][FM], fb[2][4];  // [kk parity][fragment]
-  // copies in step 0 (MFMAs 0, 3, 6, ...) and step 1 of a K tile
-  constexpr int kStep0 = (NM + 2) / 3;
+  // copies in step 0 (MFMAs 0, kEvery, 2 kEvery, ...) and step 1 of a K tile
+  constexpr int kStep0 = (NM + S::kEvery - 1) / S::kEvery;
   static_assert(kStep0 * 2 == S::kCopies, "the copies split evenly over the two steps");
   if (kt > 0) {
 #pragma unroll
@@ -263,31 +277,31 @@ __device__ __forceinline__ void ghat_w4(const GhatW4Params& prm) {
       for (int c = 0; c < S::kCopies; ++c) copy(u, c);
     w4_wait_vm<0>();
     asm volatile("s_barrier" ::: "memory");
-    gh_read<TALL>(lbase, 0, S::kBBase, wr0, wc0, lane, 0, fa[0], fb[0]);
+    gh_read<SHAPE>(lbase, 0, S::kBBase, wr0, wc0, lane, 0, fa[0], fb[0]);
     gh_wait_frags<FM>(fa, fb);
     for (int t = 0; t < kt; ++t) {
       const uint32_t st0 = static_cast<uint32_t>(t % kGhStages), st1 = static_cast<uint32_t>((t + 1) % kGhStages);
       const uint32_t sa = st0 * S::kAStage, sb = S::kBBase + st0 * S::kBStage;
       const uint32_t sa1 = st1 * S::kAStage, sb1 = S::kBBase + st1 * S::kBStage;
       // step 0
-      gh_read<TALL>(lbase, sa, sb, wr0, wc0, lane, 1, fa[1], fb[1]);
+      gh_read<SHAPE>(lbase, sa, sb, wr0, wc0, lane, 1, fa[1], fb[1]);
 #pragma unroll
       for (int i = 0; i < NM; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[0][fi], fb[0][fj], acc[fi][fj]);
-        if (i % 3 == 0) copy(t + kGhAhead, i / 3);
+        if (i % S::kEvery == 0) copy(t + kGhAhead, i / S::kEvery);
       }
       gh_pin_acc<FM>(acc);
       // step 1: this wave's copies of K tile t + 1 have landed when at most the
       // copies of the next kGhAhead - 2 K tiles and the step-0 copies of the
       // one after are in flight
       gh_wait_barrier<S::kCopies * (kGhAhead - 2) + kStep0, FM>(fa, fb);
-      gh_read<TALL>(lbase, sa1, sb1, wr0, wc0, lane, 0, fa[0], fb[0]);
+      gh_read<SHAPE>(lbase, sa1, sb1, wr0, wc0, lane, 0, fa[0], fb[0]);
 #pragma unroll
       for (int i = 0; i < NM; ++i) {
         const int fi = i >> 2, fj = i & 3;
         acc[fi][fj] = mfma32x32x16(fa[1][fi], fb[1][fj], acc[fi][fj]);
-        if (i % 3 == 0) copy(t + kGhAhead, kStep0 + i / 3);
+        if (i % S::kEvery == 0) copy(t + kGhAhead, kStep0 + i / S::kEvery);
       }
       gh_wait_frags<FM>(fa, fb);
     }

@@ -17,9 +17,9 @@ __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
   gemm_w4_persistent<KMASK, ODD>(g);
 }
 
-template <bool TALL>
+template <int SHAPE>
 __global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) {
-  ghat_w4<TALL>(p);
+  ghat_w4<SHAPE>(p);
 }
 
 // Three workgroups per CU for bf16 W (168 registers per lane), two for fp32 W.
@@ -34,7 +34,7 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
-std::atomic<bool> g_lds_set[kMaxDevices][10];  // dynamic LDS limit raised: the 8 k_gemm_w4, the 2 k_ghat_w4
+std::atomic<bool> g_lds_set[kMaxDevices][11];  // dynamic LDS limit raised: the 8 k_gemm_w4, the 3 k_ghat_w4
 
 bool fits_offsets(int64_t ld, int64_t K) {
   // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
@@ -129,20 +129,25 @@ hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  const int v = p.tall ? 1 : 0;
-  const void* fn = p.tall ? reinterpret_cast<const void*>(k_ghat_w4<true>) : reinterpret_cast<const void*>(k_ghat_w4<false>);
-  const size_t lds = p.tall ? GhShape<true>::kLds : GhShape<false>::kLds;
-  if (!g_lds_set[dev][8 + v].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  if (p.shape < 0 || p.shape > 2) return hipErrorInvalidValue;
+  static const void* const fns[3] = {reinterpret_cast<const void*>(k_ghat_w4<0>),
+                                     reinterpret_cast<const void*>(k_ghat_w4<1>),
+                                     reinterpret_cast<const void*>(k_ghat_w4<2>)};
+  static const size_t lds[3] = {GhShape<0>::kLds, GhShape<1>::kLds, GhShape<2>::kLds};
+  if (!g_lds_set[dev][8 + p.shape].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(fns[p.shape], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds[p.shape]));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][8 + v].store(true, std::memory_order_release);
+    g_lds_set[dev][8 + p.shape].store(true, std::memory_order_release);
   }
   const int64_t blocks = int64_t(p.tile_begin[p.count]) * p.splits;
   if (blocks <= 0) return hipSuccess;
-  if (p.tall)
-    hipLaunchKernelGGL(k_ghat_w4<true>, dim3(static_cast<uint32_t>(blocks)), dim3(256), lds, stream, p);
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (p.shape == 1)
+    hipLaunchKernelGGL(k_ghat_w4<1>, grid, dim3(256), lds[1], stream, p);
+  else if (p.shape == 2)
+    hipLaunchKernelGGL(k_ghat_w4<2>, grid, dim3(256), lds[2], stream, p);
   else
-    hipLaunchKernelGGL(k_ghat_w4<false>, dim3(static_cast<uint32_t>(blocks)), dim3(256), lds, stream, p);
+    hipLaunchKernelGGL(k_ghat_w4<0>, grid, dim3(256), lds[0], stream, p);
   return hipGetLastError();
 }
 
