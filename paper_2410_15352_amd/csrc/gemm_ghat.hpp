@@ -70,11 +70,11 @@ struct GhShape {
   static constexpr int kEvery = SHAPE == 2 ? 4 : 3;                      // a copy at every kEvery-th MFMA
   static constexpr int kACopies = kTm * kGhK * 2 / 1024 / 4;  // 1 KB copies per wave per K tile: z^T
   static constexpr int kBCopies = kTn * kGhK * 2 / 1024 / 4;  //   dL/do
-  static constexpr int kCopies = kACopies + kBCopies;         // 6 or 8
-  static constexpr int kAStage = kGhK * kTm * 2;              // 8 or 24 KB
-  static constexpr int kBStage = kGhK * kTn * 2;              // 16 or 8 KB
+  static constexpr int kCopies = kACopies + kBCopies;         // 6, 8, 8
+  static constexpr int kAStage = kGhK * kTm * 2;              // 8, 24, 16 KB
+  static constexpr int kBStage = kGhK * kTn * 2;              // 16, 8, 16 KB
   static constexpr int kBBase = kGhStages * kAStage;
-  static constexpr size_t kLds = size_t(kGhStages) * (kAStage + kBStage);  // 96 or 128 KB
+  static constexpr size_t kLds = size_t(kGhStages) * (kAStage + kBStage);  // 96, 128, 128 KB
   static_assert(kWaveRowGroups * (kTn / 128) == 4, "four waves per tile");
 };
 constexpr int kGhTm = GhShape<0>::kTm, kGhTn = GhShape<0>::kTn;
