@@ -14,14 +14,15 @@
 //
 // Workgroup: 4 waves, each 64 (columns of W) x 64 (rows of W) = 2 x 2 MFMA
 // 32x32x16 fragments.  Both operands are K-row major (N [r][m], P^T [r][n]); they
-// are copied to LDS as 16-deep K steps by buffer_load_dwordx4 ... lds (6 stages,
-// copies 5 K steps ahead) and read as fragments with the transposing LDS read,
-// as in the G^ kernel (same 256-byte K rows and swizzle).  48 KB of LDS lets
-// three workgroups share a CU.  The tile of W (32 KB bf16) is loaded into
-// registers right after the first 5 K steps' copies and only consumed after the
-// K loop.  Loads complete in issue order, so every copy issued after the W loads
-// waits for them; the 5 steps before cover part of that HBM latency, the other
-// two workgroups of the CU the rest.
+// are copied to LDS as 16-deep K steps by buffer_load_dwordx4 ... lds (4 stages,
+// copies 3 K steps ahead) and read as fragments with the transposing LDS read,
+// as in the G^ kernel (same 256-byte K rows and swizzle).  32 KB of LDS and at
+// most 128 registers per lane let four workgroups share a CU.  The tile of W
+// (32 KB bf16) is loaded into registers after the K loop: held through the
+// loop it would cost 32 registers per lane and one workgroup per CU (measured:
+// 81.4 us per launch with three workgroups and W loaded early, 77.6 us with
+// four and W loaded late), and the other workgroups of the CU cover its
+// latency.
 //
 // Edges: K rows past r read as zero (buffer range ends at row r of N and P^T),
 // rows of W past n are out of range (loads zero, stores dropped), columns of W
@@ -33,11 +34,11 @@ namespace compact {
 
 constexpr int kDecT = 128;                            // tile rows and columns
 constexpr int kDecK = 16;                             // K step (rank): one MFMA deep
-constexpr int kDecStages = 6;
+constexpr int kDecStages = 4;
 constexpr int kDecAhead = kDecStages - 1;             // K steps copied ahead
 constexpr uint32_t kDecStage = kDecK * kDecT * 2;     // 4 KB, one operand
 constexpr uint32_t kDecBBase = kDecStages * kDecStage;
-constexpr size_t kDecLds = 2u * kDecStages * kDecStage;  // 48 KB
+constexpr size_t kDecLds = 2u * kDecStages * kDecStage;  // 32 KB
 constexpr int kDecBatch = 40;                         // layers per launch
 
 struct DecW4Layer {
@@ -155,6 +156,32 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
   // accumulators reach that layout through an 8 x 8 transpose across lanes
   const int tr = lane & 7, row_r = wi * 64 + 8 * (tr >> 2) + 4 * (lane >> 5) + (tr & 3);
   const int col_r = wc * 64 + 8 * ((lane & 31) >> 3);
+  f32x16 acc[2][2];  // [b][a]
+  const f32x16 zero = {};
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int a = 0; a < 2; ++a) acc[b][a] = zero;
+  for (int t = 0; t < kt; ++t) {
+    // this wave's copies of K step t have landed (later VMEM operations: the
+    // copies of the next kDecAhead - 1 K steps); the barrier makes the whole
+    // stage visible and ends every wave's reads of stage
+    // (t + kDecAhead) % kDecStages = (t - 1) % kDecStages, which the next
+    // copies overwrite
+    dec_wait_barrier<2 * (kDecAhead - 1)>();
+    copy(t + kDecAhead);
+    const uint32_t st = static_cast<uint32_t>(t % kDecStages) * kDecStage;
+    u32x4 fa[2], fb[2];  // fragments of N (columns of W) and of P^T (rows of W)
+#pragma unroll
+    for (int a = 0; a < 2; ++a) fa[a] = gh_frag<kDecT>(lbase + st, wc * 64 + a * 32, 0, lane);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) fb[b] = gh_frag<kDecT>(lbase + kDecBBase + st, wi * 64 + b * 32, 0, lane);
+    dec_wait_frags(fa, fb);
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int a = 0; a < 2; ++a) acc[b][a] = mfma32x32x16(fb[b], fa[a], acc[b][a]);
+  }
   WVec wv[2][2][4][2];
   u32x4 wr[2][2][2];
   if constexpr (WF32) {
@@ -181,35 +208,6 @@ __device__ __forceinline__ void dec_w4_tile(const DecW4Layer& p, int tile) {
         }
   }
 
-  f32x16 acc[2][2];  // [b][a]
-  const f32x16 zero = {};
-#pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int a = 0; a < 2; ++a) acc[b][a] = zero;
-  for (int t = 0; t < kt; ++t) {
-    // this wave's copies of K step t have landed (later VMEM operations: the
-    // copies of the next 4 K steps and, before step 5, the W loads: 32 for fp32
-    // W, 8 for bf16); the
-    // barrier makes the whole stage visible and ends every wave's reads of
-    // stage (t + 5) % 6 = (t - 1) % 6, which the next copies overwrite
-    if (t < kDecAhead)
-      dec_wait_barrier<2 * (kDecAhead - 1) + (WF32 ? 32 : 8)>();
-    else
-      dec_wait_barrier<2 * (kDecAhead - 1)>();
-    copy(t + kDecAhead);
-    const uint32_t st = static_cast<uint32_t>(t % kDecStages) * kDecStage;
-    u32x4 fa[2], fb[2];  // fragments of N (columns of W) and of P^T (rows of W)
-#pragma unroll
-    for (int a = 0; a < 2; ++a) fa[a] = gh_frag<kDecT>(lbase + st, wc * 64 + a * 32, 0, lane);
-#pragma unroll
-    for (int b = 0; b < 2; ++b) fb[b] = gh_frag<kDecT>(lbase + kDecBBase + st, wi * 64 + b * 32, 0, lane);
-    dec_wait_frags(fa, fb);
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int a = 0; a < 2; ++a) acc[b][a] = mfma32x32x16(fb[b], fa[a], acc[b][a]);
-  }
   w4_wait_vm<0>();  // the W tile, and every copy (past-the-end ones too) has landed in LDS
 
   // W <- W - coef acc, one rounding (RNE for bf16); columns past m not stored

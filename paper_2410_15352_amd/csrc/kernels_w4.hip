@@ -22,9 +22,9 @@ __global__ __launch_bounds__(256, 1) void k_ghat_w4(GhatW4Params p) {
   ghat_w4<SHAPE>(p);
 }
 
-// Three workgroups per CU for bf16 W (168 registers per lane), two for fp32 W.
+// Four workgroups per CU for bf16 W (at most 128 registers per lane), two for fp32 W.
 template <bool WF32>
-__global__ __launch_bounds__(256, WF32 ? 2 : 3) void k_dec_w4(DecW4Batch d) {
+__global__ __launch_bounds__(256, WF32 ? 2 : 4) void k_dec_w4(DecW4Batch d) {
   const int b = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
   const int l = batch_layer_of(d.begin, d.count, b);
   dec_w4_tile<WF32>(d.layer[l], b - d.begin[l]);
