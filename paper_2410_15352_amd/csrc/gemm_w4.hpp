@@ -48,6 +48,10 @@
 // bytes): the 16 consecutive rows those lanes read then fill 16 distinct
 // 16-byte bank groups (4 rows per 256 bytes, 4 chunk positions).
 //
+// With an even number of K tiles per output tile, A is held in 64-deep slots
+// instead (w4p_ktile below): 3 slots of 32 KB + the 4 B stages = 160 KB, and
+// each A copy instruction fetches 8 rows x 128 bytes.
+//
 // Edges: operand rows past the matrix and chunks at k >= K read as zero (buffer
 // range check), so the K sum is exact; stores past the last row are dropped by
 // the same check, column pairs past the last column are steered out of range
@@ -71,6 +75,13 @@ constexpr int kW4StageBytes = kW4Tile * kW4K * 2;          // one operand, one s
 constexpr int kW4BBase = kW4Stages * kW4StageBytes;        // B stages follow A stages
 constexpr size_t kW4Lds = 2u * kW4Stages * kW4StageBytes;  // 128 KB
 constexpr int kW4MinKTiles = 10;                           // the store schedule spans K tiles 0 .. 9
+
+// A in 64-deep slots (an even number of K tiles, see gemm_w4_persistent):
+// three slots of [256 rows][64] bf16, then the four B stages.
+constexpr int kW4PairBytes = kW4Tile * 2 * kW4K * 2;                      // 32 KB
+constexpr int kW4PairSlots = 3;
+constexpr int kW4PBBase = kW4PairSlots * kW4PairBytes;                    // 96 KB
+constexpr size_t kW4PLds = size_t(kW4PBBase) + kW4Stages * kW4StageBytes;  // 160 KB
 
 // Output columns come in up to two segments (the forward pass writes y and z
 // in one launch): column tile ct < seg[0].tiles writes columns 256 ct .. of
@@ -196,6 +207,9 @@ struct W4Lane {
   int qa, qb;               // what the offsets add per block q (16 rows; wave-uniform)
   int kchunk;               // 8 * logical chunk this lane copies
   int ksb;                  // bytes the B offsets advance per element of k0
+  // A in 64-deep slots only: the copy offset of the odd copy blocks (the even
+  // ones use va) and the element offset of this lane's chunk in an even block
+  int va2, kca;
 };
 
 // Fragment chunk of lane `lane` for step kk (0, 1), fragment 0, stage 0, in a
@@ -214,6 +228,30 @@ __device__ __forceinline__ int w4_copy_off(int64_t ld, int lane, int j, int& kch
   return static_cast<int>((16 * j + (lane >> 2)) * ld * 2) + 16 * c;
 }
 
+// A in 64-deep slots.  Row R of a slot is 128 bytes, 8 chunks: chunks 0 .. 3
+// hold the first K tile of the pair, 4 .. 7 the second; logical chunk c of
+// row R sits at c ^ ((R >> 1) & 7).  The 16 rows that 16 lanes of a
+// ds_read_b128 read fill 16 distinct 16-byte bank groups (2 rows per 256
+// bytes, 8 chunk positions).  Fragment chunk of lane `lane` for step kk of
+// the pair's first K tile, fragment 0, in a wave tile starting at row `wrow`
+// (a multiple of 16); the second K tile flips bit 6 of the offset (chunk
+// c + 4 = c ^ 4), fragment i adds 4096 i.
+__device__ __forceinline__ uint32_t w4p_frag_off(int wrow, int lane, int kk) {
+  const int lr = lane & 31, lh = lane >> 5;
+  const int phys = (2 * kk + lh) ^ ((lr >> 1) & 7);
+  return static_cast<uint32_t>((wrow + lr) * 128 + phys * 16);
+}
+
+// A copy block j (0 .. 7) of wave w fetches rows 64 w + 8 j .. + 7 of a pair,
+// 128 bytes each: lane L lands at row 64 w + 8 j + L / 8, physical chunk
+// L % 8, so it fetches logical chunk (L % 8) ^ (L / 16) ^ 4 (j % 2).
+__device__ __forceinline__ int w4p_copy_off(int64_t ld, int lane, int w, int jodd, int& kchunk) {
+  const int c = (lane & 7) ^ (lane >> 4) ^ (4 * jodd);
+  kchunk = 8 * c;
+  return static_cast<int>((64 * w + (lane >> 3)) * ld * 2) + 16 * c;
+}
+
+template <bool PAIRS>
 __device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
   W4Lane L;
   const int tid = threadIdx.x;
@@ -222,18 +260,36 @@ __device__ __forceinline__ W4Lane w4_lane(const W4Gemm& g) {
   L.wm = L.wave >> 1;
   L.wn = L.wave & 1;
   L.lds = __builtin_amdgcn_groupstaticsize();
-  L.a0 = L.lds + w4_frag_off(L.wm * 128, L.lane, 0);
-  L.a1 = L.lds + w4_frag_off(L.wm * 128, L.lane, 1);
-  L.b0 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 0);
-  L.b1 = L.lds + kW4BBase + w4_frag_off(L.wn * 128, L.lane, 1);
+  const int bbase = PAIRS ? kW4PBBase : kW4BBase;
+  if constexpr (PAIRS) {
+    // lane-relative offsets (the slot and the LDS base are added where they
+    // are read, after the bit-6 flip of a pair's second K tile)
+    L.a0 = w4p_frag_off(L.wm * 128, L.lane, 0);
+    L.a1 = w4p_frag_off(L.wm * 128, L.lane, 1);
+  } else {
+    L.a0 = L.lds + w4_frag_off(L.wm * 128, L.lane, 0);
+    L.a1 = L.lds + w4_frag_off(L.wm * 128, L.lane, 1);
+  }
+  L.b0 = L.lds + bbase + w4_frag_off(L.wn * 128, L.lane, 0);
+  L.b1 = L.lds + bbase + w4_frag_off(L.wn * 128, L.lane, 1);
   // block q = 0 of this wave; block q adds 16 q rows (a wave-uniform step),
   // so only one offset per operand stays in a vector register
   const int ldb_rows = g.b_tiled ? 32 : g.ldb;
-  L.va = w4_copy_off(g.lda, L.lane, L.wave * 4, L.kchunk);
   L.vb = w4_copy_off(ldb_rows, L.lane, L.wave * 4, L.kchunk);
-  L.qa = 32 * g.lda;
   L.qb = 32 * ldb_rows;
   L.ksb = g.b_tiled ? 2 * g.rows_b : 2;
+  if constexpr (PAIRS) {
+    int unused;
+    L.va = w4p_copy_off(g.lda, L.lane, L.wave, 0, L.kca);
+    L.va2 = w4p_copy_off(g.lda, L.lane, L.wave, 1, unused);
+    L.qa = 16 * g.lda;  // block j adds 8 j rows
+  } else {
+    int kca;
+    L.va = w4_copy_off(g.lda, L.lane, L.wave * 4, kca);  // the same chunk as B
+    L.va2 = 0;
+    L.kca = kca;
+    L.qa = 32 * g.lda;
+  }
   return L;
 }
 
@@ -594,10 +650,136 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
   w4_copy_advance(g, cc, kt, n_my, wk);
 }
 
+// ------------------------- A in 64-deep slots ------------------------------
+// With an even number kt of K tiles per tile, K tiles 2P and 2P + 1 of the
+// flat sequence (pair P, never split across two tiles) read A from slot
+// P % 3, and A is copied a pair at a time: each group of 8 lanes fetches one
+// 128-byte row piece (a whole cache line) instead of two 64-byte halves in
+// two K tiles.  The row-major A is the operand whose copies cost the
+// vector-memory path most (B is K-tiled: 1 KB of contiguous memory per copy
+// instruction already).  Pair P + 2 is copied during K tiles 2P (blocks
+// 0 .. 3 of each wave) and 2P + 1 (blocks 4 .. 7), at the MFMAs where the
+// 32-deep layout issues its A copies, so the copies per K tile and the vmcnt
+// accounting (w4_vm_allow) stay the same: the last copies that K tile h + 1
+// needs are still the B copies issued during K tile h - 2 (the second half of
+// pair (h + 1) / 2 went out in the step before them, or earlier).  Slot
+// (P + 2) % 3 last held pair P - 1, whose last fragments were read before the
+// barrier of K tile 2P - 1.
+struct W4PairCursor {
+  W4Cursor c;   // tile of the pair being copied
+  int kp;       // its pair index in that tile
+  __amdgpu_buffer_rsrc_t ra;
+  uint32_t sa;  // slot byte offset of the pair the MFMAs are on
+};
+
+__device__ __forceinline__ void w4p_advance(const W4Gemm& g, W4PairCursor& ap, int kt, int n_my, const W4Walk& wk) {
+  ap.kp += 1;
+  if (2 * ap.kp == kt) {
+    ap.kp = 0;
+    w4_next_tile(g, wk, ap.c);
+    ap.ra = w4_copy_desc(g, ap.c, n_my).ra;
+  }
+}
+
+// Out-of-range bits of the even (oe) and odd (oo) A blocks of the pair that
+// starts at element k0.
+__device__ __forceinline__ void w4p_oob(const W4Gemm& g, const W4Lane& L, int k0, uint32_t& oe, uint32_t& oo) {
+  oe = ~static_cast<uint32_t>(k0 + L.kca - g.K) & kW4Oob;
+  oo = ~static_cast<uint32_t>(k0 + (L.kca ^ 32) - g.K) & kW4Oob;
+}
+
+// A copy block j (0 .. 7) of the pair at element k0 into slot byte offset `slot`.
+__device__ __forceinline__ void w4p_copy_a(const W4Lane& L, __amdgpu_buffer_rsrc_t ra, int k0, uint32_t oob,
+                                           uint32_t slot, int j) {
+  const uint32_t vo = static_cast<uint32_t>(((j & 1) ? L.va2 : L.va) + j * L.qa + 2 * k0) | oob;
+  const uint32_t dst = L.lds + slot + static_cast<uint32_t>(L.wave * 8 + j) * 1024u;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
+                                           static_cast<int>(vo), 0, 0, 0);
+}
+
+// B copy block q (0 .. 3) of the K tile at element k3 into the B stage at byte
+// offset `stage` (from the B base).
+__device__ __forceinline__ void w4p_copy_b(const W4Lane& L, __amdgpu_buffer_rsrc_t rb, int k3, uint32_t oob,
+                                           uint32_t stage, int q) {
+  const uint32_t vo = static_cast<uint32_t>(L.vb + q * L.qb + L.ksb * k3) | oob;
+  const uint32_t dst = L.lds + kW4PBBase + stage + static_cast<uint32_t>(L.wave * 4 + q) * 1024u;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, reinterpret_cast<w4_lds_void*>(static_cast<uintptr_t>(dst)), 16,
+                                           static_cast<int>(vo), 0, 0, 0);
+}
+
+// w4_ktile with A in 64-deep slots (T = 10 and 11: any even and odd T >= 10).
+template <int T, bool KMASK, bool ODD>
+__device__ __forceinline__ void w4p_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc,
+                                          W4PairCursor& ap, int kt, int n_my, const W4Walk& wk, const W4Out& od,
+                                          uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4],
+                                          bool last = false) {
+  constexpr uint32_t e = T & 1;  // K tile h is the first (0) or second (1) of its pair
+  const bool odd = w4_drip(T) ? (w4_lane_id() & 1) != 0 : false;
+  uint32_t hold = 0;
+  const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
+  const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
+  const uint32_t s3 = static_cast<uint32_t>((h + 3) & 3) * kW4StageBytes;
+  const uint32_t sa_next = ap.sa == 2u * kW4PairBytes ? 0u : ap.sa + kW4PairBytes;
+  const uint32_t sa_copy = ap.sa == 0u ? 2u * kW4PairBytes : ap.sa - kW4PairBytes;  // slot of pair + 2
+  const uint32_t ar1 = (L.a1 ^ (64u * e)) + L.lds + ap.sa;                         // A fragments (h, 1)
+  const uint32_t ar0 = (L.a0 ^ (64u * (1u - e))) + L.lds + (e ? sa_next : ap.sa);  // A fragments (h + 1, 0)
+  const f32x16 zero = {};
+  const int k3 = cc.k * kW4K;  // B copies: step h + 3
+  const uint32_t oobb = ~static_cast<uint32_t>(k3 + L.kchunk - g.K) & kW4Oob;
+  const int k0 = ap.kp * (2 * kW4K);  // A copies: pair h / 2 + 2
+  uint32_t oe, oo;
+  w4p_oob(g, L, k0, oe, oo);
+  if constexpr (KMASK) w4_mask_k(g, f[0], 0, last);
+  // step 0: MFMAs on f[0]; reads of f[1]; A copy blocks 4 e .. 4 e + 3 of pair h / 2 + 2
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int fa = i >> 2, fb = i & 3;
+    acc[fa][fb] = mfma32x32x16(f[0].a[fa], f[0].b[fb], T == 0 ? zero : acc[fa][fb]);
+    if (i < 4) {
+      f[1].a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(ar1 + i * 4096));
+    } else if (i < 8) {
+      f[1].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b1 + s0 + (i - 4) * 2048));
+    }
+    if (i % 4 == 0) {
+      const int j = 4 * static_cast<int>(e) + i / 4;
+      w4p_copy_a(L, ap.ra, k0, (j & 1) ? oo : oe, sa_copy, j);
+    }
+    if constexpr (w4_drip(T)) {
+      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, i / 2);
+    }
+  }
+  w4_pin_acc(acc);
+  // step 1: MFMAs on f[1]; reads of f[0] for step h + 1; B copies of step h + 3
+  w4_wait_vm<w4_vm_allow<T>()>();
+  w4_lds_barrier(f[1]);
+  if constexpr (KMASK) w4_mask_k(g, f[1], 1, last);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int fa = i >> 2, fb = i & 3;
+    acc[fa][fb] = mfma32x32x16(f[1].a[fa], f[1].b[fb], acc[fa][fb]);
+    if (i < 4) {
+      f[0].a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(ar0 + i * 4096));
+    } else if (i < 8) {
+      f[0].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b0 + s1 + (i - 4) * 2048));
+    }
+    if (i % 4 == 2) w4p_copy_b(L, cc.d.rb, k3, oobb, s3, i / 4);
+    if constexpr (w4_drip(T)) {
+      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, 8 + i / 2);
+    }
+  }
+  w4_pin(f[0]);
+  w4_copy_advance(g, cc, kt, n_my, wk);
+  if constexpr (e == 1) {
+    w4p_advance(g, ap, kt, n_my, wk);
+    ap.sa = sa_next;
+  }
+}
+
 // The whole persistent GEMM for this workgroup.  Launch with kW4Threads
 // threads, kW4Lds bytes of dynamic LDS and at most one workgroup per CU.
-// KMASK: K % 8 != 0 (B K-tiled); ODD: an output width is odd.
-template <bool KMASK, bool ODD>
+// KMASK: K % 8 != 0 (B K-tiled); ODD: an output width is odd; PAIRS: A in
+// 64-deep slots (an even number of K tiles; kW4PLds bytes of LDS).
+template <bool KMASK, bool ODD, bool PAIRS>
 __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   const int G = static_cast<int>(gridDim.x);
   const int p = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
@@ -605,17 +787,42 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   const int n_my = (g.tiles - p + G - 1) / G;
   const int kt = static_cast<int>(ceil_div(g.K, kW4K));
   const W4Walk wk = w4_walk(g, p, G);
-  const W4Lane L = w4_lane(g);
+  const W4Lane L = w4_lane<PAIRS>(g);
 
   W4CopyCursor cc;
   cc.c = W4Cursor{0, 0, 0};
   w4_tile_at(g, wk, cc.c);
   cc.k = 0;
   cc.d = w4_copy_desc(g, cc.c, n_my);
+  W4PairCursor ap;
+  if constexpr (PAIRS) {
+    ap.c = cc.c;
+    ap.kp = 0;
+    ap.ra = cc.d.ra;
+    ap.sa = 0;
+    // A pairs 0 and 1 (steps 0 .. 3) into slots 0 and 1, B of steps 0 .. 2
 #pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    w4_copy(g, L, cc.d, cc.k * kW4K, L.lds + s * kW4StageBytes, L.lds + kW4BBase + s * kW4StageBytes);
-    w4_copy_advance(g, cc, kt, n_my, wk);
+    for (int pp = 0; pp < 2; ++pp) {
+      uint32_t oe, oo;
+      w4p_oob(g, L, ap.kp * (2 * kW4K), oe, oo);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w4p_copy_a(L, ap.ra, ap.kp * (2 * kW4K), (j & 1) ? oo : oe, pp * kW4PairBytes, j);
+      w4p_advance(g, ap, kt, n_my, wk);
+    }
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int k3 = cc.k * kW4K;
+      const uint32_t oob = ~static_cast<uint32_t>(k3 + L.kchunk - g.K) & kW4Oob;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) w4p_copy_b(L, cc.d.rb, k3, oob, s * kW4StageBytes, q);
+      w4_copy_advance(g, cc, kt, n_my, wk);
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      w4_copy(g, L, cc.d, cc.k * kW4K, L.lds + s * kW4StageBytes, L.lds + kW4BBase + s * kW4StageBytes);
+      w4_copy_advance(g, cc, kt, n_my, wk);
+    }
   }
   W4Frags f[2];
   f32x16 acc[4][4];
@@ -627,21 +834,47 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   W4Out od = w4_out_desc(g, L, oc, false);  // nothing to store before the first tile
   w4_wait_vm<0>();
   w4_lds_barrier(f[1]);
-  w4_read(L.a0, L.b0, f[0]);
+  if constexpr (PAIRS) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      f[0].a[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.a0 + L.lds + i * 4096));
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      f[0].b[i] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b0 + i * 2048));
+  } else {
+    w4_read(L.a0, L.b0, f[0]);
+  }
   int h = 0;
   for (int q = 0; q < n_my; ++q) {
-    w4_ktile<0, KMASK, ODD>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<1, KMASK, ODD>(g, L, h + 1, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<2, KMASK, ODD>(g, L, h + 2, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<3, KMASK, ODD>(g, L, h + 3, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<4, KMASK, ODD>(g, L, h + 4, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<5, KMASK, ODD>(g, L, h + 5, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<6, KMASK, ODD>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<7, KMASK, ODD>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<8, KMASK, ODD>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
-    w4_ktile<9, KMASK, ODD>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc, kt == 10);
-    for (int t = 10; t < kt; ++t)
-      w4_ktile<10, KMASK, ODD>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc, t == kt - 1);
+    if constexpr (PAIRS) {
+      w4p_ktile<0, KMASK, ODD>(g, L, h + 0, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<1, KMASK, ODD>(g, L, h + 1, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<2, KMASK, ODD>(g, L, h + 2, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<3, KMASK, ODD>(g, L, h + 3, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<4, KMASK, ODD>(g, L, h + 4, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<5, KMASK, ODD>(g, L, h + 5, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<6, KMASK, ODD>(g, L, h + 6, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<7, KMASK, ODD>(g, L, h + 7, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<8, KMASK, ODD>(g, L, h + 8, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<9, KMASK, ODD>(g, L, h + 9, cc, ap, kt, n_my, wk, od, raw, f, acc, kt == 10);
+      for (int t = 10; t < kt; t += 2) {
+        w4p_ktile<10, KMASK, ODD>(g, L, h + t, cc, ap, kt, n_my, wk, od, raw, f, acc);
+        w4p_ktile<11, KMASK, ODD>(g, L, h + t + 1, cc, ap, kt, n_my, wk, od, raw, f, acc, t + 1 == kt - 1);
+      }
+    } else {
+      w4_ktile<0, KMASK, ODD>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<1, KMASK, ODD>(g, L, h + 1, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<2, KMASK, ODD>(g, L, h + 2, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<3, KMASK, ODD>(g, L, h + 3, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<4, KMASK, ODD>(g, L, h + 4, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<5, KMASK, ODD>(g, L, h + 5, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<6, KMASK, ODD>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<7, KMASK, ODD>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<8, KMASK, ODD>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
+      w4_ktile<9, KMASK, ODD>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc, kt == 10);
+      for (int t = 10; t < kt; ++t)
+        w4_ktile<10, KMASK, ODD>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc, t == kt - 1);
+    }
     // bf16 pairs only here (the stores of the next tile's first K tiles do
     // the lane shuffles, in the shadow of its MFMAs)
 #pragma unroll

@@ -11,10 +11,11 @@ namespace compact {
 
 // One instantiation per use, so that profiles report the forward and the dx
 // GEMM separately; KMASK: K % 8 != 0, ODD: an odd output width (the LLaMA-1B
-// widths of 5461).
-template <int USE, bool KMASK = false, bool ODD = false>
+// widths of 5461); PAIRS: an even number of 32-deep K tiles, A copied in
+// 64-deep slots.
+template <int USE, bool KMASK = false, bool ODD = false, bool PAIRS = false>
 __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
-  gemm_w4_persistent<KMASK, ODD>(g);
+  gemm_w4_persistent<KMASK, ODD, PAIRS>(g);
 }
 
 template <int SHAPE>
@@ -34,7 +35,8 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];        // CU count per device, 0 until queried
-std::atomic<bool> g_lds_set[kMaxDevices][11];  // dynamic LDS limit raised: the 8 k_gemm_w4, the 3 k_ghat_w4
+constexpr int kGemmVariants = 16;
+std::atomic<bool> g_lds_set[kMaxDevices][kGemmVariants + 3];  // dynamic LDS limit raised: k_gemm_w4, k_ghat_w4
 
 bool fits_offsets(int64_t ld, int64_t K) {
   // 32-bit buffer offsets: 256 rows of ld elements plus K, in bytes
@@ -76,14 +78,28 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   }
   const bool kmask = g.K % 8 != 0;
   const bool odd = g.seg[0].cols % 2 != 0 || (g.seg[1].tiles > 0 && g.seg[1].cols % 2 != 0);
-  const int u = (use == W4Use::kForward ? 0 : 4) + (kmask ? 2 : 0) + (odd ? 1 : 0);
-  static const void* const fns[8] = {
-      reinterpret_cast<const void*>(k_gemm_w4<0, false, false>), reinterpret_cast<const void*>(k_gemm_w4<0, false, true>),
-      reinterpret_cast<const void*>(k_gemm_w4<0, true, false>), reinterpret_cast<const void*>(k_gemm_w4<0, true, true>),
-      reinterpret_cast<const void*>(k_gemm_w4<1, false, false>), reinterpret_cast<const void*>(k_gemm_w4<1, false, true>),
-      reinterpret_cast<const void*>(k_gemm_w4<1, true, false>), reinterpret_cast<const void*>(k_gemm_w4<1, true, true>)};
+  const bool pairs = ceil_div(g.K, kW4K) % 2 == 0;
+  const int u = (use == W4Use::kForward ? 0 : 8) + (pairs ? 4 : 0) + (kmask ? 2 : 0) + (odd ? 1 : 0);
+  static const void* const fns[kGemmVariants] = {
+      reinterpret_cast<const void*>(k_gemm_w4<0, false, false, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, false, true, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, true, false, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, true, true, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, false, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, false, true, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, true, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<0, true, true, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, false, false, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, false, true, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, true, false, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, true, true, false>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, false, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, false, true, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, true, false, true>),
+      reinterpret_cast<const void*>(k_gemm_w4<1, true, true, true>)};
+  const size_t lds = pairs ? kW4PLds : kW4Lds;
   if (!g_lds_set[dev][u].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(fns[u], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kW4Lds));
+    e = hipFuncSetAttribute(fns[u], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
     if (e != hipSuccess) return e;
     g_lds_set[dev][u].store(true, std::memory_order_release);
   }
@@ -91,16 +107,9 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   const dim3 grid(static_cast<uint32_t>(g.tiles < cus ? g.tiles : cus));
   W4Gemm gg = g;
   gg.band_rows = w4_band_rows(g.tiles / g.tiles_n);
-  switch (u) {
-    case 0: hipLaunchKernelGGL((k_gemm_w4<0, false, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 1: hipLaunchKernelGGL((k_gemm_w4<0, false, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 2: hipLaunchKernelGGL((k_gemm_w4<0, true, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 3: hipLaunchKernelGGL((k_gemm_w4<0, true, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 4: hipLaunchKernelGGL((k_gemm_w4<1, false, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 5: hipLaunchKernelGGL((k_gemm_w4<1, false, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    case 6: hipLaunchKernelGGL((k_gemm_w4<1, true, false>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-    default: hipLaunchKernelGGL((k_gemm_w4<1, true, true>), grid, dim3(kW4Threads), kW4Lds, stream, gg); break;
-  }
+  void* args[] = {&gg};
+  e = hipLaunchKernel(fns[u], grid, dim3(kW4Threads), args, lds, stream);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
@@ -134,10 +143,10 @@ hipError_t ghat_w4_launch(const GhatW4Params& p, hipStream_t stream) {
                                      reinterpret_cast<const void*>(k_ghat_w4<1>),
                                      reinterpret_cast<const void*>(k_ghat_w4<2>)};
   static const size_t lds[3] = {GhShape<0>::kLds, GhShape<1>::kLds, GhShape<2>::kLds};
-  if (!g_lds_set[dev][8 + p.shape].load(std::memory_order_acquire)) {
+  if (!g_lds_set[dev][kGemmVariants + p.shape].load(std::memory_order_acquire)) {
     e = hipFuncSetAttribute(fns[p.shape], hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds[p.shape]));
     if (e != hipSuccess) return e;
-    g_lds_set[dev][8 + p.shape].store(true, std::memory_order_release);
+    g_lds_set[dev][kGemmVariants + p.shape].store(true, std::memory_order_release);
   }
   const int64_t blocks = int64_t(p.tile_begin[p.count]) * p.splits;
   if (blocks <= 0) return hipSuccess;

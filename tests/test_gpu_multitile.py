@@ -41,6 +41,13 @@ FWD = [
     (16384 + 77, 5461, (2048,), (1365,)),
     (8192 + 77, 2048, (5461,), (512,)),
 ]
+# K edges of the K loop: an even number of 32-deep K tiles runs A in 64-deep
+# slots, an odd number in 32-deep stages; each with K % 8 != 0 and odd widths
+FWD_K = [
+    (22016 + 77, 320, (2048,), (40,)),      # K = 320: the fewest K tiles (10, even)
+    (22016 + 77, 352, (2048,), (45,)),      # 11 K tiles (odd), odd z width
+    (32768 + 77, 1021, (1000,), (512,)),    # K % 8 != 0, 32 K tiles (even)
+]
 # dx = dL/do W^T has n output columns: more tokens for three tiles per CU
 DX = [
     (49152 + 77, 1024, (1024, 1024, 1024), (128, 128, 128)),
@@ -48,6 +55,7 @@ DX = [
     (49152 + 77, 1024, (2736, 2736), (128, 128)),
     (12288 + 77, 5461, (2048,), (1365,)),     # odd output width (dL/dx of down)
     (24576 + 77, 2048, (5461,), (512,)),      # K % 8 != 0 (dL/dx of gate)
+    (49152 + 77, 1021, (1021,), (128,)),      # K % 8 != 0 with 32 K tiles (even), odd output width
 ]
 
 
@@ -70,7 +78,7 @@ def _rows_np(t, r0, r1):
 CHUNK = 8192
 
 
-@pytest.mark.parametrize("case", FWD, ids=_ids)
+@pytest.mark.parametrize("case", FWD + FWD_K, ids=_ids)
 def test_multitile_forward_every_element(case):
     T, n, ms, rs = case
     M, R = sum(ms), sum(rs)

@@ -47,7 +47,7 @@ def _remarks(unit):
 def test_persistent_kernels_use_no_scratch():
     kernels = _remarks("kernels_w4.hip")
     names = [k for k in kernels if "k_gemm_w4" in k or "k_ghat_w4" in k or "k_dec_w4" in k]
-    assert len([k for k in names if "k_gemm_w4" in k]) == 8, sorted(kernels)
+    assert len([k for k in names if "k_gemm_w4" in k]) == 16, sorted(kernels)
     assert len([k for k in names if "k_ghat_w4" in k]) == 3, sorted(kernels)
     for k in names:
         r = kernels[k]
