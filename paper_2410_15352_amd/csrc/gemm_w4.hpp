@@ -48,9 +48,9 @@
 // bytes): the 16 consecutive rows those lanes read then fill 16 distinct
 // 16-byte bank groups (4 rows per 256 bytes, 4 chunk positions).
 //
-// With an even number of K tiles per output tile, A is held in 64-deep slots
-// instead (w4p_ktile below): 3 slots of 32 KB + the 4 B stages = 160 KB, and
-// each A copy instruction fetches 8 rows x 128 bytes.
+// With A in 64-deep slots (w4p_ktile below) the K tiles of an output tile are
+// taken in pairs: 3 slots of 32 KB + the 4 B stages = 160 KB, and each A copy
+// instruction fetches 8 rows x 128 bytes.
 //
 // Edges: operand rows past the matrix and chunks at k >= K read as zero (buffer
 // range check), so the K sum is exact; stores past the last row are dropped by
@@ -651,8 +651,9 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
 }
 
 // ------------------------- A in 64-deep slots ------------------------------
-// With an even number kt of K tiles per tile, K tiles 2P and 2P + 1 of the
-// flat sequence (pair P, never split across two tiles) read A from slot
+// With an even number kt of K tiles per tile (an odd count is rounded up: the
+// last K tile then lies wholly past K and reads zeros), K tiles 2P and 2P + 1
+// of the flat sequence (pair P, never split across two tiles) read A from slot
 // P % 3, and A is copied a pair at a time: each group of 8 lanes fetches one
 // 128-byte row piece (a whole cache line) instead of two 64-byte halves in
 // two K tiles.  The row-major A is the operand whose copies cost the
@@ -778,14 +779,18 @@ __device__ __forceinline__ void w4p_ktile(const W4Gemm& g, const W4Lane& L, int 
 // The whole persistent GEMM for this workgroup.  Launch with kW4Threads
 // threads, kW4Lds bytes of dynamic LDS and at most one workgroup per CU.
 // KMASK: K % 8 != 0 (B K-tiled); ODD: an output width is odd; PAIRS: A in
-// 64-deep slots (an even number of K tiles; kW4PLds bytes of LDS).
+// 64-deep slots (kW4PLds bytes of LDS).
 template <bool KMASK, bool ODD, bool PAIRS>
 __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
   const int G = static_cast<int>(gridDim.x);
   const int p = static_cast<int>(xcd_remap(blockIdx.x, gridDim.x));
   if (p >= g.tiles) return;
   const int n_my = (g.tiles - p + G - 1) / G;
-  const int kt = static_cast<int>(ceil_div(g.K, kW4K));
+  // K tiles per output tile; with PAIRS an odd count gets one more, all past
+  // K (its copies read zero), so that pairs never straddle two output tiles
+  const int kt_k = static_cast<int>(ceil_div(g.K, kW4K));
+  const int kt = PAIRS ? (kt_k + 1) & ~1 : kt_k;
+  const int kl = kt_k - 1;  // the K tile that holds element K - 1
   const W4Walk wk = w4_walk(g, p, G);
   const W4Lane L = w4_lane<PAIRS>(g);
 
@@ -856,10 +861,10 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
       w4p_ktile<6, KMASK, ODD>(g, L, h + 6, cc, ap, kt, n_my, wk, od, raw, f, acc);
       w4p_ktile<7, KMASK, ODD>(g, L, h + 7, cc, ap, kt, n_my, wk, od, raw, f, acc);
       w4p_ktile<8, KMASK, ODD>(g, L, h + 8, cc, ap, kt, n_my, wk, od, raw, f, acc);
-      w4p_ktile<9, KMASK, ODD>(g, L, h + 9, cc, ap, kt, n_my, wk, od, raw, f, acc, kt == 10);
+      w4p_ktile<9, KMASK, ODD>(g, L, h + 9, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == 9);
       for (int t = 10; t < kt; t += 2) {
-        w4p_ktile<10, KMASK, ODD>(g, L, h + t, cc, ap, kt, n_my, wk, od, raw, f, acc);
-        w4p_ktile<11, KMASK, ODD>(g, L, h + t + 1, cc, ap, kt, n_my, wk, od, raw, f, acc, t + 1 == kt - 1);
+        w4p_ktile<10, KMASK, ODD>(g, L, h + t, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t);
+        w4p_ktile<11, KMASK, ODD>(g, L, h + t + 1, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t + 1);
       }
     } else {
       w4_ktile<0, KMASK, ODD>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);
@@ -871,9 +876,9 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
       w4_ktile<6, KMASK, ODD>(g, L, h + 6, cc, kt, n_my, wk, od, raw, f, acc);
       w4_ktile<7, KMASK, ODD>(g, L, h + 7, cc, kt, n_my, wk, od, raw, f, acc);
       w4_ktile<8, KMASK, ODD>(g, L, h + 8, cc, kt, n_my, wk, od, raw, f, acc);
-      w4_ktile<9, KMASK, ODD>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc, kt == 10);
+      w4_ktile<9, KMASK, ODD>(g, L, h + 9, cc, kt, n_my, wk, od, raw, f, acc, kl == 9);
       for (int t = 10; t < kt; ++t)
-        w4_ktile<10, KMASK, ODD>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc, t == kt - 1);
+        w4_ktile<10, KMASK, ODD>(g, L, h + t, cc, kt, n_my, wk, od, raw, f, acc, kl == t);
     }
     // bf16 pairs only here (the stores of the next tile's first K tiles do
     // the lane shuffles, in the shadow of its MFMAs)

@@ -11,8 +11,8 @@ namespace compact {
 
 // One instantiation per use, so that profiles report the forward and the dx
 // GEMM separately; KMASK: K % 8 != 0, ODD: an odd output width (the LLaMA-1B
-// widths of 5461); PAIRS: an even number of 32-deep K tiles, A copied in
-// 64-deep slots.
+// widths of 5461); PAIRS: A copied in 64-deep slots, two 32-deep K tiles at a
+// time.
 template <int USE, bool KMASK = false, bool ODD = false, bool PAIRS = false>
 __global__ __launch_bounds__(kW4Threads, 1) void k_gemm_w4(W4Gemm g) {
   gemm_w4_persistent<KMASK, ODD, PAIRS>(g);
@@ -78,7 +78,10 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   }
   const bool kmask = g.K % 8 != 0;
   const bool odd = g.seg[0].cols % 2 != 0 || (g.seg[1].tiles > 0 && g.seg[1].cols % 2 != 0);
-  const bool pairs = ceil_div(g.K, kW4K) % 2 == 0;
+  // A in 64-deep slots: an odd number of K tiles is padded by one (a zero K
+  // tile, 1/kt more matrix work), which pays from about 40 K tiles on
+  const int64_t kt = ceil_div(g.K, kW4K);
+  const bool pairs = kt % 2 == 0 || kt >= 41;
   const int u = (use == W4Use::kForward ? 0 : 8) + (pairs ? 4 : 0) + (kmask ? 2 : 0) + (odd ? 1 : 0);
   static const void* const fns[kGemmVariants] = {
       reinterpret_cast<const void*>(k_gemm_w4<0, false, false, false>),

@@ -41,12 +41,15 @@ FWD = [
     (16384 + 77, 5461, (2048,), (1365,)),
     (8192 + 77, 2048, (5461,), (512,)),
 ]
-# K edges of the K loop: an even number of 32-deep K tiles runs A in 64-deep
-# slots, an odd number in 32-deep stages; each with K % 8 != 0 and odd widths
+# K edges of the K loop: an even number of 32-deep K tiles, or an odd number
+# from 41 on (padded by a zero K tile), runs A in 64-deep slots, a smaller odd
+# number in 32-deep stages; each with K % 8 != 0 and odd widths.  (K = 5461 and
+# 5472 above: 171 K tiles, padded.)
 FWD_K = [
     (22016 + 77, 320, (2048,), (40,)),      # K = 320: the fewest K tiles (10, even)
     (22016 + 77, 352, (2048,), (45,)),      # 11 K tiles (odd), odd z width
     (32768 + 77, 1021, (1000,), (512,)),    # K % 8 != 0, 32 K tiles (even)
+    (32768 + 77, 1053, (1000,), (257,)),    # K % 8 != 0, 33 K tiles (odd), odd z width
 ]
 # dx = dL/do W^T has n output columns: more tokens for three tiles per CU
 DX = [
@@ -56,6 +59,7 @@ DX = [
     (12288 + 77, 5461, (2048,), (1365,)),     # odd output width (dL/dx of down)
     (24576 + 77, 2048, (5461,), (512,)),      # K % 8 != 0 (dL/dx of gate)
     (49152 + 77, 1021, (1021,), (128,)),      # K % 8 != 0 with 32 K tiles (even), odd output width
+    (24576 + 77, 2048, (1053,), (128,)),      # K % 8 != 0 with 33 K tiles (odd)
 ]
 
 
