@@ -21,8 +21,8 @@
 // Why persistent.  With one workgroup per output tile, all 256 workgroups
 // finish their tiles together and write 32 MB at once while no MFMA work is
 // left to overlap it.  Here a finished tile is converted to bf16 pairs in
-// registers and written out 16 stores at a time during the first 8 K tiles of
-// the next tile.
+// registers and written out 16 stores a K tile during the first 8 K tiles of
+// the next tile (8 a K tile over 16 K tiles with A in 64-deep slots).
 //
 // Step h of the flat sequence (K tile t of tile q, LDS stage h % 4):
 //   step 0: 16 MFMAs on fragments (h, 0) (t = 0: accumulators start from
@@ -82,6 +82,8 @@ constexpr int kW4PairBytes = kW4Tile * 2 * kW4K * 2;                      // 32 
 constexpr int kW4PairSlots = 3;
 constexpr int kW4PBBase = kW4PairSlots * kW4PairBytes;                    // 96 KB
 constexpr size_t kW4PLds = size_t(kW4PBBase) + kW4Stages * kW4StageBytes;  // 160 KB
+constexpr int kW4PDrip = 16;                                              // K tiles the stores drip over
+constexpr int kW4PMinKTiles = kW4PDrip + 2;                               // 18: K >= 545
 
 // Output columns come in up to two segments (the forward pass writes y and z
 // in one launch): column tile ct < seg[0].tiles writes columns 256 ct .. of
@@ -179,16 +181,24 @@ __device__ __forceinline__ void w4_wait_vm() {
 }
 
 // VMEM operations issued after the last copy of step h + 1 by the time step
-// (h, 1) waits, for K tile T of a tile (T = 10 stands for every T >= 10).
-// Copies of step h + 3 go out at MFMAs 0, 4, 8, 12 of step (h, 0) and 2, 6,
-// 10, 14 of step (h, 1); during K tiles 0 .. 7 stores go out at the odd MFMAs
-// of both steps.  After copy 7 of step h + 1 (issued in step (h - 2, 1)) come
-// the store at MFMA 15 of that step, all of K tile h - 1 and step (h, 0).
-constexpr bool w4_drip(int T) { return T >= 0 && T < 8; }
-template <int T>
-constexpr int w4_vm_allow() {
-  return (w4_drip(T - 2) ? 1 : 0) + 8 + (w4_drip(T - 1) ? 16 : 0) + 4 + (w4_drip(T) ? 8 : 0);
+// (h, 1) waits, for K tile T of a tile (T past the drip span stands for every
+// later T).  Copies of step h + 3 go out at MFMAs 0, 4, 8, 12 of step (h, 0)
+// and 2, 6, 10, 14 of step (h, 1).  The 128 stores of the previous tile drip
+// out over its first S K tiles: S = 8, at the odd MFMAs of both steps (16 per
+// K tile); S = 16, at MFMAs 3, 7, 11, 15 of both steps (8 per K tile).  After
+// copy 7 of step h + 1 (issued in step (h - 2, 1)) come the store at MFMA 15
+// of that step, all of K tile h - 1 and step (h, 0).
+template <int S>
+constexpr bool w4_drip(int T) {
+  return T >= 0 && T < S;
 }
+template <int T, int S>
+constexpr int w4_vm_allow() {
+  return (w4_drip<S>(T - 2) ? 1 : 0) + 8 + (w4_drip<S>(T - 1) ? 128 / S : 0) + 4 + (w4_drip<S>(T) ? 64 / S : 0);
+}
+static_assert(w4_vm_allow<0, 8>() == 20 && w4_vm_allow<2, 8>() == 37 && w4_vm_allow<2, 16>() == 25 &&
+                  w4_vm_allow<17, 16>() == 13 && w4_vm_allow<18, 16>() == 12,
+              "vmcnt allowances");
 
 // The lane id, computed where it is used (volatile: not merged with another
 // computation of it, so no register holds it across the tile loop).
@@ -557,13 +567,15 @@ __device__ __forceinline__ void w4_copy_one(const W4Lane& L, const W4CopyCursor&
                                            static_cast<int>(vo), 0, 0, 0);
 }
 
-// Store n (0 .. 15) of K tile T: block 2 T + n / 8, row group (n / 2) % 4, row n % 2.
+// Store n (0 .. 128 / S - 1) of K tile T in a drip span of S K tiles: store
+// i = 128 T / S + n of the tile, block i / 8, row group (i / 2) % 4, row i % 2.
 // An even n shuffles the pair of its (block, row group) and keeps the second
 // value in `hold` for store n + 1.
-template <int T>
+template <int T, int S>
 __device__ __forceinline__ void w4_store_one(const W4Out& od, const uint32_t (&raw)[128], bool odd, uint32_t& hold,
                                              int n) {
-  const int b = 2 * T + (n >> 3), gr = (n >> 1) & 3, w = n & 1;
+  const int idx = T * (128 / S) + n;
+  const int b = idx >> 3, gr = (idx >> 1) & 3, w = idx & 1;
   uint32_t v;
   if (w == 0) {
     w4_shuffle(raw[(b * 4 + gr) * 2], raw[(b * 4 + gr) * 2 + 1], odd, v, hold);
@@ -603,7 +615,7 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
                                          int n_my, const W4Walk& wk, const W4Out& od,
                                          uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4],
                                          bool last = false) {
-  const bool odd = w4_drip(T) ? (w4_lane_id() & 1) != 0 : false;
+  const bool odd = w4_drip<8>(T) ? (w4_lane_id() & 1) != 0 : false;
   uint32_t hold = 0;
   const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
   const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
@@ -623,13 +635,13 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
       f[1].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b1 + s0 + (i - 4) * 2048));
     }
     if (i % 4 == 0) w4_copy_one<T>(L, cc, i / 4, oob, k3, s3);
-    if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, i / 2);
+    if constexpr (w4_drip<8>(T)) {
+      if (i % 2 == 1) w4_store_one<T, 8>(od, raw, odd, hold, i / 2);
     }
   }
   w4_pin_acc(acc);
   // step 1: MFMAs on f[1]; reads of f[0] for step h + 1; copies 4 .. 7
-  w4_wait_vm<w4_vm_allow<T>()>();
+  w4_wait_vm<w4_vm_allow<T, 8>()>();
   w4_lds_barrier(f[1]);
   if constexpr (KMASK) w4_mask_k(g, f[1], 1, last);
 #pragma unroll
@@ -642,8 +654,8 @@ __device__ __forceinline__ void w4_ktile(const W4Gemm& g, const W4Lane& L, int h
       f[0].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b0 + s1 + (i - 4) * 2048));
     }
     if (i % 4 == 2) w4_copy_one<T>(L, cc, 4 + i / 4, oob, k3, s3);
-    if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, 8 + i / 2);
+    if constexpr (w4_drip<8>(T)) {
+      if (i % 2 == 1) w4_store_one<T, 8>(od, raw, odd, hold, 8 + i / 2);
     }
   }
   w4_pin(f[0]);
@@ -708,14 +720,15 @@ __device__ __forceinline__ void w4p_copy_b(const W4Lane& L, __amdgpu_buffer_rsrc
                                            static_cast<int>(vo), 0, 0, 0);
 }
 
-// w4_ktile with A in 64-deep slots (T = 10 and 11: any even and odd T >= 10).
+// w4_ktile with A in 64-deep slots (T = 18 and 19: any even and odd T >= 18);
+// the previous tile's stores drip out over K tiles 0 .. 15, 8 per K tile.
 template <int T, bool KMASK, bool ODD>
 __device__ __forceinline__ void w4p_ktile(const W4Gemm& g, const W4Lane& L, int h, W4CopyCursor& cc,
                                           W4PairCursor& ap, int kt, int n_my, const W4Walk& wk, const W4Out& od,
                                           uint32_t (&raw)[128], W4Frags (&f)[2], f32x16 (&acc)[4][4],
                                           bool last = false) {
   constexpr uint32_t e = T & 1;  // K tile h is the first (0) or second (1) of its pair
-  const bool odd = w4_drip(T) ? (w4_lane_id() & 1) != 0 : false;
+  const bool odd = w4_drip<kW4PDrip>(T) ? (w4_lane_id() & 1) != 0 : false;
   uint32_t hold = 0;
   const uint32_t s0 = static_cast<uint32_t>(h & 3) * kW4StageBytes;
   const uint32_t s1 = static_cast<uint32_t>((h + 1) & 3) * kW4StageBytes;
@@ -745,13 +758,13 @@ __device__ __forceinline__ void w4p_ktile(const W4Gemm& g, const W4Lane& L, int 
       const int j = 4 * static_cast<int>(e) + i / 4;
       w4p_copy_a(L, ap.ra, k0, (j & 1) ? oo : oe, sa_copy, j);
     }
-    if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, i / 2);
+    if constexpr (w4_drip<kW4PDrip>(T)) {
+      if (i % 4 == 3) w4_store_one<T, kW4PDrip>(od, raw, odd, hold, i / 4);
     }
   }
   w4_pin_acc(acc);
   // step 1: MFMAs on f[1]; reads of f[0] for step h + 1; B copies of step h + 3
-  w4_wait_vm<w4_vm_allow<T>()>();
+  w4_wait_vm<w4_vm_allow<T, kW4PDrip>()>();
   w4_lds_barrier(f[1]);
   if constexpr (KMASK) w4_mask_k(g, f[1], 1, last);
 #pragma unroll
@@ -764,8 +777,8 @@ __device__ __forceinline__ void w4p_ktile(const W4Gemm& g, const W4Lane& L, int 
       f[0].b[i - 4] = *reinterpret_cast<const w4_lds_u32x4*>(static_cast<uintptr_t>(L.b0 + s1 + (i - 4) * 2048));
     }
     if (i % 4 == 2) w4p_copy_b(L, cc.d.rb, k3, oobb, s3, i / 4);
-    if constexpr (w4_drip(T)) {
-      if (i % 2 == 1) w4_store_one<T>(od, raw, odd, hold, 8 + i / 2);
+    if constexpr (w4_drip<kW4PDrip>(T)) {
+      if (i % 4 == 3) w4_store_one<T, kW4PDrip>(od, raw, odd, hold, 4 + i / 4);
     }
   }
   w4_pin(f[0]);
@@ -861,10 +874,18 @@ __device__ __forceinline__ void gemm_w4_persistent(const W4Gemm& g) {
       w4p_ktile<6, KMASK, ODD>(g, L, h + 6, cc, ap, kt, n_my, wk, od, raw, f, acc);
       w4p_ktile<7, KMASK, ODD>(g, L, h + 7, cc, ap, kt, n_my, wk, od, raw, f, acc);
       w4p_ktile<8, KMASK, ODD>(g, L, h + 8, cc, ap, kt, n_my, wk, od, raw, f, acc);
-      w4p_ktile<9, KMASK, ODD>(g, L, h + 9, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == 9);
-      for (int t = 10; t < kt; t += 2) {
-        w4p_ktile<10, KMASK, ODD>(g, L, h + t, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t);
-        w4p_ktile<11, KMASK, ODD>(g, L, h + t + 1, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t + 1);
+      w4p_ktile<9, KMASK, ODD>(g, L, h + 9, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<10, KMASK, ODD>(g, L, h + 10, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<11, KMASK, ODD>(g, L, h + 11, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<12, KMASK, ODD>(g, L, h + 12, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<13, KMASK, ODD>(g, L, h + 13, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<14, KMASK, ODD>(g, L, h + 14, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<15, KMASK, ODD>(g, L, h + 15, cc, ap, kt, n_my, wk, od, raw, f, acc);
+      w4p_ktile<16, KMASK, ODD>(g, L, h + 16, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == 16);
+      w4p_ktile<17, KMASK, ODD>(g, L, h + 17, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == 17);
+      for (int t = kW4PMinKTiles; t < kt; t += 2) {
+        w4p_ktile<18, KMASK, ODD>(g, L, h + t, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t);
+        w4p_ktile<19, KMASK, ODD>(g, L, h + t + 1, cc, ap, kt, n_my, wk, od, raw, f, acc, kl == t + 1);
       }
     } else {
       w4_ktile<0, KMASK, ODD>(g, L, h + 0, cc, kt, n_my, wk, od, raw, f, acc);

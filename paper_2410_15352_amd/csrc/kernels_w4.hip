@@ -78,10 +78,11 @@ hipError_t gemm_w4_launch(const W4Gemm& g, W4Use use, hipStream_t stream) {
   }
   const bool kmask = g.K % 8 != 0;
   const bool odd = g.seg[0].cols % 2 != 0 || (g.seg[1].tiles > 0 && g.seg[1].cols % 2 != 0);
-  // A in 64-deep slots: an odd number of K tiles is padded by one (a zero K
-  // tile, 1/kt more matrix work), which pays from about 40 K tiles on
+  // A in 64-deep slots (at least kW4PMinKTiles K tiles): an odd number of K
+  // tiles is padded by one (a zero K tile, 1/kt more matrix work), which pays
+  // from about 40 K tiles on
   const int64_t kt = ceil_div(g.K, kW4K);
-  const bool pairs = kt % 2 == 0 || kt >= 41;
+  const bool pairs = kt >= kW4PMinKTiles && (kt % 2 == 0 || kt >= 41);
   const int u = (use == W4Use::kForward ? 0 : 8) + (pairs ? 4 : 0) + (kmask ? 2 : 0) + (odd ? 1 : 0);
   static const void* const fns[kGemmVariants] = {
       reinterpret_cast<const void*>(k_gemm_w4<0, false, false, false>),

@@ -41,13 +41,14 @@ FWD = [
     (16384 + 77, 5461, (2048,), (1365,)),
     (8192 + 77, 2048, (5461,), (512,)),
 ]
-# K edges of the K loop: an even number of 32-deep K tiles, or an odd number
-# from 41 on (padded by a zero K tile), runs A in 64-deep slots, a smaller odd
-# number in 32-deep stages; each with K % 8 != 0 and odd widths.  (K = 5461 and
-# 5472 above: 171 K tiles, padded.)
+# K edges of the K loop: from 18 32-deep K tiles on, an even number of them,
+# or an odd number from 41 on (padded by a zero K tile), runs A in 64-deep
+# slots, the rest in 32-deep stages; each with K % 8 != 0 and odd widths.
+# (K = 5461 and 5472 above: 171 K tiles, padded.)
 FWD_K = [
     (22016 + 77, 320, (2048,), (40,)),      # K = 320: the fewest K tiles (10, even)
     (22016 + 77, 352, (2048,), (45,)),      # 11 K tiles (odd), odd z width
+    (22016 + 77, 571, (2048,), (72,)),      # K % 8 != 0, 18 K tiles: the fewest in 64-deep slots
     (32768 + 77, 1021, (1000,), (512,)),    # K % 8 != 0, 32 K tiles (even)
     (32768 + 77, 1053, (1000,), (257,)),    # K % 8 != 0, 33 K tiles (odd), odd z width
 ]
