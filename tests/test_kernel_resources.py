@@ -1,10 +1,11 @@
 """Register budget of the persistent kernels (CPU only: a compile, no launch).
 
-The persistent GEMM, G^ and decompression kernels run one wave per SIMD and
-keep their accumulators in the 256 accumulation registers; any VGPR spill or
-private (scratch) array inside them turns into scratch-memory traffic whose
-waits share the vector-memory counter with the operand copies, and each such
-wait drains every copy in flight.  The unit is compiled as build.py compiles
+The persistent GEMM and G^ kernels run one wave per SIMD and keep their
+accumulators in the accumulation registers, the decompression runs four
+workgroups per CU in at most 128 registers per lane; any VGPR spill or private
+(scratch) array inside them turns into scratch-memory traffic whose waits
+share the vector-memory counter with the operand copies, and each such wait
+drains every copy in flight.  The unit is compiled as build.py compiles
 it, with the compiler's resource-usage remarks, and every kernel of the unit
 must use no scratch memory and spill no VGPR."""
 import os
