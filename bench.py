@@ -55,8 +55,8 @@ def parse_args():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain copy kernel over 256 MiB first (HBM counter calibration)")
     ap.add_argument("--proj", default="gaussian",
-                    help="projection: gaussian (the paper's method), or sparse-jl[:s] (the ablation's sparse JL, "
-                         "s draws per row, default 8)")
+                    help="projection: gaussian (the paper's method), or sparse-jl[:s][:gather] (the ablation's "
+                         "sparse JL, s draws per row, default 8; :gather computes z by gather-add)")
     ap.add_argument("--model-sweep", action="store_true",
                     help="instead of the benchmark: whole-model training steps of a LLaMA-350M-shaped model "
                          "(baseline, CompAct r=n/4, r=n/8) over batch sizes; one JSON line per point with the "
@@ -490,7 +490,7 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         code = cp.proj_code(args.proj)
-        sparse_s = ((code >> 8) or cp.SPARSE_JL_DEFAULT_S) if (code & 0xFF) == cp.PROJ["sparse-jl"] else 0
+        sparse_s = (((code >> 8) & 0xFF) or cp.SPARSE_JL_DEFAULT_S) if (code & 0xFF) == cp.PROJ["sparse-jl"] else 0
         cpu = cpu_baseline(wl, args.cpu_tokens, sparse_s=sparse_s)
     act = [{"layer": L.name, "n": L.n, "r": L.r, "saved_bytes": 2 * T * L.r, "uncompressed_bytes": 2 * T * L.n}
            for L in wl.distinct_shapes()]

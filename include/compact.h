@@ -93,6 +93,28 @@ typedef enum {
 #define COMPACT_PROJ_SPARSE_JL_S(s) (COMPACT_PROJ_SPARSE_JL | ((s) << 8))
 
 /*
+ * Gather-add forward for the sparse projection (the sparse JL route of §6-§7
+ * to cheaper projections: z as sums of signed input features rather than a
+ * dense product).  OR-ed into a sparse code with at most
+ * COMPACT_GATHER_MAX_S draws per row, it changes how compact_fwd and
+ * compact_fwd_group compute z on the bf16 path with a workspace: y comes from
+ * the persistent GEMM over W^T alone, and z from one gather launch in which
+ * the lane of token t adds, in order of the input feature i and then of the
+ * draw, x[t][i] * bf16(S[i][c] / sqrt(s)) into an fp32 sum per column c (draws
+ * of row i that share a column are merged first, and entries with S[i][c] = 0
+ * are skipped), rounded once to bf16.  y is bitwise the same as without the
+ * flag; z differs from the GEMM paths only in the order of the fp32 additions.
+ * A NaN or infinity at x[t][i] then reaches z[t][c] only where S[i][c] != 0.
+ * The flag is ignored on the fp32 path, without a workspace and by every
+ * other entry point (the backward and Alg. 3 do not depend on it), so one
+ * code can be passed to all of them.  It is an alternative for measurement,
+ * not a faster path: on MI355X the LDS float additions it is built on make
+ * it much slower than the MFMA columns of the fused GEMM at every s.
+ */
+#define COMPACT_PROJ_GATHER (1 << 16)
+#define COMPACT_GATHER_MAX_S 16
+
+/*
  * Forward pass, Alg. 1:  y = x W  and  z = x P.
  *
  *   x  [tokens x n]  (ld ldx)  input activations

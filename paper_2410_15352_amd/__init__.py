@@ -21,19 +21,24 @@ from . import _lib
 F32, BF16 = 0, 1
 PROJ = {"gaussian": 0, "identity": 1, "sparse-jl": 2}
 SPARSE_JL_DEFAULT_S = 8
+PROJ_GATHER = 1 << 16  # COMPACT_PROJ_GATHER: the forward's z of a sparse projection by gather-add
 
 
 def proj_code(proj):
     """The ABI's compact_proj code of a projection: "gaussian", "identity",
-    "sparse-jl" (s = 8 draws per row), "sparse-jl:<s>", or an int code."""
+    "sparse-jl" (s = 8 draws per row), "sparse-jl:<s>", either sparse form
+    with the suffix ":gather" (COMPACT_PROJ_GATHER), or an int code."""
     if isinstance(proj, int):
         return proj
+    flags = 0
+    if proj.startswith("sparse-jl") and proj.endswith(":gather"):
+        proj, flags = proj[: -len(":gather")], PROJ_GATHER
     if proj.startswith("sparse-jl:"):
         s_ = int(proj.split(":", 1)[1])
         if not 1 <= s_ <= 64:
             raise ValueError("sparse-jl draws per row must be in [1, 64]")
-        return PROJ["sparse-jl"] | (s_ << 8)
-    return PROJ[proj]
+        return PROJ["sparse-jl"] | (s_ << 8) | flags
+    return PROJ[proj] | flags
 
 
 __all__ = ["compact_fwd", "compact_fwd_group", "compact_projection", "proj_code", "fwd_group_workspace_bytes", "compact_bwd", "compact_bwd_noalloc", "compact_step", "compact_pstream", "compact_next_seed",

@@ -67,12 +67,19 @@ int check_dense(const char* name, const void* p) {
 int check_shape(int64_t tokens, int64_t n, int64_t m, int64_t r, int proj) {
   if (tokens < 0 || n < 1 || m < 1) return fail(COMPACT_EINVAL, "bad shape tokens=%lld n=%lld m=%lld", (long long)tokens, (long long)n, (long long)m);
   if (r < 1 || r > n) return fail(COMPACT_EINVAL, "rank r=%lld must satisfy 1 <= r <= n=%lld", (long long)r, (long long)n);
-  const int kind = proj & 0xFF, draws = proj >> 8;
+  const int kind = proj & 0xFF, draws = (proj >> 8) & 0xFF, flags = proj >> 16;
   if (proj < 0 || (kind != COMPACT_PROJ_GAUSSIAN && kind != COMPACT_PROJ_IDENTITY && kind != COMPACT_PROJ_SPARSE_JL))
     return fail(COMPACT_EINVAL, "unknown projection %d", proj);
-  if (kind != COMPACT_PROJ_SPARSE_JL && draws != 0) return fail(COMPACT_EINVAL, "unknown projection %d", proj);
+  if (kind != COMPACT_PROJ_SPARSE_JL && (draws != 0 || flags != 0))
+    return fail(COMPACT_EINVAL, "unknown projection %d", proj);
+  if (flags & ~(COMPACT_PROJ_GATHER >> 16)) return fail(COMPACT_EINVAL, "unknown projection %d", proj);
   if (kind == COMPACT_PROJ_SPARSE_JL && draws > kSjltMaxS)
     return fail(COMPACT_EINVAL, "sparse projection: %d draws per row (at most %d)", draws, kSjltMaxS);
+  if ((proj & COMPACT_PROJ_GATHER) && (draws != 0 ? draws : COMPACT_SPARSE_JL_DEFAULT_S) > COMPACT_GATHER_MAX_S)
+    return fail(COMPACT_EUNSUPPORTED, "gather-add forward: %d draws per row (at most %d)",
+                draws != 0 ? draws : COMPACT_SPARSE_JL_DEFAULT_S, COMPACT_GATHER_MAX_S);
+  if ((proj & COMPACT_PROJ_GATHER) && r >= int64_t(kGatherSkip))
+    return fail(COMPACT_EUNSUPPORTED, "gather-add forward: r=%lld (below %u)", (long long)r, kGatherSkip);
   if (kind == COMPACT_PROJ_IDENTITY && r != n) return fail(COMPACT_EINVAL, "identity projection needs r == n (r=%lld, n=%lld)", (long long)r, (long long)n);
   if (n > (int64_t(1) << 31) || r > (int64_t(1) << 31)) return fail(COMPACT_EUNSUPPORTED, "n and r must be below 2^31");
   return COMPACT_OK;
@@ -256,6 +263,22 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
 // start on a 256-row tile.
 int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + round_up(r, kW4Tile); }
 
+// Gather-add tables (COMPACT_PROJ_GATHER): [n + pad][s] entries per
+// projection, each 256-byte aligned.
+size_t gather_table_bytes(int64_t n, int s) {
+  return size_t(round_up((n * s + kGatherPad) * int64_t(sizeof(uint32_t)), int64_t(kWsAlign)));
+}
+
+// Forward workspace of `count` projections of widths msum and ranks rsum in
+// total: the stacked operand, or with the gather flag W^T alone followed by
+// the tables (at most kGatherMaxS draws per row), whichever is larger.
+size_t fwd_ws_bytes(int64_t n, int64_t msum, int64_t rsum, int count) {
+  const size_t stacked = size_t(stacked_rows(msum, rsum)) * size_t(pt_ld(n)) * sizeof(uint16_t);
+  const size_t gathered = size_t(round_up(msum, kW4Tile)) * size_t(pt_ld(n)) * sizeof(uint16_t) +
+                          size_t(count) * gather_table_bytes(n, kGatherMaxS);
+  return std::max(stacked, gathered) + kWsAlign;
+}
+
 // A K-tiled B operand of `rows` rows and K columns fits the persistent GEMM's
 // 32-bit buffer offsets.
 bool tiled_fits(int64_t rows, int64_t K) { return ceil_div(K, kW4K) * rows * 64 < (int64_t(1) << 31); }
@@ -272,8 +295,14 @@ ProjDesc proj_desc(int proj, int64_t r) {
   ProjDesc d{};
   d.kind = proj & 0xFF;
   d.r = static_cast<int>(r);
-  d.s = d.kind == COMPACT_PROJ_SPARSE_JL ? ((proj >> 8) != 0 ? (proj >> 8) : COMPACT_SPARSE_JL_DEFAULT_S) : 0;
+  const int draws = (proj >> 8) & 0xFF;
+  d.s = d.kind == COMPACT_PROJ_SPARSE_JL ? (draws != 0 ? draws : COMPACT_SPARSE_JL_DEFAULT_S) : 0;
   return d;
+}
+
+// The forward computes z of a sparse projection by the gather-add launch.
+bool proj_gather(int proj) {
+  return (proj & 0xFF) == COMPACT_PROJ_SPARSE_JL && (proj & COMPACT_PROJ_GATHER) != 0;
 }
 
 // P = scale x the unscaled stream: 1/sqrt(r) for the Gaussian, 1/sqrt(s) for
@@ -359,7 +388,7 @@ int64_t compact_saved_activation_elems(int64_t tokens, int64_t n, int64_t r) {
 
 size_t compact_fwd_workspace_bytes(int64_t n, int64_t m, int64_t r, int dtype) {
   if (dtype != COMPACT_BF16 || n < 1 || m < 1 || r < 1) return 0;
-  return size_t(stacked_rows(m, r)) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
+  return fwd_ws_bytes(n, m, r, 1);
 }
 
 size_t compact_bwd_workspace_bytes(int64_t tokens, int64_t n, int64_t m, int64_t r, int dtype) {
@@ -394,9 +423,7 @@ struct FwdGroup {
   int64_t msum, rsum;
 };
 
-size_t fwd_group_ws_bytes(int64_t n, const FwdGroup& G) {
-  return size_t(stacked_rows(G.msum, G.rsum)) * size_t(pt_ld(n)) * sizeof(uint16_t) + kWsAlign;
-}
+size_t fwd_group_ws_bytes(int64_t n, const FwdGroup& G) { return fwd_ws_bytes(n, G.msum, G.rsum, G.count); }
 
 // The persistent bf16 forward over the stacked operand [W^T; pad to 256;
 // P_0^T; P_1^T; ...]: y in the first column tiles, z after.  Sets `taken`
@@ -407,12 +434,17 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
                  hipStream_t s, bool& taken) {
   int st;
   const int64_t ldb = pt_ld(n);
-  const int64_t rows_b = stacked_rows(G.msum, G.rsum);
-  taken = ws != nullptr && gemm_w4_eligible(tokens, n, ldx, ldb, rows_b, ldy, G.msum, ldz, G.rsum, true) &&
+  // gather-add z: the GEMM computes y alone and its B operand is W^T alone
+  const bool gather = proj_gather(proj);
+  const int64_t rows_b = gather ? round_up(G.msum, kW4Tile) : stacked_rows(G.msum, G.rsum);
+  taken = ws != nullptr &&
+          gemm_w4_eligible(tokens, n, ldx, ldb, rows_b, ldy, G.msum, gather ? 0 : ldz, gather ? 0 : G.rsum, true) &&
           tiled_fits(rows_b, n);
   if (!taken) return COMPACT_OK;
   uint16_t* bs = static_cast<uint16_t*>(align_ws(ws));
   const int64_t mp = round_up(G.msum, kW4Tile);
+  const int sparse_s = proj_desc(proj, 1).s;
+  char* tables = reinterpret_cast<char*>(bs) + round_up(rows_b * ldb * int64_t(sizeof(uint16_t)), int64_t(kWsAlign));
   FwdStage fs{};
   fs.W = static_cast<const uint16_t*>(W); fs.ldw = ldw; fs.n = n; fs.m = G.msum;
   fs.b = PanelOut{bs, ldb, rows_b}; fs.ldb = ldb;
@@ -427,7 +459,12 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
     fs.r[j] = G.r[j];
     fs.key[j] = philox_key(G.seed[j]);
     fs.pscale[j] = proj_scale(proj, G.r[j]);
-    fs.pt_begin[j + 1] = fs.pt_begin[j] + pt_blocks(fs.kind, G.r[j], ldb);
+    if (gather) {  // a table row per thread, and one thread for the pad
+      fs.table[j] = reinterpret_cast<uint32_t*>(tables + size_t(j) * gather_table_bytes(n, sparse_s));
+      fs.pt_begin[j + 1] = fs.pt_begin[j] + static_cast<int>(ceil_div(n + 1, 256));
+    } else {
+      fs.pt_begin[j + 1] = fs.pt_begin[j] + pt_blocks(fs.kind, G.r[j], ldb);
+    }
     row += G.r[j];
   }
   const int64_t stage_blocks = fs.pt_begin[G.count] + ceil_div(n, 64) * fs.tiles_c;
@@ -439,14 +476,30 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
   g.M = static_cast<int>(tokens); g.K = static_cast<int>(n);
   g.B = bs; g.ldb = static_cast<int>(ldb); g.rows_b = static_cast<int>(rows_b); g.b_tiled = 1;
   g.seg[0] = W4Seg{static_cast<uint16_t*>(y), static_cast<int>(ldy), static_cast<int>(G.msum), w4_tiles(G.msum)};
-  g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(G.rsum), w4_tiles(G.rsum)};
+  if (!gather)
+    g.seg[1] = W4Seg{static_cast<uint16_t*>(z), static_cast<int>(ldz), static_cast<int>(G.rsum), w4_tiles(G.rsum)};
   g.tiles_n = g.seg[0].tiles + g.seg[1].tiles;
   const int64_t tiles = ceil_div(tokens, kW4Tile) * g.tiles_n;
   if (tiles > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "grid too large");
   g.tiles = static_cast<int>(tiles);
   const hipError_t e = gemm_w4_launch(g, W4Use::kForward, s);
   if (e != hipSuccess) return fail(COMPACT_EHIP, "forward GEMM (bf16): %s", hipGetErrorString(e));
-  return COMPACT_OK;
+  if (!gather) return COMPACT_OK;
+  GatherParams gp{};
+  gp.x = static_cast<const uint16_t*>(x); gp.ldx = ldx; gp.T = tokens; gp.ldz = ldz;
+  gp.n = static_cast<int>(n); gp.s = sparse_s;
+  gp.count = G.count;
+  int64_t ro = 0;
+  gp.chunk_begin[0] = 0;
+  for (int j = 0; j < G.count; ++j) {
+    gp.layer[j] = GatherLayer{fs.table[j], static_cast<uint16_t*>(z) + ro, static_cast<int>(G.r[j])};
+    gp.chunk_begin[j + 1] = gp.chunk_begin[j] + static_cast<int>(ceil_div(G.r[j], kGatherChunk));
+    ro += G.r[j];
+  }
+  const int64_t blocks = ceil_div(tokens, kGatherTok) * gp.chunk_begin[G.count];
+  if (blocks > 0x7FFFFFFF) return fail(COMPACT_EUNSUPPORTED, "gather grid too large");
+  hipLaunchKernelGGL(k_sjl_gather, dim3(static_cast<uint32_t>(blocks)), dim3(kGatherTok), 0, s, gp);
+  return check_launch("gather-add z (bf16)");
 }
 
 }  // namespace

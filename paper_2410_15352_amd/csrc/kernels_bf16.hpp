@@ -128,6 +128,52 @@ __device__ __forceinline__ void transpose_tile_bf16(const uint16_t* in, int64_t 
 // the staged operand.
 constexpr int kMaxGroup = 8;  // projections sharing one input
 
+// ---------------------------------------------------------------------------
+// Gather-add z of a sparse projection (COMPACT_PROJ_GATHER).  Row i of S has
+// s <= kGatherMaxS draws (pstream.hpp); its table row holds s entries
+//   column | bf16(S[i][column] * scale) << 16
+// at the first draw of each column (the signs of the row's draws on that
+// column summed), and kGatherSkip where a draw repeats an earlier column or
+// the signs cancel.  The value half, read as fp32 bits, is that bf16 value
+// exactly: the same P = bf16(S / sqrt(s)) element the P^T panel holds.
+constexpr int kGatherMaxS = 16;
+constexpr uint32_t kGatherSkip = 0xFFFFu;  // column of a skipped entry
+constexpr int kGatherPad = 16;             // entries after the last row (whole-row reads)
+
+__device__ __forceinline__ void gather_table_row(const ProjDesc& d, PhiloxKey key, float scale, uint32_t i,
+                                                 uint32_t* row) {
+  uint32_t h[kGatherMaxS];
+  float v[kGatherMaxS];
+#pragma unroll
+  for (int p = 0; p < kGatherMaxS / 2; ++p) {
+    h[2 * p] = h[2 * p + 1] = kGatherSkip;
+    v[2 * p] = v[2 * p + 1] = 0.0f;
+    if (2 * p < d.s) {
+      sjlt_pair(key, i, static_cast<uint32_t>(p), static_cast<uint32_t>(d.r), h[2 * p], v[2 * p], h[2 * p + 1],
+                v[2 * p + 1]);
+      if (2 * p + 1 >= d.s) {  // odd s: the pair's second draw is not taken
+        h[2 * p + 1] = kGatherSkip;
+        v[2 * p + 1] = 0.0f;
+      }
+    }
+  }
+  // a later draw on a column adds its sign to the first draw on it
+#pragma unroll
+  for (int q = 1; q < kGatherMaxS; ++q)
+#pragma unroll
+    for (int p = 0; p < q; ++p)
+      if (h[q] != kGatherSkip && h[p] == h[q]) {
+        v[p] += v[q];
+        h[q] = kGatherSkip;
+      }
+#pragma unroll
+  for (int q = 0; q < kGatherMaxS; ++q)
+    if (q < d.s)
+      row[q] = (h[q] == kGatherSkip || v[q] == 0.0f)
+                   ? kGatherSkip
+                   : (h[q] | (static_cast<uint32_t>(f32_to_bf16(v[q] * scale)) << 16));
+}
+
 struct FwdStage {
   const uint16_t* W;
   int64_t ldw, n, m;      // W [n x m]; m = the sum of the projections' widths
@@ -141,6 +187,7 @@ struct FwdStage {
   int64_t r[kMaxGroup];
   PhiloxKey key[kMaxGroup];
   float pscale[kMaxGroup];
+  uint32_t* table[kMaxGroup];   // gather-add tables ([n + pad][s]) instead of P^T rows, or NULL
 };
 
 __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
@@ -149,12 +196,107 @@ __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
     int j = 0;
     while (j + 1 < a.count && a.pt_begin[j + 1] <= b) ++j;
     const int64_t u = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
+    const ProjDesc d{a.kind, static_cast<int>(a.r[j]), a.sparse_s};
+    if (a.table[j] != nullptr) {  // one table row per thread; the pad rows skip
+      if (u >= a.n + 1) return;
+      if (u < a.n)
+        gather_table_row(d, a.key[j], a.pscale[j], static_cast<uint32_t>(u), a.table[j] + u * a.sparse_s);
+      else
+        for (int q = 0; q < kGatherPad; ++q) a.table[j][a.n * a.sparse_s + q] = kGatherSkip;
+      return;
+    }
     if (u >= proj_t_units(a.kind, a.r[j], a.ldb)) return;
-    proj_t_unit(ProjDesc{a.kind, static_cast<int>(a.r[j]), a.sparse_s}, a.key[j], a.n, a.pscale[j], a.b,
-                a.row_off[j], a.ldb, u);
+    proj_t_unit(d, a.key[j], a.n, a.pscale[j], a.b, a.row_off[j], a.ldb, u);
   } else {
     transpose_tile_bf16(a.W, a.ldw, a.n, a.m, a.b, a.tiles_c, b - a.pt_begin[a.count]);
   }
+}
+
+// z_j = x P_j for sparse projections by gather-add (COMPACT_PROJ_GATHER).
+// One workgroup is one wave: lane L owns token t = 64 b + L and an fp32 row of
+// kGatherChunk columns of z_j in LDS (plus one dummy column that takes the
+// skipped entries).  For each input feature i in order and each of the s
+// table entries of row i in order, the lane adds x[t][i] * P[i][c] (exact in
+// fp32: two bf16 factors) into column c of its row; the entry is the same for
+// every lane, so the work per entry is one multiply, one address add and one
+// LDS add, with the table read through the scalar cache.  Rows of 129 floats
+// put the 64 lanes of an LDS access on distinct banks.  The sum is rounded
+// once to bf16 and stored row by row (16-byte stores).
+// Workgroup b: token block b / chunks, column chunk b % chunks (the chunks of
+// a token block are adjacent in the grid, so x is read from memory once).
+constexpr int kGatherChunk = 128;
+constexpr int kGatherTok = 64;
+constexpr int kGatherRow = kGatherChunk + 1;
+
+struct GatherLayer {
+  const uint32_t* table;  // [n + pad][s]
+  uint16_t* z;            // first column of z_j
+  int r;
+};
+
+struct GatherParams {
+  const uint16_t* x;
+  int64_t ldx, T, ldz;
+  int n, s;
+  int count;
+  GatherLayer layer[kMaxGroup];
+  int chunk_begin[kMaxGroup + 1];  // first column chunk of each projection
+};
+
+__global__ __launch_bounds__(kGatherTok) void k_sjl_gather(GatherParams g) {
+  __shared__ float acc[kGatherTok * kGatherRow];
+  const int chunks = g.chunk_begin[g.count];
+  const int b = static_cast<int>(blockIdx.x);
+  const int tb = b / chunks, ch = b - tb * chunks;
+  const int l = batch_layer_of(g.chunk_begin, g.count, ch);
+  const GatherLayer& L = g.layer[l];
+  const uint32_t c0 = static_cast<uint32_t>(ch - g.chunk_begin[l]) * kGatherChunk;
+  const int lane = static_cast<int>(threadIdx.x);
+  const int64_t t = static_cast<int64_t>(tb) * kGatherTok + lane;
+  const bool live = t < g.T;
+  float* my = acc + lane * kGatherRow;
+  for (int c = 0; c < kGatherRow; ++c) my[c] = 0.0f;
+  // lanes past T read the last token's row and store nothing; the 16-byte
+  // chunk holding x[t][i0 .. i0 + 7] lies inside the row's leading dimension
+  // (a multiple of 8), and features past n are not used
+  const uint16_t* xr = g.x + (live ? t : g.T - 1) * g.ldx;
+  // the table is read-only in this kernel: read through the constant address
+  // space, so that wave-uniform reads become scalar loads
+  typedef __attribute__((address_space(4))) const uint32_t const_u32;
+  const_u32* tab = (const_u32*)(L.table);
+  const int s = g.s;
+  u32x4 xn = *reinterpret_cast<const u32x4*>(xr);
+  for (int i0 = 0; i0 < g.n; i0 += 8) {
+    const u32x4 xv = xn;
+    if (i0 + 8 < g.n) xn = *reinterpret_cast<const u32x4*>(xr + i0 + 8);  // the next chunk, one step ahead
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (i0 + e >= g.n) break;
+      const uint32_t w = xv[e >> 1];
+      const float xf = __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+      // the table row is the same for every lane: a wave-uniform index, so
+      // its entries come through the scalar cache
+      const int row = __builtin_amdgcn_readfirstlane(i0 + e);
+      const_u32* ent = tab + static_cast<int64_t>(row) * s;
+      for (int q = 0; q < s; ++q) {
+        const uint32_t en = ent[q];
+        const uint32_t d = min((en & 0xFFFFu) - c0, static_cast<uint32_t>(kGatherChunk));
+        __hip_atomic_fetch_add(my + d, xf * __uint_as_float(en & 0xFFFF0000u), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  }
+  if (!live) return;
+  const int cnt = min(kGatherChunk, L.r - static_cast<int>(c0));
+  uint16_t* zr = L.z + t * g.ldz + c0;
+  int c = 0;
+  for (; c + 8 <= cnt; c += 8) {
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = pack_bf16x2(my[c + 2 * k], my[c + 2 * k + 1]);
+    *reinterpret_cast<u32x4*>(zr + c) = o;
+  }
+  for (; c < cnt; ++c) zr[c] = f32_to_bf16(my[c]);
 }
 
 // The dx GEMM's B operand, W [n x m] (row R = input feature, K = m), copied

@@ -95,6 +95,11 @@ FAKE = 0x100000  # an aligned non-NULL address; never dereferenced (validation f
     (dict(proj=4 << 8), -1),         # draws given to the Gaussian
     (dict(proj=-1), -1),
     (dict(proj=2 | (64 << 8), ws=FAKE, ws_bytes=16), -4),  # a valid sparse code reaches the workspace check
+    (dict(proj=0 | (1 << 16)), -1),          # the gather flag on the Gaussian
+    (dict(proj=2 | (1 << 17)), -1),          # an unknown flag bit
+    (dict(proj=2 | (17 << 8) | (1 << 16)), -3),  # gather-add: at most 16 draws per row
+    (dict(proj=2 | (16 << 8) | (1 << 16), ws=FAKE, ws_bytes=16), -4),  # a valid gather code
+    (dict(proj=2 | (1 << 16), n=70000, r=65535), -3),  # gather-add: r below 65535
     (dict(ldx=1000), -1),           # ld < n
     (dict(ldx=1028), -2),           # bf16 ld not a multiple of 8
     (dict(x=FAKE + 2), -2),         # misaligned pointer

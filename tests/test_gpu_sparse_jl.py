@@ -14,6 +14,11 @@ sparse JL matrices, §5) against the fp64 oracle.
   to bf16, of the (at most s nonzero) terms' sum and of W, for ragged widths,
   rows padded past m (a column slice), wide rows and s = 64 with repeated
   columns.
+* The gather-add forward (COMPACT_PROJ_GATHER): z against the oracle element
+  by element for s = 1, 3, 8, 16, ragged T and n and r over several column
+  chunks; y bitwise the flag-free y; deterministic; a group bitwise its
+  per-projection calls; a NaN in x reaches exactly the columns its row of S
+  draws; the flag ignored where the persistent GEMM does not run.
 """
 import numpy as np
 import pytest
@@ -204,3 +209,109 @@ def test_step_update_every_element(case):
     if ldw > m:
         full = Wd.as_strided((n, ldw), (Wd.stride(0), 1))
         assert not torch.any(full[:, m:].float() != 0)
+
+
+# Gather-add forward (COMPACT_PROJ_GATHER): z = sum over features i, in order,
+# of x[t][i] * bf16(S[i][c] / sqrt(s)) in fp32.  Shapes the persistent GEMM
+# takes (n >= 320): token counts with a partial 64-token block, n with a
+# partial 8-feature chunk (333), r over one, two and three 128-column chunks,
+# and s = 1, 3 (odd), 8 and 16 (the largest the flag takes).
+GATHER_SHAPES = [(300, 512, 512, 128), (1000, 1376, 512, 344), (777, 333, 136, 200), (65, 1024, 2736, 342),
+                 (130, 2736, 1024, 342)]
+
+
+def _bf(rows, cols):
+    return empty(rows, cols, "bf16", ld_for(cols, "bf16"))
+
+
+def _gather_ref(x, seed, r, s):
+    P = sparse_jl_raw(seed, x.shape[1], r, s) / np.sqrt(s)
+    return x.astype(np.float64) @ P, np.abs(x.astype(np.float64)) @ np.abs(P)
+
+
+@pytest.mark.parametrize("shape", GATHER_SHAPES, ids=lambda sh: "T{}-n{}-m{}-r{}".format(*sh))
+@pytest.mark.parametrize("s", [1, 3, 8, 16])
+def test_gather_forward_parity(shape, s):
+    T, n, m, r = shape
+    seed = (21 << 32) | (n + s)
+    x, W = fwd_inputs(T, n, m, "bf16", data_seed=T + 3 * s)
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(m, "bf16"))
+    y, z, y2, z2 = _bf(T, m), _bf(T, r), _bf(T, m), _bf(T, r)
+    yd, zd = _bf(T, m), _bf(T, r)
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, 1))
+    cp.compact_fwd(xd, Wd, y, z, seed, proj=f"sparse-jl:{s}:gather", ws=ws)
+    cp.compact_fwd(xd, Wd, yd, zd, seed, proj=f"sparse-jl:{s}", ws=ws)
+    cp.compact_fwd(xd, Wd, y2, z2, seed, proj=f"sparse-jl:{s}:gather", ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), yd.view(torch.int16)), "the flag changed y"
+    assert torch.equal(z.view(torch.int16), z2.view(torch.int16)), "gather-add z not deterministic"
+    z_ref, absprod = _gather_ref(x, seed, r, s)
+    # each term carries P rounded to bf16 (2^-8 of its share) and the sum at
+    # most n terms of fp32 rounding
+    assert_elementwise(to_np(z), z_ref, absprod, K=n, operand_rel=BF16_U, what="gather-add z")
+    assert_elementwise(to_np(zd), z_ref, absprod, K=n, operand_rel=BF16_U, what="MFMA z")
+
+
+def test_gather_group_equals_per_projection():
+    T, n, ms, rs = 333, 1024, (512, 512, 512), (128, 136, 64)
+    seeds = [((j + 5) << 32) | 13 for j in range(3)]
+    x, _ = fwd_inputs(T, n, 8, "bf16", data_seed=91)
+    W = np.concatenate([fwd_inputs(8, n, m, "bf16", data_seed=92 + j)[1] for j, m in enumerate(ms)], axis=1)
+    M, R = sum(ms), sum(rs)
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(M, "bf16"))
+    y, z = _bf(T, M), _bf(T, R)
+    y1, z1 = _bf(T, M), _bf(T, R)
+    proj = "sparse-jl:4:gather"
+    cp.compact_fwd_group(xd, Wd, y, z, ms, rs, seeds, proj=proj,
+                         ws=workspace(cp.fwd_group_workspace_bytes(n, ms, rs)))
+    mo = ro = 0
+    for j, (m, r) in enumerate(zip(ms, rs)):
+        cp.compact_fwd(xd, Wd[:, mo:mo + m], y1[:, mo:mo + m], z1[:, ro:ro + r], seeds[j], proj=proj,
+                       ws=workspace(cp.fwd_workspace_bytes(n, m, r)))
+        mo += m
+        ro += r
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y1.view(torch.int16))
+    assert torch.equal(z.view(torch.int16), z1.view(torch.int16))
+    ro = 0
+    for j, r in enumerate(rs):
+        z_ref, absprod = _gather_ref(x, seeds[j], r, 4)
+        assert_elementwise(to_np(z)[:, ro:ro + r], z_ref, absprod, K=n, operand_rel=BF16_U, what=f"z_{j}")
+        ro += r
+
+
+def test_gather_nan_reaches_only_drawn_columns():
+    # the gather path's own semantics: a NaN at x[t][i] reaches z[t][c] only
+    # where S[i][c] != 0 (the MFMA path multiplies it by every P[i][c], zeros
+    # included), so this also shows that the gather launch computed z
+    T, n, m, r, s, seed = 200, 512, 256, 128, 8, (4 << 32) | 9
+    x, W = fwd_inputs(T, n, m, "bf16", data_seed=5)
+    t0, i0 = 70, 301
+    x[t0, i0] = np.nan
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(m, "bf16"))
+    y, z, zd = _bf(T, m), _bf(T, r), _bf(T, r)
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, 1))
+    cp.compact_fwd(xd, Wd, y, z, seed, proj=f"sparse-jl:{s}:gather", ws=ws)
+    cp.compact_fwd(xd, Wd, y, zd, seed, proj=f"sparse-jl:{s}", ws=ws)
+    torch.cuda.synchronize()
+    zg, zm = to_np(z), to_np(zd)
+    drawn = sparse_jl_raw(seed, n, r, s)[i0] != 0
+    assert np.array_equal(np.isnan(zg[t0]), drawn)
+    assert np.isnan(zm[t0]).all()
+    assert np.isfinite(np.delete(zg, t0, axis=0)).all()
+    assert np.isnan(to_np(y)[t0]).all()
+
+
+@pytest.mark.parametrize("n,use_ws", [(200, True), (512, False)])
+def test_gather_flag_ignored_off_the_persistent_path(n, use_ws):
+    # n < 320 (the fused 8-wave GEMM) or no workspace: z as without the flag
+    T, m, r, s, seed = 150, 136, 24, 8, (8 << 32) | 3
+    x, W = fwd_inputs(T, n, m, "bf16", data_seed=n)
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(m, "bf16"))
+    y, z, y2, z2 = _bf(T, m), _bf(T, r), _bf(T, m), _bf(T, r)
+    ws = workspace(cp.fwd_workspace_bytes(n, m, r, 1)) if use_ws else None
+    cp.compact_fwd(xd, Wd, y, z, seed, proj=f"sparse-jl:{s}:gather", ws=ws)
+    cp.compact_fwd(xd, Wd, y2, z2, seed, proj=f"sparse-jl:{s}", ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(z.view(torch.int16), z2.view(torch.int16))
