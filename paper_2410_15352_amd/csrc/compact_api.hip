@@ -263,10 +263,10 @@ int launch_ghat_group(const GhatGroupPlan& g, int64_t tokens, const void* const*
 // start on a 256-row tile.
 int64_t stacked_rows(int64_t m, int64_t r) { return round_up(m, kW4Tile) + round_up(r, kW4Tile); }
 
-// Gather-add tables (COMPACT_PROJ_GATHER): [n + pad][s] entries per
-// projection, each 256-byte aligned.
+// Gather-add tables (COMPACT_PROJ_GATHER): [n][s] entries per projection,
+// each 256-byte aligned.
 size_t gather_table_bytes(int64_t n, int s) {
-  return size_t(round_up((n * s + kGatherPad) * int64_t(sizeof(uint32_t)), int64_t(kWsAlign)));
+  return size_t(round_up(n * s * int64_t(sizeof(uint32_t)), int64_t(kWsAlign)));
 }
 
 // Forward workspace of `count` projections of widths msum and ranks rsum in
@@ -459,9 +459,9 @@ int fwd_group_w4(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y
     fs.r[j] = G.r[j];
     fs.key[j] = philox_key(G.seed[j]);
     fs.pscale[j] = proj_scale(proj, G.r[j]);
-    if (gather) {  // a table row per thread, and one thread for the pad
+    if (gather) {  // a table row per thread
       fs.table[j] = reinterpret_cast<uint32_t*>(tables + size_t(j) * gather_table_bytes(n, sparse_s));
-      fs.pt_begin[j + 1] = fs.pt_begin[j] + static_cast<int>(ceil_div(n + 1, 256));
+      fs.pt_begin[j + 1] = fs.pt_begin[j] + static_cast<int>(ceil_div(n, 256));
     } else {
       fs.pt_begin[j + 1] = fs.pt_begin[j] + pt_blocks(fs.kind, G.r[j], ldb);
     }

@@ -138,7 +138,6 @@ constexpr int kMaxGroup = 8;  // projections sharing one input
 // exactly: the same P = bf16(S / sqrt(s)) element the P^T panel holds.
 constexpr int kGatherMaxS = 16;
 constexpr uint32_t kGatherSkip = 0xFFFFu;  // column of a skipped entry
-constexpr int kGatherPad = 16;             // entries after the last row (whole-row reads)
 
 __device__ __forceinline__ void gather_table_row(const ProjDesc& d, PhiloxKey key, float scale, uint32_t i,
                                                  uint32_t* row) {
@@ -187,7 +186,7 @@ struct FwdStage {
   int64_t r[kMaxGroup];
   PhiloxKey key[kMaxGroup];
   float pscale[kMaxGroup];
-  uint32_t* table[kMaxGroup];   // gather-add tables ([n + pad][s]) instead of P^T rows, or NULL
+  uint32_t* table[kMaxGroup];   // gather-add tables ([n][s]) instead of P^T rows, or NULL
 };
 
 __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
@@ -197,12 +196,8 @@ __global__ __launch_bounds__(256) void k_fwd_stage_bf16(FwdStage a) {
     while (j + 1 < a.count && a.pt_begin[j + 1] <= b) ++j;
     const int64_t u = static_cast<int64_t>(b - a.pt_begin[j]) * 256 + threadIdx.x;
     const ProjDesc d{a.kind, static_cast<int>(a.r[j]), a.sparse_s};
-    if (a.table[j] != nullptr) {  // one table row per thread; the pad rows skip
-      if (u >= a.n + 1) return;
-      if (u < a.n)
-        gather_table_row(d, a.key[j], a.pscale[j], static_cast<uint32_t>(u), a.table[j] + u * a.sparse_s);
-      else
-        for (int q = 0; q < kGatherPad; ++q) a.table[j][a.n * a.sparse_s + q] = kGatherSkip;
+    if (a.table[j] != nullptr) {  // one table row per thread
+      if (u < a.n) gather_table_row(d, a.key[j], a.pscale[j], static_cast<uint32_t>(u), a.table[j] + u * a.sparse_s);
       return;
     }
     if (u >= proj_t_units(a.kind, a.r[j], a.ldb)) return;
@@ -229,7 +224,7 @@ constexpr int kGatherTok = 64;
 constexpr int kGatherRow = kGatherChunk + 1;
 
 struct GatherLayer {
-  const uint32_t* table;  // [n + pad][s]
+  const uint32_t* table;  // [n][s]
   uint16_t* z;            // first column of z_j
   int r;
 };
