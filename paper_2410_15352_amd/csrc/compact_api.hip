@@ -125,9 +125,9 @@ SplitPlan ghat_plan(int64_t tokens, int64_t r, int64_t m) {
 
 // Split-K plan of the transposing-read G^ kernel (gemm_ghat.hpp) for one or
 // more projections of the same tokens (one launch): tm x tn tiles (256 x 256
-// when every projection of the launch has r >= 256 and 256-row tiles pad r no
-// further than 128-row ones; else 384 x 128 when 256 < r and 384-row tiles
-// pad no further; else 128 x 256), one split count for all of them,
+// when every projection of the launch has r >= 1024, or r >= 256 and 256-row
+// tiles pad r no further than 128-row ones; else 384 x 128 when 256 < r and
+// 384-row tiles pad no further; else 128 x 256), one split count for all of them,
 // at most one workgroup per CU (256 on MI355X), splits of whole 32-token K
 // tiles.  Projection j's partial sums take splits x (tiles_r tm) x
 // (tiles_m tn) fp32 at byte offset part_off[j].
@@ -144,8 +144,13 @@ bool ghat_tall_fits(int64_t r) {
   return r > 256 && round_up(r, kGhTallTm) <= round_up(r, kGhTm);
 }
 
+// From r = 1024 on the 256 x 256 tiles are taken whatever their padding (at
+// most 1280 rows for 1152, 11%): there G^ is bound by the MFMAs and their
+// fragment reads, not by HBM, and these tiles read a third fewer fragments per
+// MFMA than the 128-row ones (LLaMA-1B's down at r = 1365: G^ phase 42.9 ->
+// 41.0 ms per step, measured on one box).
 bool ghat_square_fits(int64_t r) {
-  return r >= 256 && round_up(r, kGhSqTm) <= round_up(r, kGhTm);
+  return r >= 1024 || (r >= 256 && round_up(r, kGhSqTm) <= round_up(r, kGhTm));
 }
 
 GhatGroupPlan ghat_group_plan(int64_t tokens, int count, const int64_t* r, const int64_t* m) {

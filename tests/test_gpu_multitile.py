@@ -160,12 +160,14 @@ def test_multitile_dx_every_element(case):
 # projection of the launch with 256 < r, no more padding than 128-row tiles
 # and not a fit for 256-row ones): a group of two such projections; and on
 # the 256 x 256 tiles: r = 512 and 256 (LLaMA-1B at n/4 and n/8), a group of
-# both, and r = 682 (LLaMA-1B's down at n/8)
+# both, r = 682 (LLaMA-1B's down at n/8), and r >= 1024 padded past what
+# 128-row tiles would (1365 among the forward groups; 1100 with a ragged m)
 GHAT = FWD + [
     (16384 + 77, 1024, (1024, 520), (344, 300)),
     (8192 + 77, 5461, (2048,), (682,)),
     (16384 + 77, 2048, (2048, 2048, 2048), (512, 512, 512)),
     (8192 + 77, 2048, (2048, 1000), (256, 512)),
+    (4096 + 77, 2048, (700,), (1100,)),
 ]
 
 
