@@ -18,7 +18,8 @@ sparse JL matrices, §5) against the fp64 oracle.
   by element for s = 1, 3, 8, 16, ragged T and n and r over several column
   chunks; y bitwise the flag-free y; deterministic; a group bitwise its
   per-projection calls; a NaN in x reaches exactly the columns its row of S
-  draws; the flag ignored where the persistent GEMM does not run.
+  draws; the flag ignored where the persistent GEMM does not run; one token,
+  the smallest n of the persistent path, odd r, eight projections, r = n.
 """
 import numpy as np
 import pytest
@@ -315,3 +316,26 @@ def test_gather_flag_ignored_off_the_persistent_path(n, use_ws):
     torch.cuda.synchronize()
     assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
     assert torch.equal(z.view(torch.int16), z2.view(torch.int16))
+
+
+@pytest.mark.parametrize("T,ms,rs,s", [(1, (64,), (13,), 2),                       # one token, odd r
+                                       (129, (64,) * 7 + (40,), (8,) * 7 + (13,), 5),  # 8 projections
+                                       (64, (320,), (320,), 16)])                     # r = n, s at its maximum
+def test_gather_edge_cases(T, ms, rs, s):
+    n = 320  # the smallest n the persistent GEMM (and so the gather path) takes
+    seeds = [((j + 11) << 32) | 7 for j in range(len(ms))]
+    x, _ = fwd_inputs(T, n, 8, "bf16", data_seed=T + 5)
+    W = np.concatenate([fwd_inputs(8, n, m, "bf16", data_seed=40 + j)[1] for j, m in enumerate(ms)], axis=1)
+    M, R = sum(ms), sum(rs)
+    xd, Wd = to_dev(x, "bf16", ld_for(n, "bf16")), to_dev(W, "bf16", ld_for(M, "bf16"))
+    y, z, y2, z2 = _bf(T, M), _bf(T, R), _bf(T, M), _bf(T, R)
+    ws = workspace(cp.fwd_group_workspace_bytes(n, list(ms), list(rs)))
+    cp.compact_fwd_group(xd, Wd, y, z, list(ms), list(rs), seeds, proj=f"sparse-jl:{s}:gather", ws=ws)
+    cp.compact_fwd_group(xd, Wd, y2, z2, list(ms), list(rs), seeds, proj=f"sparse-jl:{s}", ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+    ro = 0
+    for j, r in enumerate(rs):
+        z_ref, absprod = _gather_ref(x, seeds[j], r, s)
+        assert_elementwise(to_np(z)[:, ro:ro + r], z_ref, absprod, K=n, operand_rel=BF16_U, what=f"gather z_{j}")
+        ro += r
