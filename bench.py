@@ -61,6 +61,10 @@ def parse_args():
                     help="instead of the benchmark: whole-model training steps of a LLaMA-350M-shaped model "
                          "(baseline, CompAct r=n/4, r=n/8) over batch sizes; one JSON line per point with the "
                          "peak allocated memory and the step time")
+    ap.add_argument("--compare-blas", action="store_true",
+                    help="instead of the benchmark: the dL/dx GEMM of compact_bwd (with its staging launch) "
+                         "against torch.matmul (hipBLASLt) at 65536 tokens, n = 1024 and several K; one JSON "
+                         "line per K")
     ap.add_argument("--sweep-batches", default="32,64,128,256,512",
                     help="batch sizes (sequences of 256 tokens) for --model-sweep")
     return ap.parse_args()
@@ -422,6 +426,46 @@ def model_sweep(args):
             print(json.dumps(rec), flush=True)
 
 
+def compare_blas():
+    """dL/dx = dL/do W^T through compact_bwd (the K-tiled staging of W and the
+    persistent GEMM) against torch.matmul on the same bf16 operands: T = 65536
+    tokens, n = 1024 outputs, K = m from 1024 to 8192 (the dx shapes of the
+    LLaMA workloads and beyond).  Event-timed, 10 calls after one warm-up."""
+    import torch
+    import paper_2410_15352_amd as cp
+    cp.library()
+    dev = torch.device("cuda:0")
+    T, n = 65536, 1024
+
+    def timed(fn, reps=10):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    for K in (1024, 2048, 2736, 3072, 4096, 5472, 8192):
+        g = torch.Generator(device=dev)
+        g.manual_seed(K)
+        dy = torch.empty(T, K, device=dev).normal_(0.0, 0.01, generator=g).to(torch.bfloat16)
+        W = torch.empty(n, K, device=dev).normal_(0.0, 0.02, generator=g).to(torch.bfloat16)
+        Wt = W.t().contiguous()
+        dx = torch.empty(T, n, dtype=torch.bfloat16, device=dev)
+        ws = torch.zeros(cp.bwd_workspace_bytes(T, n, K, 128), dtype=torch.uint8, device=dev)
+        ours = timed(lambda: cp.compact_bwd(dy, W, None, dx, None, ws=ws))
+        lib = timed(lambda: torch.matmul(dy, Wt))
+        fl = 2.0 * T * n * K
+        print(json.dumps({"K": K, "tokens": T, "n": n, "compact_bwd_dx_us": round(ours * 1e3, 1),
+                          "compact_bwd_dx_tflops": round(fl / ours / 1e9, 1),
+                          "torch_matmul_us": round(lib * 1e3, 1), "torch_matmul_tflops": round(fl / lib / 1e9, 1)}),
+              flush=True)
+        del dy, W, Wt, dx, ws
+
+
 def main():
     args = parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -431,6 +475,8 @@ def main():
         sys.exit(2)
     if args.model_sweep:
         return model_sweep(args)
+    if args.compare_blas:
+        return compare_blas()
     import torch
     import paper_2410_15352_amd as cp
     from synthetic import workload
