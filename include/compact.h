@@ -254,10 +254,12 @@ size_t compact_bwd_group_workspace_bytes(int64_t tokens, int64_t n, int32_t coun
  * without ordering between them) race and must be serialised by the caller.
  * Errors: as compact_bwd, and COMPACT_EUNSUPPORTED when G is requested and
  * compact_bwd_workspace_bytes(tokens, n, m, r, dtype) exceeds the scratch
- * (then nothing is launched).  This covers every layer of the LLaMA-60M,
- * RoBERTa-Base, LLaMA-350M and LLaMA-1B shapes.
+ * (then nothing is launched).  The size, 64 MiB and the 256-byte alignment
+ * allowance every workspace size includes, covers every layer of the
+ * LLaMA-60M, RoBERTa-Base, LLaMA-350M and LLaMA-1B shapes at any token count
+ * (the most, 64 MiB of G^ partial sums, at n = m = 2048, r = 512 or 256).
  */
-#define COMPACT_NOALLOC_SCRATCH_BYTES (48u << 20)
+#define COMPACT_NOALLOC_SCRATCH_BYTES ((64u << 20) + 256u)
 
 int compact_bwd_noalloc(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z, int64_t ldz,
                         void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n, int64_t m, int64_t r,

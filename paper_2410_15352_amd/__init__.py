@@ -172,7 +172,7 @@ def compact_bwd(dy, W, z, dx, G, ws=None, stream=None):
     _check("compact_bwd", st)
 
 
-NOALLOC_SCRATCH_BYTES = 48 << 20
+NOALLOC_SCRATCH_BYTES = (64 << 20) + 256
 
 
 def compact_bwd_noalloc(dy, W, z, dx, G, stream=None):

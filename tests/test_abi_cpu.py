@@ -84,6 +84,29 @@ def test_workspace_sizes(lib):
     assert lib.compact_step_workspace_bytes(256, 512, 32, 0) >= 32 * 512 * 4
 
 
+
+def _header_define(name):
+    m = re.search(r"#define\s+" + name + r"\s+(.+)", open(HEADER).read())
+    return eval(re.sub(r"(\d+)u\b", r"\1", m.group(1)), {})
+
+
+@pytest.mark.parametrize("tokens", [1, 1000, 4096, 8192, 32768, 65536, 1 << 20])
+def test_noalloc_scratch_covers_every_workload_layer(lib, tokens):
+    # compact_bwd_noalloc's scratch holds the backward of every layer of the
+    # bf16 workloads (LLaMA-60M/350M/1B, RoBERTa-Base) at any token count
+    import paper_2410_15352_amd as cp
+    from synthetic import WORKLOAD_NAMES, workload
+    size = _header_define("COMPACT_NOALLOC_SCRATCH_BYTES")
+    assert size == cp.NOALLOC_SCRATCH_BYTES and size % 256 == 0
+    most = 0
+    for name in WORKLOAD_NAMES:
+        wl = workload(name)
+        if wl.dtype != "bf16":
+            continue
+        for L in wl.layers:
+            most = max(most, lib.compact_bwd_workspace_bytes(tokens, L.n, L.m, L.r, 1))
+    assert 0 < most <= size
+
 FAKE = 0x100000  # an aligned non-NULL address; never dereferenced (validation fails first)
 
 

@@ -50,6 +50,30 @@ def test_noalloc_matches_workspace_path_twice():
     assert oc.rel_fro(G1.cpu().numpy(), G_ref) <= 2e-2
 
 
+def test_noalloc_largest_workload_layer():
+    # a LLaMA-1B q/k/v/o projection at r = n/4: the largest need of the bf16
+    # workloads, every byte of the scratch (G^ partial sums up to its end)
+    lib = cp.library()
+    T, n, m, r = 1000, 2048, 2048, 512
+    assert cp.bwd_workspace_bytes(T, n, m, r) == cp.NOALLOC_SCRATCH_BYTES
+    dy, z, W = bwd_inputs(T, n, m, r, "bf16", data_seed=17)
+    dyd, zd, Wd = to_dev(dy, "bf16", m), to_dev(z, "bf16", r), to_dev(W, "bf16", m)
+    outs = []
+    for fn in ("compact_bwd", "compact_bwd_noalloc"):
+        dx = empty(T, n, "bf16", n, fill=float("nan"))
+        G = torch.full((r, m), float("nan"), dtype=torch.float32, device=dev())
+        ws = workspace(cp.NOALLOC_SCRATCH_BYTES) if fn == "compact_bwd" else None
+        _call(lib, fn, dyd, Wd, zd, dx, G, T, n, m, r, ws)
+        outs.append((dx, G))
+    torch.cuda.synchronize()
+    (dx0, G0), (dx1, G1) = outs
+    assert torch.equal(dx0.view(torch.int16), dx1.view(torch.int16))
+    assert torch.equal(G0.view(torch.int32), G1.view(torch.int32))
+    dx_ref, G_ref = oc.ref_bwd(dy, z, W)
+    assert oc.rel_fro(to_np(dx1), dx_ref) <= 2e-2
+    assert oc.rel_fro(G1.cpu().numpy(), G_ref) <= 2e-2
+
+
 def test_noalloc_rejects_oversized_requests():
     # G^ of r = 2048, m = 16384 needs more partial sums than the scratch holds:
     # a clear error and nothing launched (the pointers are never touched)
