@@ -39,6 +39,8 @@ GROUPS = [
     (300, 1024, (256, 512), (64, 96)),                 # mixed widths
     (300, 200, (136, 72), (40, 24)),                   # K < 320: per projection
     (129, 512, (512, 203), (64, 30)),                  # odd last width: per projection
+    # eight projections, the most one group takes (persistent GEMM, one G^ layer table)
+    (1000, 512, (64, 128, 64, 256, 72, 80, 128, 64), (8, 16, 8, 32, 8, 16, 16, 8)),
 ]
 
 
@@ -174,6 +176,7 @@ def _bwd_group_inputs(T, n, ms, rs, data_seed, dt="bf16"):
 BWD_GROUPS = GROUPS + [
     (65, 512, (512, 512, 512), (128, 128, 128)),       # fewer tokens than splits x 32
     (2048, 2736, (1024,), (342,)),                     # one projection (down), r past one row tile
+    (777, 1024, (256,) * 8, (256,) * 8),               # eight projections on the 256 x 256 G^ tiles
 ]
 
 
