@@ -134,6 +134,12 @@ typedef enum {
  *         identical y and z.  The workspace is scratch: it is dead when the
  *         call's kernels have finished.
  * Requirements: tokens >= 0, n >= 1, m >= 1, 1 <= r <= n.
+ * Errors: COMPACT_EINVAL (shapes, a NULL tensor, ld smaller than the row,
+ * an unknown dtype or projection code, the identity with r != n),
+ * COMPACT_EALIGN, COMPACT_EWORKSPACE (a workspace smaller than the size
+ * above), COMPACT_EUNSUPPORTED (n or r of 2^31 or more; the gather flag with
+ * more than COMPACT_GATHER_MAX_S draws or r >= 65535), COMPACT_EHIP; nothing
+ * is launched on a validation error, and tokens = 0 launches nothing.
  */
 int compact_fwd(const void* x, int64_t ldx, const void* W, int64_t ldw, void* y, int64_t ldy,
                 void* z, int64_t ldz, int64_t tokens, int64_t n, int64_t m, int64_t r,
@@ -194,6 +200,13 @@ size_t compact_fwd_group_workspace_bytes(int64_t n, int32_t count, const int64_t
  *         order, so G^ is deterministic) and, before them, a K-tiled copy of W
  *         that the dx GEMM reads (with NULL or a smaller workspace dx reads W
  *         itself; dx is bitwise the same either way).
+ * Requirements as compact_fwd.  tokens = 0: dx has no rows and G^ = 0 is
+ * written.
+ * Errors: COMPACT_EINVAL (shapes, dx and G both NULL, a NULL operand of a
+ * requested output, ld smaller than the row, an unknown dtype),
+ * COMPACT_EALIGN, COMPACT_EWORKSPACE (G requested on the bf16 path without a
+ * workspace of the size above), COMPACT_EUNSUPPORTED (n or r of 2^31 or
+ * more), COMPACT_EHIP; nothing is launched on a validation error.
  */
 int compact_bwd(const void* dy, int64_t lddy, const void* W, int64_t ldw, const void* z,
                 int64_t ldz, void* dx, int64_t lddx, float* G, int64_t tokens, int64_t n,
@@ -288,6 +301,12 @@ int compact_bwd_noalloc(const void* dy, int64_t lddy, const void* W, int64_t ldw
  *         dtype) bytes (holds N between the two kernels)
  * The seed schedule of Alg. 3 (t <- t+1, new seed every T steps) is host logic:
  * compact_next_seed.
+ * Errors: COMPACT_EINVAL (shapes, NULL tensors, t < 1, a beta outside [0, 1),
+ * eps not positive and finite, lr negative or not finite, alpha not finite,
+ * an unknown dtype or projection code), COMPACT_EALIGN, COMPACT_EWORKSPACE,
+ * COMPACT_EUNSUPPORTED (fp32 compute into bf16 W; a bf16 shape whose tiles
+ * need offsets of 2^31 bytes or more), COMPACT_EHIP; nothing is launched on a
+ * validation error.
  */
 int compact_step(void* W, int64_t ldw, const float* G, float* M, float* V, int64_t n,
                  int64_t m, int64_t r, uint64_t seed, int64_t t, double lr, double beta1,
