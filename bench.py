@@ -518,6 +518,23 @@ def main():
     gemm_frac = (flops["fwd"] + flops["dx"] + flops["ghat"]) / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
     upd_gbs = (bytes_["adam"] + bytes_["dec"]) / (phases["step"] * 1e-3) / 1e9
 
+    def phase(bound, work, ms):
+        rate = work / (ms * 1e-3)
+        if bound == "mfma":
+            return {"bound": bound, "achieved": round(rate / 1e12, 1), "unit": "TFLOP/s",
+                    "frac": round(rate / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        return {"bound": bound, "achieved": round(rate / 1e9, 1), "unit": "GB/s",
+                "frac": round(rate / 1e9 / PEAK_HBM_GBS, 4)}
+
+    # each phase against its own bound: the GEMMs against the bf16 MFMA peak,
+    # G^ (HBM-bound at r = n/8) and Alg. 3 against the HBM peak
+    phase_roofline = {
+        "fwd": phase("mfma", flops["fwd"], phases["fwd"]),
+        "bwd_dx": phase("mfma", flops["dx"], phases["bwd_dx"]),
+        "bwd_ghat": phase("hbm", bytes_["ghat"], phases["bwd_ghat"]),
+        "step": phase("hbm", bytes_["adam"] + bytes_["dec"], phases["step"]),
+    }
+
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         rec = json.load(open(TRAFFIC_FILE))
@@ -565,6 +582,7 @@ def main():
         "gemm_phases_mfma_frac": round(gemm_frac, 4),
         "update_phase_hbm_GBs": round(upd_gbs, 1),
         "update_phase_hbm_frac": round(upd_gbs / PEAK_HBM_GBS, 4),
+        "phase_roofline": phase_roofline,
         "activation_bytes_per_layer": act,
     }
     print(json.dumps(line), flush=True)
