@@ -76,3 +76,19 @@ def test_algorithmic_work_per_step():
     assert b["ghat"] == pytest.approx(BLOCKS * gb, rel=1e-12)
     assert b["adam"] == pytest.approx(BLOCKS * ab, rel=1e-12)
     assert b["dec"] == pytest.approx(BLOCKS * deb, rel=1e-12)
+
+
+def test_more_than_one_gpu_is_refused():
+    # the benchmark runs on exactly one GPU: --gpus N > 1 (or a multi-rank
+    # launch) prints a JSON error line and exits with status 2 before any GPU work
+    import json
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for args, env in ((["--gpus", "2"], {}), ([], {"WORLD_SIZE": "4"})):
+        p = subprocess.run([sys.executable, os.path.join(root, "bench.py"), *args], capture_output=True, text=True,
+                           env={**os.environ, **env}, timeout=120)
+        assert p.returncode == 2, p.stderr[-500:]
+        line = json.loads(p.stdout.strip().splitlines()[-1])
+        assert "one GPU" in line["error"]
